@@ -1,0 +1,159 @@
+"""CPU oracle for the per-frame clustering and density path.
+
+TEST INFRASTRUCTURE ONLY: imported by the test suite, the smoke check and the
+benchmark's CPU-baseline leg, never by the GPU library or its binding.
+
+The arithmetic lives in ``oracle.c`` (plain C, fp64 for the density, int64 for
+distances); this module only compiles it with gcc and marshals numpy arrays.
+The definitions it follows are stated at the top of ``oracle.c``:
+standard DBSCAN (Ester et al., 1996) as the point-level reading of the
+paper's connected-component clustering (Section 2.3), and the direct-sum
+Gaussian density grid of Algorithm 1 (Section 3.6).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+# A test-only hook: load a differently built oracle (the mutation tests build
+# copies of oracle.c with one planted mistake each and point this at them).
+_LIB_OVERRIDE = os.environ.get("ORACLE_LIB_OVERRIDE")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c into liboracle.so (gcc -O2, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread",
+                               "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if _LIB_OVERRIDE:
+            lib = ctypes.CDLL(_LIB_OVERRIDE)
+        else:
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build(force=True)
+            lib = ctypes.CDLL(_LIB)
+        p = ctypes.c_void_p
+        i32 = ctypes.c_int32
+        lib.oracle_dbscan_frame.argtypes = [p, i32, i32, i32, p, p]
+        lib.oracle_dbscan_frame.restype = i32
+        lib.oracle_neighbour_counts.argtypes = [p, i32, i32, p]
+        lib.oracle_neighbour_counts.restype = i32
+        lib.oracle_density_cell.argtypes = [p, i32, i32, i32, i32, i32, ctypes.c_double, i32, i32]
+        lib.oracle_density_cell.restype = ctypes.c_double
+        lib.oracle_cluster_frames.argtypes = [p, p, i32, i32, i32, p, p, p, i32]
+        lib.oracle_cluster_frames.restype = i32
+        lib.oracle_density_frames.argtypes = [p, p, i32, i32, i32, i32, i32, ctypes.c_double, p, i32]
+        lib.oracle_density_frames.restype = i32
+        lib.oracle_density_cells.argtypes = [p, p, i32, i32, i32, i32, i32, ctypes.c_double,
+                                             p, p, p, ctypes.c_int64, p, i32]
+        lib.oracle_density_cells.restype = i32
+        _lib = lib
+    return _lib
+
+
+def default_threads() -> int:
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _xy(xy) -> np.ndarray:
+    a = np.ascontiguousarray(np.asarray(xy, dtype=np.int32).reshape(-1, 2))
+    return a
+
+
+def _check(rc: int, what: str):
+    if rc < 0:
+        raise ValueError(f"oracle {what}: error {rc}")
+
+
+def neighbour_counts(xy, eps_q: int) -> np.ndarray:
+    """Per-point count of points within eps (self included), one frame."""
+    a = _xy(xy)
+    out = np.zeros(a.shape[0], np.int32)
+    _check(_load().oracle_neighbour_counts(_ptr(a), a.shape[0], int(eps_q), _ptr(out)), "counts")
+    return out
+
+
+def dbscan_frame(xy, eps_q: int, min_pts: int):
+    """One frame: returns (labels int32[n], kind uint8[n], n_clusters)."""
+    a = _xy(xy)
+    n = a.shape[0]
+    labels = np.zeros(n, np.int32)
+    kind = np.zeros(n, np.uint8)
+    r = _load().oracle_dbscan_frame(_ptr(a), n, int(eps_q), int(min_pts), _ptr(labels), _ptr(kind))
+    _check(r, "dbscan_frame")
+    return labels, kind, int(r)
+
+
+def cluster_frames(xy, offsets, eps_q: int, min_pts: int, n_threads: int | None = None):
+    """Batch: returns (labels int32[T], kind uint8[T], n_clusters int32[F])."""
+    a = _xy(xy)
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32))
+    F = off.shape[0] - 1
+    T = a.shape[0]
+    if F < 0 or (F >= 0 and int(off[-1]) != T):
+        raise ValueError("offsets do not describe xy")
+    labels = np.zeros(T, np.int32)
+    kind = np.zeros(T, np.uint8)
+    ncl = np.zeros(max(F, 0), np.int32)
+    r = _load().oracle_cluster_frames(_ptr(a), _ptr(off), F, int(eps_q), int(min_pts),
+                                      _ptr(labels), _ptr(kind), _ptr(ncl),
+                                      n_threads or default_threads())
+    _check(r, "cluster_frames")
+    return labels, kind, ncl
+
+
+def density_frames(xy, offsets, width_px: int, height_px: int, grid_w: int, grid_h: int,
+                   sigma_px: float, n_threads: int | None = None) -> np.ndarray:
+    """Batch: returns float64[F, grid_h, grid_w] in birds per px^2."""
+    a = _xy(xy)
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32))
+    F = off.shape[0] - 1
+    if int(off[-1]) != a.shape[0]:
+        raise ValueError("offsets do not describe xy")
+    out = np.zeros((F, grid_h, grid_w), np.float64)
+    r = _load().oracle_density_frames(_ptr(a), _ptr(off), F, int(width_px), int(height_px),
+                                      int(grid_w), int(grid_h), float(sigma_px), _ptr(out),
+                                      n_threads or default_threads())
+    _check(r, "density_frames")
+    return out
+
+
+def density_cells(xy, offsets, width_px: int, height_px: int, grid_w: int, grid_h: int,
+                  sigma_px: float, frame, gx, gy, n_threads: int | None = None) -> np.ndarray:
+    """Density at sampled cells (frame[k], gy[k], gx[k]); float64[m]."""
+    a = _xy(xy)
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32))
+    F = off.shape[0] - 1
+    fr = np.ascontiguousarray(np.asarray(frame, dtype=np.int32))
+    cx = np.ascontiguousarray(np.asarray(gx, dtype=np.int32))
+    cy = np.ascontiguousarray(np.asarray(gy, dtype=np.int32))
+    m = fr.shape[0]
+    out = np.zeros(m, np.float64)
+    r = _load().oracle_density_cells(_ptr(a), _ptr(off), F, int(width_px), int(height_px),
+                                     int(grid_w), int(grid_h), float(sigma_px), _ptr(fr),
+                                     _ptr(cx), _ptr(cy), m, _ptr(out),
+                                     n_threads or default_threads())
+    _check(r, "density_cells")
+    return out

@@ -1,0 +1,344 @@
+/*
+ * oracle.c - plain, slow, obviously correct CPU oracle for the per-frame
+ * clustering and density-grid path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg load this library.  The GPU library shares no
+ * code, header, table or constant with it.
+ *
+ * What it computes (the paper's clustering module, Section 2.3, and its
+ * per-frame density computation, Section 3.6 / Algorithm 1):
+ *
+ *  1. Radius-neighbour clustering of the birds of each frame.  The paper's
+ *     clustering module finds groups of nearby birds by connected-component
+ *     analysis (Section 2.3); the point-level reading used here is standard
+ *     DBSCAN (Ester, Kriegel, Sander and Xu, KDD 1996):
+ *       - two birds are neighbours when their Euclidean distance is <= eps
+ *         (closed ball; a bird is its own neighbour, duplicates count);
+ *       - a bird is a core point when it has >= min_pts neighbours;
+ *       - clusters are the connected components of the core points under the
+ *         neighbour relation, found by breadth-first expansion from each
+ *         unvisited core point in ascending index order, so a cluster's label
+ *         is the smallest frame-local index among its core points;
+ *       - a non-core bird with at least one core neighbour is a border point
+ *         and joins the cluster of its nearest core neighbour, ties broken by
+ *         the smaller (y, x) of that core; any other bird is noise (-1).
+ *     Coordinates are integers in 1/16 px and eps_q = 16 * eps, so the
+ *     neighbour test is the exact integer comparison dx^2 + dy^2 <= eps_q^2
+ *     (done in int64).
+ *
+ *  2. The Gaussian density grid of each frame (Algorithm 1, DefaultClustering:
+ *     for every grid cell, for every bird, accumulate a distance-based
+ *     contribution).  The grid has grid_w x grid_h cells tiling the frame
+ *     [0, W) x [0, H) px, evaluated at cell centres
+ *         cx = (gx + 1/2) W / grid_w,   cy = (gy + 1/2) H / grid_h,
+ *     and each bird at (x, y) = (x_q / 16, y_q / 16) px contributes the
+ *     isotropic 2-D Gaussian with bandwidth sigma px, normalised to unit mass:
+ *         density[gy][gx] = sum_i exp(-((cx - x)^2 + (cy - y)^2) / (2 sigma^2))
+ *                           / (2 pi sigma^2)            [birds per px^2]
+ *     This is the direct double sum in fp64 with libm exp, one grid cell at a
+ *     time; it makes no use of the sum's separability.
+ *
+ * Threads only split independent work items (whole frames for clustering,
+ * whole grid rows for density); each item is computed exactly as above.
+ */
+
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_OK 0
+#define ORACLE_EINVAL (-1)
+#define ORACLE_ENOMEM (-2)
+
+/* ------------------------------------------------------------------------ */
+/* Clustering of one frame                                                  */
+/* ------------------------------------------------------------------------ */
+
+static int64_t sq_dist(const int32_t *xy, int32_t i, int32_t j)
+{
+    int64_t dx = (int64_t)xy[2 * i] - (int64_t)xy[2 * j];
+    int64_t dy = (int64_t)xy[2 * i + 1] - (int64_t)xy[2 * j + 1];
+    return dx * dx + dy * dy;
+}
+
+/* Returns the number of clusters (>= 0), or a negative error code.
+ * labels[i]: frame-local label (smallest core index of the cluster) or -1.
+ * kind[i]:   0 noise, 1 border, 2 core. */
+int32_t oracle_dbscan_frame(const int32_t *xy, int32_t n, int32_t eps_q, int32_t min_pts,
+                            int32_t *labels, uint8_t *kind)
+{
+    if (n < 0 || eps_q < 0 || min_pts < 1) return ORACLE_EINVAL;
+    if (n == 0) return 0;
+    const int64_t e2 = (int64_t)eps_q * (int64_t)eps_q;
+
+    int64_t *count = (int64_t *)calloc((size_t)n, sizeof(int64_t));
+    uint8_t *core = (uint8_t *)calloc((size_t)n, 1);
+    int32_t *comp = (int32_t *)malloc((size_t)n * sizeof(int32_t));
+    int32_t *queue = (int32_t *)malloc((size_t)n * sizeof(int32_t));
+    if (!count || !core || !comp || !queue) {
+        free(count); free(core); free(comp); free(queue);
+        return ORACLE_ENOMEM;
+    }
+
+    /* Neighbour counts (self and duplicates included) and core flags. */
+    for (int32_t i = 0; i < n; ++i) {
+        int64_t c = 0;
+        for (int32_t j = 0; j < n; ++j)
+            if (sq_dist(xy, i, j) <= e2) ++c;
+        count[i] = c;
+        core[i] = (uint8_t)(c >= (int64_t)min_pts);
+    }
+
+    /* Clusters: breadth-first expansion over core points, seeds ascending. */
+    for (int32_t i = 0; i < n; ++i) comp[i] = -1;
+    int32_t n_clusters = 0;
+    for (int32_t s = 0; s < n; ++s) {
+        if (!core[s] || comp[s] >= 0) continue;
+        ++n_clusters;
+        int32_t head = 0, tail = 0;
+        comp[s] = s;
+        queue[tail++] = s;
+        while (head < tail) {
+            int32_t p = queue[head++];
+            for (int32_t j = 0; j < n; ++j) {
+                if (core[j] && comp[j] < 0 && sq_dist(xy, p, j) <= e2) {
+                    comp[j] = s;
+                    queue[tail++] = j;
+                }
+            }
+        }
+    }
+
+    /* Cores keep their component; non-cores take the nearest core neighbour's
+     * component (key: squared distance, then y, then x of the core). */
+    for (int32_t i = 0; i < n; ++i) {
+        if (core[i]) {
+            labels[i] = comp[i];
+            kind[i] = 2;
+            continue;
+        }
+        int32_t best = -1;
+        int64_t best_d2 = 0;
+        for (int32_t j = 0; j < n; ++j) {
+            if (!core[j]) continue;
+            int64_t d2 = sq_dist(xy, i, j);
+            if (d2 > e2) continue;
+            int better = 0;
+            if (best < 0) better = 1;
+            else if (d2 != best_d2) better = d2 < best_d2;
+            else if (xy[2 * j + 1] != xy[2 * best + 1]) better = xy[2 * j + 1] < xy[2 * best + 1];
+            else better = xy[2 * j] < xy[2 * best];
+            if (better) { best = j; best_d2 = d2; }
+        }
+        if (best >= 0) {
+            labels[i] = comp[best];
+            kind[i] = 1;
+        } else {
+            labels[i] = -1;
+            kind[i] = 0;
+        }
+    }
+
+    free(count); free(core); free(comp); free(queue);
+    return n_clusters;
+}
+
+/* Neighbour counts alone (self included), for tests of the count step. */
+int32_t oracle_neighbour_counts(const int32_t *xy, int32_t n, int32_t eps_q, int32_t *count)
+{
+    if (n < 0 || eps_q < 0) return ORACLE_EINVAL;
+    const int64_t e2 = (int64_t)eps_q * (int64_t)eps_q;
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t c = 0;
+        for (int32_t j = 0; j < n; ++j)
+            if (sq_dist(xy, i, j) <= e2) ++c;
+        count[i] = c;
+    }
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Density of one grid cell / one frame                                     */
+/* ------------------------------------------------------------------------ */
+
+static const double kPi = 3.14159265358979323846;
+
+double oracle_density_cell(const int32_t *xy, int32_t n, int32_t width_px, int32_t height_px,
+                           int32_t grid_w, int32_t grid_h, double sigma_px, int32_t gx, int32_t gy)
+{
+    const double cx = ((double)gx + 0.5) * (double)width_px / (double)grid_w;
+    const double cy = ((double)gy + 0.5) * (double)height_px / (double)grid_h;
+    const double two_s2 = 2.0 * sigma_px * sigma_px;
+    double acc = 0.0;
+    for (int32_t i = 0; i < n; ++i) {
+        const double x = (double)xy[2 * i] / 16.0;
+        const double y = (double)xy[2 * i + 1] / 16.0;
+        const double dx = cx - x, dy = cy - y;
+        acc += exp(-(dx * dx + dy * dy) / two_s2);
+    }
+    return acc / (kPi * two_s2);
+}
+
+static int density_args_ok(int32_t width_px, int32_t height_px, int32_t grid_w, int32_t grid_h,
+                           double sigma_px)
+{
+    return width_px >= 1 && height_px >= 1 && grid_w >= 1 && grid_h >= 1 &&
+           isfinite(sigma_px) && sigma_px > 0.0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Batches: a thread pool over independent work items                       */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    /* batch */
+    const int32_t *xy;
+    const int32_t *offsets;
+    int32_t n_frames;
+    /* clustering */
+    int32_t eps_q, min_pts;
+    int32_t *labels;
+    uint8_t *kind;
+    int32_t *n_clusters;
+    /* density */
+    int32_t width_px, height_px, grid_w, grid_h;
+    double sigma_px;
+    double *density;
+    const int32_t *cell_frame, *cell_gx, *cell_gy;
+    /* work distribution */
+    int64_t n_items;
+    int64_t next;          /* shared counter */
+    int32_t status;        /* first error seen */
+    int mode;              /* 0 cluster, 1 density grid, 2 density cells */
+} job_t;
+
+static void run_item(job_t *job, int64_t item)
+{
+    if (job->mode == 0) {
+        int32_t f = (int32_t)item;
+        int32_t b = job->offsets[f], e = job->offsets[f + 1];
+        int32_t r = oracle_dbscan_frame(job->xy + 2 * (int64_t)b, e - b, job->eps_q, job->min_pts,
+                                        job->labels + b, job->kind + b);
+        if (r < 0) __atomic_store_n(&job->status, r, __ATOMIC_RELAXED);
+        else if (job->n_clusters) job->n_clusters[f] = r;
+    } else if (job->mode == 1) {
+        int32_t f = (int32_t)(item / job->grid_h);
+        int32_t gy = (int32_t)(item % job->grid_h);
+        int32_t b = job->offsets[f], e = job->offsets[f + 1];
+        double *row = job->density + ((int64_t)f * job->grid_h + gy) * job->grid_w;
+        for (int32_t gx = 0; gx < job->grid_w; ++gx)
+            row[gx] = oracle_density_cell(job->xy + 2 * (int64_t)b, e - b, job->width_px,
+                                          job->height_px, job->grid_w, job->grid_h, job->sigma_px,
+                                          gx, gy);
+    } else {
+        int32_t f = job->cell_frame[item];
+        int32_t b = job->offsets[f], e = job->offsets[f + 1];
+        job->density[item] = oracle_density_cell(job->xy + 2 * (int64_t)b, e - b, job->width_px,
+                                                  job->height_px, job->grid_w, job->grid_h,
+                                                  job->sigma_px, job->cell_gx[item],
+                                                  job->cell_gy[item]);
+    }
+}
+
+static void *worker(void *arg)
+{
+    job_t *job = (job_t *)arg;
+    for (;;) {
+        int64_t item = __atomic_fetch_add(&job->next, 1, __ATOMIC_RELAXED);
+        if (item >= job->n_items) break;
+        run_item(job, item);
+    }
+    return NULL;
+}
+
+static int32_t run_job(job_t *job, int32_t n_threads)
+{
+    if (n_threads < 1) n_threads = 1;
+    if ((int64_t)n_threads > job->n_items) n_threads = (int32_t)(job->n_items > 0 ? job->n_items : 1);
+    job->next = 0;
+    job->status = ORACLE_OK;
+    if (n_threads == 1) {
+        worker(job);
+        return job->status;
+    }
+    pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * (size_t)n_threads);
+    if (!th) return ORACLE_ENOMEM;
+    int32_t started = 0;
+    for (; started < n_threads; ++started)
+        if (pthread_create(&th[started], NULL, worker, job) != 0) break;
+    if (started == 0) worker(job);
+    for (int32_t t = 0; t < started; ++t) pthread_join(th[t], NULL);
+    free(th);
+    return job->status;
+}
+
+static int offsets_ok(const int32_t *offsets, int32_t n_frames)
+{
+    if (n_frames < 0 || (n_frames > 0 && !offsets)) return 0;
+    if (n_frames > 0 && offsets[0] != 0) return 0;
+    for (int32_t f = 0; f < n_frames; ++f)
+        if (offsets[f + 1] < offsets[f]) return 0;
+    return 1;
+}
+
+int32_t oracle_cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
+                              int32_t eps_q, int32_t min_pts, int32_t *labels, uint8_t *kind,
+                              int32_t *n_clusters, int32_t n_threads)
+{
+    if (!offsets_ok(offsets, n_frames) || eps_q < 0 || min_pts < 1) return ORACLE_EINVAL;
+    job_t job;
+    memset(&job, 0, sizeof job);
+    job.xy = xy; job.offsets = offsets; job.n_frames = n_frames;
+    job.eps_q = eps_q; job.min_pts = min_pts;
+    job.labels = labels; job.kind = kind; job.n_clusters = n_clusters;
+    job.n_items = n_frames;
+    job.mode = 0;
+    return run_job(&job, n_threads);
+}
+
+/* density: [n_frames][grid_h][grid_w] fp64 */
+int32_t oracle_density_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
+                              int32_t width_px, int32_t height_px, int32_t grid_w, int32_t grid_h,
+                              double sigma_px, double *density, int32_t n_threads)
+{
+    if (!offsets_ok(offsets, n_frames) ||
+        !density_args_ok(width_px, height_px, grid_w, grid_h, sigma_px))
+        return ORACLE_EINVAL;
+    job_t job;
+    memset(&job, 0, sizeof job);
+    job.xy = xy; job.offsets = offsets; job.n_frames = n_frames;
+    job.width_px = width_px; job.height_px = height_px;
+    job.grid_w = grid_w; job.grid_h = grid_h; job.sigma_px = sigma_px;
+    job.density = density;
+    job.n_items = (int64_t)n_frames * grid_h;
+    job.mode = 1;
+    return run_job(&job, n_threads);
+}
+
+/* Density at m sampled cells: cell k is (frame[k], gx[k], gy[k]); out[k] fp64. */
+int32_t oracle_density_cells(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
+                             int32_t width_px, int32_t height_px, int32_t grid_w, int32_t grid_h,
+                             double sigma_px, const int32_t *cell_frame, const int32_t *cell_gx,
+                             const int32_t *cell_gy, int64_t m, double *out, int32_t n_threads)
+{
+    if (!offsets_ok(offsets, n_frames) ||
+        !density_args_ok(width_px, height_px, grid_w, grid_h, sigma_px) || m < 0)
+        return ORACLE_EINVAL;
+    for (int64_t k = 0; k < m; ++k)
+        if (cell_frame[k] < 0 || cell_frame[k] >= n_frames || cell_gx[k] < 0 ||
+            cell_gx[k] >= grid_w || cell_gy[k] < 0 || cell_gy[k] >= grid_h)
+            return ORACLE_EINVAL;
+    job_t job;
+    memset(&job, 0, sizeof job);
+    job.xy = xy; job.offsets = offsets; job.n_frames = n_frames;
+    job.width_px = width_px; job.height_px = height_px;
+    job.grid_w = grid_w; job.grid_h = grid_h; job.sigma_px = sigma_px;
+    job.density = out;
+    job.cell_frame = cell_frame; job.cell_gx = cell_gx; job.cell_gy = cell_gy;
+    job.n_items = m;
+    job.mode = 2;
+    return run_job(&job, n_threads);
+}

@@ -1,0 +1,71 @@
+"""The oracle's pins catch plausible mistakes (no GPU).
+
+Each case below plants one mistake in a copy of oracle/oracle.c (a dropped
+term, a wrong comparison, a swapped axis, a wrong constant), builds it with
+gcc in a temporary directory, and runs the oracle pin tests against that
+build in a child process.  The pins must fail for every mutant.
+"""
+
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "oracle.c")
+DBSCAN_PINS = "tests/test_oracle_dbscan.py"
+KDE_PINS = "tests/test_oracle_kde.py"
+
+MUTANTS = [
+    # (name, old text, new text, which pin file must fail)
+    ("strict_ball", "if (sq_dist(xy, i, j) <= e2) ++c;\n        count[i] = c;\n        core[i]",
+     "if (sq_dist(xy, i, j) < e2) ++c;\n        count[i] = c;\n        core[i]", DBSCAN_PINS),
+    ("self_not_counted", "if (sq_dist(xy, i, j) <= e2) ++c;\n        count[i] = c;\n        core[i]",
+     "if (j != i && sq_dist(xy, i, j) <= e2) ++c;\n        count[i] = c;\n        core[i]",
+     DBSCAN_PINS),
+    ("core_strict", "c >= (int64_t)min_pts", "c > (int64_t)min_pts", DBSCAN_PINS),
+    ("expand_through_border", "if (core[j] && comp[j] < 0 && sq_dist(xy, p, j) <= e2)",
+     "if (comp[j] < 0 && sq_dist(xy, p, j) <= e2)", DBSCAN_PINS),
+    ("seeds_descending", "for (int32_t s = 0; s < n; ++s) {",
+     "for (int32_t s = n - 1; s >= 0; --s) {", DBSCAN_PINS),
+    ("border_first_core", "else if (d2 != best_d2) better = d2 < best_d2;", "", DBSCAN_PINS),
+    ("border_x_before_y",
+     "else if (xy[2 * j + 1] != xy[2 * best + 1]) better = xy[2 * j + 1] < xy[2 * best + 1];\n"
+     "            else better = xy[2 * j] < xy[2 * best];",
+     "else if (xy[2 * j] != xy[2 * best]) better = xy[2 * j] < xy[2 * best];\n"
+     "            else better = xy[2 * j + 1] < xy[2 * best + 1];", DBSCAN_PINS),
+    ("border_larger_y", "better = xy[2 * j + 1] < xy[2 * best + 1];",
+     "better = xy[2 * j + 1] > xy[2 * best + 1];", DBSCAN_PINS),
+    ("dy_uses_x", "int64_t dy = (int64_t)xy[2 * i + 1] - (int64_t)xy[2 * j + 1];",
+     "int64_t dy = (int64_t)xy[2 * i] - (int64_t)xy[2 * j + 1];", DBSCAN_PINS),
+    ("kde_no_half_cell", "const double cx = ((double)gx + 0.5)", "const double cx = ((double)gx)",
+     KDE_PINS),
+    ("kde_norm_2pi_sigma", "return acc / (kPi * two_s2);", "return acc / (kPi * sigma_px * 2.0);",
+     KDE_PINS),
+    ("kde_sigma_sq_not_doubled", "const double two_s2 = 2.0 * sigma_px * sigma_px;",
+     "const double two_s2 = sigma_px * sigma_px;", KDE_PINS),
+    ("kde_quantum_8", "const double x = (double)xy[2 * i] / 16.0;",
+     "const double x = (double)xy[2 * i] / 8.0;", KDE_PINS),
+    ("kde_axes_swapped", "const double dx = cx - x, dy = cy - y;",
+     "const double dx = cx - y, dy = cy - x;", KDE_PINS),
+    ("kde_cy_uses_width", "const double cy = ((double)gy + 0.5) * (double)height_px",
+     "const double cy = ((double)gy + 0.5) * (double)width_px", KDE_PINS),
+    ("kde_row_layout", "double *row = job->density + ((int64_t)f * job->grid_h + gy) * job->grid_w;",
+     "double *row = job->density + ((int64_t)f * job->grid_w + gy) * job->grid_h;", KDE_PINS),
+]
+
+
+@pytest.mark.parametrize("name,old,new,pins", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, name, old, new, pins):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    mutant_c = tmp_path / "oracle_mutant.c"
+    mutant_c.write_text(src.replace(old, new))
+    lib = tmp_path / "liboracle_mutant.so"
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread", "-w",
+                           "-o", str(lib), str(mutant_c), "-lm"])
+    env = dict(os.environ, ORACLE_LIB_OVERRIDE=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", pins],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0, f"pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
