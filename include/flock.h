@@ -1,0 +1,146 @@
+/*
+ * flock.h - C ABI of the MI355X (gfx950) per-frame bird clustering and
+ * density library (libflock.so).
+ *
+ * The library computes, for a batch of video frames that each hold a ragged
+ * set of detected bird centroids, the two per-frame analytics of the paper's
+ * clustering module (Section 2.3; Section 3.6 and Algorithm 1):
+ *   - radius-neighbour clustering of the birds (core / border / noise kinds
+ *     and connected-component cluster labels), and
+ *   - a Gaussian kernel density grid.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  Batch layout (CSR over frames; the paper's "frames" of tracked positions,
+ *  Algorithm 1):
+ *    xy       device, int32[total][2]: (x, y) of each bird in 1/16 px,
+ *             0 <= x, y < 2^24.  Frame f is rows offsets[f] .. offsets[f+1]-1.
+ *    offsets  device, int32[n_frames + 1]: offsets[0] = 0, non-decreasing,
+ *             offsets[n_frames] = total.
+ *    n_frames, total: host copies of the batch sizes.
+ *  Every pointer argument is device memory owned by the caller; the library
+ *  neither frees nor keeps it after the call returns.
+ *  stream: a hipStream_t (NULL = the null stream).  Calls only enqueue work:
+ *  outputs are valid once the stream reaches the call's point.  No host-device
+ *  copy and no synchronisation happens, except when the environment variable
+ *  FLOCK_VALIDATE=1 asks for a synchronous device-side check of offsets.
+ *  Errors: a negative status; flock_last_error() then describes it.  On
+ *  FLOCK_EINVAL nothing is enqueued and the outputs are untouched.  A frame
+ *  whose offsets are inconsistent (negative count, past total) is never read;
+ *  its outputs are left untouched and its n_clusters entry is set to -1.
+ *  Thread safety: calls on different streams may run concurrently; the only
+ *  global state is a per-thread error string and a once-initialised cache of
+ *  device properties.
+ */
+#ifndef FLOCK_H
+#define FLOCK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t flock_status;
+
+#define FLOCK_OK 0
+#define FLOCK_EINVAL (-1)      /* bad argument: nothing enqueued, outputs untouched */
+#define FLOCK_ENOMEM (-2)      /* workspace too small, or allocation failed */
+#define FLOCK_EDEVICE (-3)     /* a HIP runtime call failed (message has its text) */
+#define FLOCK_EUNSUPPORTED (-4) /* device is not gfx950, or a size beyond the limits */
+
+/*
+ * cluster_frames - radius-neighbour (DBSCAN-style) clustering of every frame.
+ *
+ * The paper's clustering module groups nearby birds by connected-component
+ * analysis (Section 2.3) and names the per-frame distance loops as the
+ * bottleneck (Section 3.6).  The point-level definition computed here is
+ * standard DBSCAN (Ester et al., 1996) with these exact conventions:
+ *   neighbours   (x_i - x_j)^2 + (y_i - y_j)^2 <= eps_q^2, in exact integer
+ *                arithmetic on the 1/16-px coordinates; a bird is its own
+ *                neighbour and coincident birds count;
+ *   core         a bird with >= min_pts neighbours;
+ *   cluster      a connected component of core birds under the neighbour
+ *                relation; its label is the smallest frame-local index of a
+ *                core bird in it (global index = label + offsets[f]);
+ *   border       a non-core bird with a core neighbour: it joins the cluster
+ *                of its nearest core neighbour, ties broken by the smaller
+ *                (y, x) of that core;
+ *   noise        every other bird: label -1.
+ *
+ * Arguments:
+ *   max_frame_points  host: an upper bound on the birds in any one frame
+ *                     (used to size on-chip storage), or 0 if unknown.  A
+ *                     frame above the bound is still clustered correctly, on a
+ *                     slower path.
+ *   eps_q             radius in 1/16 px, 0 <= eps_q <= 32766 (eps px = eps_q/16).
+ *   min_pts           >= 1; the count includes the bird itself.
+ *   labels            device out, int32[total]: frame-local cluster label or -1.
+ *   kind              device out, uint8[total]: 0 noise, 1 border, 2 core.
+ *   n_clusters        device out, int32[n_frames] (or NULL): clusters per frame.
+ *   workspace         device scratch of workspace_bytes bytes, at least
+ *                     cluster_frames_workspace(...) of them, 256-byte aligned;
+ *                     or NULL, in which case the library allocates and frees
+ *                     its scratch stream-ordered (hipMallocAsync/hipFreeAsync).
+ * Labels, kinds and n_clusters are a deterministic function of the input:
+ * they do not depend on the order of birds within a frame beyond the labels'
+ * index convention, nor on thread scheduling.
+ */
+flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
+                            int32_t total, int32_t max_frame_points, int32_t eps_q,
+                            int32_t min_pts, int32_t *labels, uint8_t *kind,
+                            int32_t *n_clusters, void *workspace, size_t workspace_bytes,
+                            void *stream);
+
+/* Bytes of workspace cluster_frames needs for this batch shape (may be 0). */
+size_t cluster_frames_workspace(int32_t n_frames, int32_t total, int32_t max_frame_points);
+
+/*
+ * density_frames - Gaussian kernel density grid of every frame.
+ *
+ * Algorithm 1 (Section 3.6) computes, for every grid cell and every bird, a
+ * distance-based contribution to the cell's density; the paper vectorises
+ * the grid-to-bird distances.  The grid here has grid_w x grid_h cells tiling
+ * the frame [0, width_px) x [0, height_px), evaluated at the cell centres
+ *     cx = (gx + 1/2) width_px / grid_w,   cy = (gy + 1/2) height_px / grid_h,
+ * and each bird (x, y) = (x_q/16, y_q/16) px adds an isotropic Gaussian of
+ * bandwidth sigma_px with unit mass:
+ *     density[f][gy][gx] = sum_i exp(-((cx-x_i)^2 + (cy-y_i)^2) / (2 sigma^2))
+ *                          / (2 pi sigma^2)                    [birds / px^2]
+ * The sum factorises as density = c * Fy . Fx^T with Fx[gx][i] and Fy[gy][i]
+ * the per-axis Gaussian factors; it is evaluated as that contraction over
+ * the birds on the matrix cores, fp16 factors with fp32 accumulation.
+ * Accuracy: relative to the frame's maximum, |error| <= 1e-3 (the fp16
+ * rounding of the two factors bounds each term's relative error by about
+ * 2^-10); an empty frame gives exact zeros.
+ *
+ * Arguments:
+ *   width_px, height_px   frame extent, >= 1.
+ *   grid_w, grid_h        grid size, 1 .. 4096 each.
+ *   sigma_px              bandwidth, finite, > 0.
+ *   density               device out, float[n_frames][grid_h][grid_w].
+ *   workspace             as for cluster_frames, sized by
+ *                         density_frames_workspace(...).
+ * The result is deterministic (fixed summation order).
+ */
+flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
+                            int32_t total, int32_t width_px, int32_t height_px, int32_t grid_w,
+                            int32_t grid_h, float sigma_px, float *density, void *workspace,
+                            size_t workspace_bytes, void *stream);
+
+/* Bytes of workspace density_frames needs for this batch shape (may be 0). */
+size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h);
+
+/* Text of the last error on this thread ("" if none); valid until the next
+ * library call on this thread. */
+const char *flock_last_error(void);
+
+/* Library version string, e.g. "flock 0.1.0 gfx950". */
+const char *flock_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLOCK_H */

@@ -1,0 +1,142 @@
+"""Python binding of libflock (the C ABI in include/flock.h).
+
+Argument marshalling only: torch tensors provide device memory and the
+current HIP stream; every step of the computation runs in the library's HIP
+kernels.  There is no CPU fallback: if libflock.so is missing or the device is
+not a gfx950 GPU, calls raise.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libflock.so")
+
+FLOCK_OK = 0
+FLOCK_EINVAL = -1
+FLOCK_ENOMEM = -2
+FLOCK_EDEVICE = -3
+FLOCK_EUNSUPPORTED = -4
+
+QUANTA_PER_PX = 16
+
+_lib = None
+
+
+class FlockError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"flock status {status}: {message}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libflock.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2512_07009_amd.build` (there is no fallback path)")
+        L = ctypes.CDLL(LIB_PATH)
+        p, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        L.cluster_frames.argtypes = [p, p, i32, i32, i32, i32, i32, p, p, p, p, sz, p]
+        L.cluster_frames.restype = i32
+        L.density_frames.argtypes = [p, p, i32, i32, i32, i32, i32, i32, ctypes.c_float, p, p, sz, p]
+        L.density_frames.restype = i32
+        L.cluster_frames_workspace.argtypes = [i32, i32, i32]
+        L.cluster_frames_workspace.restype = sz
+        L.density_frames_workspace.argtypes = [i32, i32, i32, i32]
+        L.density_frames_workspace.restype = sz
+        L.flock_last_error.argtypes = []
+        L.flock_last_error.restype = ctypes.c_char_p
+        L.flock_version.argtypes = []
+        L.flock_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != FLOCK_OK:
+        msg = lib().flock_last_error().decode()
+        if status == FLOCK_EINVAL:
+            raise ValueError(f"flock: {msg}")
+        raise FlockError(status, msg)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr() if t is not None else None)
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _batch(xy: torch.Tensor, offsets: torch.Tensor):
+    if not (xy.is_cuda and offsets.is_cuda):
+        raise ValueError("xy and offsets must be device tensors")
+    if xy.dtype != torch.int32 or offsets.dtype != torch.int32:
+        raise ValueError("xy and offsets must be int32")
+    if xy.dim() != 2 or xy.shape[1] != 2 or not xy.is_contiguous():
+        raise ValueError("xy must be a contiguous [T, 2] tensor")
+    if offsets.dim() != 1 or offsets.numel() < 1 or not offsets.is_contiguous():
+        raise ValueError("offsets must be a contiguous [F + 1] tensor")
+    return offsets.numel() - 1, xy.shape[0]
+
+
+def eps_to_quanta(eps_px: float) -> int:
+    q = eps_px * QUANTA_PER_PX
+    if abs(q - round(q)) > 1e-9:
+        raise ValueError(f"eps_px = {eps_px} is not a multiple of 1/16 px")
+    return int(round(q))
+
+
+def cluster_frames(xy: torch.Tensor, offsets: torch.Tensor, eps_px: float, min_pts: int,
+                   max_frame_points: int = 0, out=None, stream=None):
+    """Cluster every frame; returns (labels int32[T], kind uint8[T], n_clusters int32[F]).
+
+    max_frame_points: an upper bound on birds per frame (0 = unknown); it
+    sizes on-chip storage and is not checked against the data.
+    out: optional (labels, kind, n_clusters) tensors to write into.
+    """
+    F, T = _batch(xy, offsets)
+    dev = xy.device
+    if out is None:
+        labels = torch.empty(T, dtype=torch.int32, device=dev)
+        kind = torch.empty(T, dtype=torch.uint8, device=dev)
+        ncl = torch.empty(max(F, 0), dtype=torch.int32, device=dev)
+    else:
+        labels, kind, ncl = out
+    ws_bytes = lib().cluster_frames_workspace(F, T, int(max_frame_points))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
+    with torch.cuda.device(dev):
+        st = lib().cluster_frames(_ptr(xy), _ptr(offsets), F, T, int(max_frame_points),
+                                  eps_to_quanta(eps_px), int(min_pts), _ptr(labels), _ptr(kind),
+                                  _ptr(ncl), _ptr(ws), ws_bytes, _stream(stream))
+    _check(st)
+    return labels, kind, ncl
+
+
+def density_frames(xy: torch.Tensor, offsets: torch.Tensor, width_px: int, height_px: int,
+                   grid_w: int, grid_h: int, sigma_px: float, out=None, stream=None):
+    """Gaussian density grid of every frame: float32[F, grid_h, grid_w] (birds / px^2)."""
+    F, T = _batch(xy, offsets)
+    dev = xy.device
+    dens = out if out is not None else torch.empty((max(F, 0), grid_h, grid_w), dtype=torch.float32,
+                                                  device=dev)
+    ws_bytes = lib().density_frames_workspace(F, T, int(grid_w), int(grid_h))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
+    with torch.cuda.device(dev):
+        st = lib().density_frames(_ptr(xy), _ptr(offsets), F, T, int(width_px), int(height_px),
+                                  int(grid_w), int(grid_h), float(sigma_px), _ptr(dens), _ptr(ws),
+                                  ws_bytes, _stream(stream))
+    _check(st)
+    return dens
+
+
+def version() -> str:
+    return lib().flock_version().decode()

@@ -1,0 +1,253 @@
+// api.cpp - the C ABI of libflock (declared in include/flock.h): argument
+// validation, launch planning and error reporting.  No computation happens
+// here; every step of the path runs in the HIP kernels.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "flock.h"
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+flock_status fail(flock_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return st;
+}
+
+flock_status hip_fail(hipError_t err, const char *what) {
+    return fail(FLOCK_EDEVICE, "%s: %s", what, hipGetErrorString(err));
+}
+
+struct DeviceInfo {
+    bool valid = false;
+    bool gfx950 = false;
+    int n_cus = 0;
+    size_t lds_per_block = 0;
+    char arch[64] = {0};
+};
+
+constexpr int kMaxDevices = 64;
+DeviceInfo g_devices[kMaxDevices];
+std::once_flag g_device_once[kMaxDevices];
+
+flock_status device_info(const DeviceInfo **out) {
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return hip_fail(err, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(FLOCK_EUNSUPPORTED, "device index %d", dev);
+    std::call_once(g_device_once[dev], [dev] {
+        hipDeviceProp_t prop;
+        if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return;
+        DeviceInfo &d = g_devices[dev];
+        std::snprintf(d.arch, sizeof d.arch, "%s", prop.gcnArchName);
+        d.gfx950 = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+        d.n_cus = prop.multiProcessorCount;
+        d.lds_per_block = prop.sharedMemPerBlock;
+        d.valid = true;
+    });
+    const DeviceInfo &d = g_devices[dev];
+    if (!d.valid) return fail(FLOCK_EDEVICE, "could not read properties of device %d", dev);
+    if (!d.gfx950) return fail(FLOCK_EUNSUPPORTED, "device %d is %s; this library is built for gfx950", dev, d.arch);
+    *out = &d;
+    return FLOCK_OK;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool validate_requested() {
+    const char *v = std::getenv("FLOCK_VALIDATE");
+    return v && v[0] == '1';
+}
+
+// Debug mode: copy offsets (and coordinates) to the host and check them.
+flock_status validate_batch(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
+                            hipStream_t stream) {
+    std::vector<int32_t> off((size_t)n_frames + 1);
+    hipError_t err = hipMemcpyAsync(off.data(), offsets, off.size() * sizeof(int32_t),
+                                    hipMemcpyDeviceToHost, stream);
+    if (err == hipSuccess) err = hipStreamSynchronize(stream);
+    if (err != hipSuccess) return hip_fail(err, "FLOCK_VALIDATE offsets copy");
+    if (off[0] != 0) return fail(FLOCK_EINVAL, "offsets[0] = %d, expected 0", off[0]);
+    for (int32_t f = 0; f < n_frames; ++f)
+        if (off[f + 1] < off[f]) return fail(FLOCK_EINVAL, "offsets decrease at frame %d", f);
+    if (off[n_frames] != total)
+        return fail(FLOCK_EINVAL, "offsets[n_frames] = %d but total = %d", off[n_frames], total);
+    if (total > 0) {
+        std::vector<int32_t> h((size_t)total * 2);
+        err = hipMemcpyAsync(h.data(), xy, h.size() * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+        if (err == hipSuccess) err = hipStreamSynchronize(stream);
+        if (err != hipSuccess) return hip_fail(err, "FLOCK_VALIDATE xy copy");
+        for (size_t i = 0; i < h.size(); ++i)
+            if (h[i] < 0 || h[i] >= (1 << 24))
+                return fail(FLOCK_EINVAL, "coordinate %d of bird %zu outside [0, 2^24)", h[i], i / 2);
+    }
+    return FLOCK_OK;
+}
+
+// Largest s >= 1 with 2 s^2 <= e^2 (cell side whose diagonal is <= e).
+int32_t diagonal_cell_side(int32_t e) {
+    const int64_t half = (int64_t)e * e / 2;
+    int64_t s = (int64_t)std::sqrt((double)half);
+    while (s * s > half) --s;
+    while ((s + 1) * (s + 1) <= half) ++s;
+    return s < 1 ? 1 : (int32_t)s;
+}
+
+struct ClusterPlan {
+    int32_t cap_points;
+    int32_t cap_cells;
+    size_t lds_bytes;
+};
+
+ClusterPlan plan_cluster(int32_t max_frame_points, size_t lds_limit) {
+    ClusterPlan p;
+    const int32_t limit = flock::cluster_max_cap_points(lds_limit);
+    p.cap_points = (max_frame_points > 0 && max_frame_points < limit) ? max_frame_points : limit;
+    const size_t reserve = 1024;  // static shared variables
+    const int64_t avail = (int64_t)lds_limit - (int64_t)reserve - 16 * (int64_t)p.cap_points;
+    int64_t cells = std::max<int64_t>(4096, 2 * (int64_t)p.cap_points);
+    cells = std::min<int64_t>(cells, avail / 4 - 1);
+    p.cap_cells = (int32_t)cells;
+    p.lds_bytes = flock::cluster_lds_bytes(p.cap_points, p.cap_cells);
+    return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *flock_last_error(void) { return g_error.c_str(); }
+
+const char *flock_version(void) { return "flock 0.1.0 gfx950"; }
+
+size_t cluster_frames_workspace(int32_t n_frames, int32_t total, int32_t max_frame_points) {
+    (void)n_frames;
+    (void)total;
+    (void)max_frame_points;
+    return 0;
+}
+
+size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h) {
+    (void)n_frames;
+    (void)total;
+    (void)grid_w;
+    (void)grid_h;
+    return 0;
+}
+
+flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
+                            int32_t max_frame_points, int32_t eps_q, int32_t min_pts, int32_t *labels,
+                            uint8_t *kind, int32_t *n_clusters, void *workspace, size_t workspace_bytes,
+                            void *stream) {
+    g_error.clear();
+    (void)workspace;
+    (void)workspace_bytes;
+    if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
+    if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
+    if (max_frame_points < 0) return fail(FLOCK_EINVAL, "max_frame_points = %d < 0", max_frame_points);
+    if (eps_q < 0 || eps_q > 32766) return fail(FLOCK_EINVAL, "eps_q = %d outside [0, 32766]", eps_q);
+    if (min_pts < 1) return fail(FLOCK_EINVAL, "min_pts = %d < 1", min_pts);
+    if (n_frames == 0) return FLOCK_OK;
+    if (!offsets) return fail(FLOCK_EINVAL, "offsets is NULL");
+    if (total > 0 && (!xy || !labels || !kind))
+        return fail(FLOCK_EINVAL, "xy, labels and kind must be non-NULL when total > 0");
+    if (!aligned(xy, 8)) return fail(FLOCK_EINVAL, "xy must be 8-byte aligned");
+    if (!aligned(offsets, 4) || !aligned(labels, 4) || !aligned(n_clusters, 4))
+        return fail(FLOCK_EINVAL, "offsets, labels and n_clusters must be 4-byte aligned");
+    if (total == 0 && !n_clusters) return FLOCK_OK;
+
+    const DeviceInfo *dev = nullptr;
+    flock_status st = device_info(&dev);
+    if (st != FLOCK_OK) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (validate_requested()) {
+        st = validate_batch(xy, offsets, n_frames, total, s);
+        if (st != FLOCK_OK) return st;
+    }
+
+    const ClusterPlan plan = plan_cluster(max_frame_points, dev->lds_per_block);
+    flock::ClusterArgs a;
+    a.xy = xy;
+    a.offsets = offsets;
+    a.n_frames = n_frames;
+    a.total = total;
+    a.eps_q = eps_q;
+    a.min_pts = min_pts;
+    a.cell_side = diagonal_cell_side(eps_q);
+    a.cap_points = plan.cap_points;
+    a.cap_cells = plan.cap_cells;
+    a.labels = labels;
+    a.kind = kind;
+    a.n_clusters = n_clusters;
+    hipError_t err = flock::launch_cluster_resident(a, plan.lds_bytes, s);
+    if (err != hipSuccess) return hip_fail(err, "cluster kernel launch");
+    return FLOCK_OK;
+}
+
+flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
+                            int32_t width_px, int32_t height_px, int32_t grid_w, int32_t grid_h,
+                            float sigma_px, float *density, void *workspace, size_t workspace_bytes,
+                            void *stream) {
+    g_error.clear();
+    (void)workspace;
+    (void)workspace_bytes;
+    if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
+    if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
+    if (width_px < 1 || height_px < 1)
+        return fail(FLOCK_EINVAL, "frame extent %d x %d px must be >= 1", width_px, height_px);
+    if (grid_w < 1 || grid_h < 1 || grid_w > 4096 || grid_h > 4096)
+        return fail(FLOCK_EINVAL, "grid %d x %d outside 1..4096", grid_w, grid_h);
+    if (!std::isfinite(sigma_px) || !(sigma_px > 0.0f))
+        return fail(FLOCK_EINVAL, "sigma_px must be finite and > 0");
+    if (n_frames == 0) return FLOCK_OK;
+    if (!offsets || !density) return fail(FLOCK_EINVAL, "offsets and density must be non-NULL");
+    if (total > 0 && !xy) return fail(FLOCK_EINVAL, "xy is NULL with total > 0");
+    if (!aligned(xy, 8)) return fail(FLOCK_EINVAL, "xy must be 8-byte aligned");
+    if (!aligned(offsets, 4) || !aligned(density, 4))
+        return fail(FLOCK_EINVAL, "offsets and density must be 4-byte aligned");
+
+    const DeviceInfo *dev = nullptr;
+    flock_status st = device_info(&dev);
+    if (st != FLOCK_OK) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (validate_requested()) {
+        st = validate_batch(xy, offsets, n_frames, total, s);
+        if (st != FLOCK_OK) return st;
+    }
+
+    flock::DensityArgs a;
+    a.xy = xy;
+    a.offsets = offsets;
+    a.n_frames = n_frames;
+    a.total = total;
+    a.width_px = width_px;
+    a.height_px = height_px;
+    a.grid_w = grid_w;
+    a.grid_h = grid_h;
+    a.sigma_px = sigma_px;
+    a.density = density;
+    const flock::DensityPlan plan = flock::plan_density(a, dev->n_cus);
+    const long long blocks = (long long)n_frames * plan.regions_y * plan.regions_x;
+    if (blocks > 0x7fffffffLL) return fail(FLOCK_EUNSUPPORTED, "batch too large for one launch");
+    hipError_t err = flock::launch_density(a, plan, s);
+    if (err != hipSuccess) return hip_fail(err, "density kernel launch");
+    return FLOCK_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,61 @@
+// internal.h - declarations shared by the library's own translation units
+// (host API and kernel launchers).  Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace flock {
+
+// ----------------------------------------------------------------------------
+// Clustering
+// ----------------------------------------------------------------------------
+struct ClusterArgs {
+    const int32_t *xy;        // [total][2] 1/16 px
+    const int32_t *offsets;   // [n_frames + 1]
+    int32_t n_frames;
+    int32_t total;
+    int32_t eps_q;            // radius in quanta
+    int32_t min_pts;
+    int32_t cell_side;        // largest s >= 1 with 2 s^2 <= eps_q^2
+    int32_t cap_points;       // frames with more points take the in-place path
+    int32_t cap_cells;        // cell-table entries available on chip
+    int32_t *labels;          // [total]
+    uint8_t *kind;            // [total]
+    int32_t *n_clusters;      // [n_frames] or nullptr
+};
+
+// Bytes of dynamic LDS the resident clustering kernel needs for these caps.
+size_t cluster_lds_bytes(int32_t cap_points, int32_t cap_cells);
+// Largest point capacity that fits the device's LDS with a cell table of
+// at least min_cells entries.
+int32_t cluster_max_cap_points(size_t lds_limit);
+
+hipError_t launch_cluster_resident(const ClusterArgs &a, size_t lds_bytes, hipStream_t stream);
+
+// ----------------------------------------------------------------------------
+// Density
+// ----------------------------------------------------------------------------
+struct DensityArgs {
+    const int32_t *xy;
+    const int32_t *offsets;
+    int32_t n_frames;
+    int32_t total;
+    int32_t width_px, height_px;
+    int32_t grid_w, grid_h;
+    float sigma_px;
+    float *density;           // [n_frames][grid_h][grid_w]
+};
+
+struct DensityPlan {
+    int tm;                   // 16-row gy tiles per workgroup region
+    int tnw;                  // 16-col gx tiles per wave (4 waves per region)
+    int regions_y, regions_x; // regions per frame
+};
+
+DensityPlan plan_density(const DensityArgs &a, int n_cus);
+hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, hipStream_t stream);
+
+}  // namespace flock

@@ -1,0 +1,100 @@
+"""The C ABI library loads, exports what include/flock.h declares, and rejects
+bad arguments on the host before touching any device (no GPU needed)."""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_2512_07009_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flock.h")
+
+FAKE = ctypes.c_void_p(0x100000)       # never dereferenced on the EINVAL paths
+FAKE4 = ctypes.c_void_p(0x100004)      # 4-byte aligned, not 8
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_function():
+    lib = binding.lib()
+    names = declared_functions()
+    assert {"cluster_frames", "density_frames", "cluster_frames_workspace",
+            "density_frames_workspace", "flock_last_error", "flock_version"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert binding.version().startswith("flock ")
+
+
+def _cluster(n_frames=1, total=4, max_fp=0, eps_q=640, min_pts=4, xy=FAKE, offsets=FAKE,
+             labels=FAKE, kind=FAKE, ncl=FAKE):
+    return binding.lib().cluster_frames(xy, offsets, n_frames, total, max_fp, eps_q, min_pts,
+                                        labels, kind, ncl, None, 0, None)
+
+
+def _density(n_frames=1, total=4, w=1920, h=1080, gx=128, gy=72, sigma=30.0, xy=FAKE,
+             offsets=FAKE, out=FAKE):
+    return binding.lib().density_frames(xy, offsets, n_frames, total, w, h, gx, gy, sigma, out,
+                                        None, 0, None)
+
+
+@pytest.mark.parametrize("kwargs,needle", [
+    (dict(n_frames=-1), "n_frames"),
+    (dict(total=-5), "total"),
+    (dict(max_fp=-1), "max_frame_points"),
+    (dict(eps_q=-1), "eps_q"),
+    (dict(eps_q=32767), "eps_q"),
+    (dict(min_pts=0), "min_pts"),
+    (dict(offsets=None), "offsets"),
+    (dict(xy=None), "non-NULL"),
+    (dict(labels=None), "non-NULL"),
+    (dict(xy=FAKE4), "aligned"),
+])
+def test_cluster_rejects_bad_arguments(kwargs, needle):
+    assert _cluster(**kwargs) == binding.FLOCK_EINVAL
+    assert needle in binding.lib().flock_last_error().decode()
+
+
+@pytest.mark.parametrize("kwargs,needle", [
+    (dict(n_frames=-1), "n_frames"),
+    (dict(w=0), "extent"),
+    (dict(h=-3), "extent"),
+    (dict(gx=0), "grid"),
+    (dict(gy=5000), "grid"),
+    (dict(sigma=0.0), "sigma"),
+    (dict(sigma=-1.0), "sigma"),
+    (dict(sigma=math.nan), "sigma"),
+    (dict(sigma=math.inf), "sigma"),
+    (dict(out=None), "non-NULL"),
+    (dict(xy=FAKE4), "aligned"),
+])
+def test_density_rejects_bad_arguments(kwargs, needle):
+    assert _density(**kwargs) == binding.FLOCK_EINVAL
+    assert needle in binding.lib().flock_last_error().decode()
+
+
+def test_empty_batches_are_noops_without_a_device():
+    assert _cluster(n_frames=0, total=0, xy=None, offsets=None, labels=None, kind=None, ncl=None) == 0
+    assert _density(n_frames=0, total=0, xy=None, offsets=None, out=None) == 0
+    assert binding.lib().flock_last_error().decode() == ""
+
+
+def test_workspace_queries():
+    lib = binding.lib()
+    assert lib.cluster_frames_workspace(64, 128000, 2000) >= 0
+    assert lib.density_frames_workspace(64, 128000, 128, 72) >= 0
+
+
+def test_eps_to_quanta():
+    assert binding.eps_to_quanta(40.0) == 640
+    assert binding.eps_to_quanta(25.0) == 400
+    assert binding.eps_to_quanta(0.0625) == 1
+    with pytest.raises(ValueError):
+        binding.eps_to_quanta(0.01)

@@ -1,0 +1,255 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bars: labels, kinds and n_clusters bit-exact; density within a relative L-inf
+error of 1e-3 of each frame's maximum (exact zeros for empty frames).
+"""
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2512_07009_amd as flock
+from paper_2512_07009_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+DENSITY_RTOL_OF_MAX = 1e-3
+
+
+def dev_batch(xy, off):
+    return (torch.from_numpy(np.ascontiguousarray(xy)).to("cuda"),
+            torch.from_numpy(np.ascontiguousarray(off)).to("cuda"))
+
+
+def max_count(off):
+    return int(np.diff(off).max()) if len(off) > 1 else 0
+
+
+def run_cluster(xy, off, eps_q, min_pts, max_fp=None):
+    dxy, doff = dev_batch(xy, off)
+    labels, kind, ncl = flock.cluster_frames(dxy, doff, eps_q / 16.0, min_pts,
+                                             max_count(off) if max_fp is None else max_fp)
+    torch.cuda.synchronize()
+    return labels.cpu().numpy(), kind.cpu().numpy(), ncl.cpu().numpy()
+
+
+def run_density(xy, off, w, h, gx, gy, sigma):
+    dxy, doff = dev_batch(xy, off)
+    d = flock.density_frames(dxy, doff, w, h, gx, gy, sigma)
+    torch.cuda.synchronize()
+    return d.cpu().numpy()
+
+
+def sub_batch(xy, off, frames):
+    parts = [xy[off[f]:off[f + 1]] for f in frames]
+    return wl.pack(parts)
+
+
+def assert_cluster_equal(got, xy, off, eps_q, min_pts, frames=None, tag=""):
+    labels, kind, ncl = got
+    if frames is None:
+        frames = list(range(len(off) - 1))
+    sxy, soff = sub_batch(xy, off, frames)
+    rl, rk, rn = oracle.cluster_frames(sxy, soff, eps_q, min_pts)
+    for j, f in enumerate(frames):
+        b, e = off[f], off[f + 1]
+        sb, se = soff[j], soff[j + 1]
+        if not np.array_equal(kind[b:e], rk[sb:se]):
+            bad = np.nonzero(kind[b:e] != rk[sb:se])[0][:5]
+            raise AssertionError(f"{tag} frame {f}: kind differs at {bad.tolist()}")
+        if not np.array_equal(labels[b:e], rl[sb:se]):
+            bad = np.nonzero(labels[b:e] != rl[sb:se])[0][:5]
+            raise AssertionError(f"{tag} frame {f}: labels differ at {bad.tolist()} "
+                                 f"got {labels[b:e][bad].tolist()} want {rl[sb:se][bad].tolist()}")
+        assert ncl[f] == rn[j], f"{tag} frame {f}: n_clusters {ncl[f]} != {rn[j]}"
+
+
+def assert_density_close(got, ref, counts=None, sigma=None, tag=""):
+    """max |got - ref| <= 1e-3 * max(ref) per frame.
+
+    With counts and sigma given, an absolute floor of n_f * c * 2^-24 is added
+    (c = 1 / (2 pi sigma^2)): fp16 factors carry an absolute error of up to
+    2^-25 each in their subnormal range, so a frame whose whole density lies
+    below that range (every bird > 5.9 sigma from every cell centre) is only
+    resolved to that floor.  The five workloads are checked without it.
+    """
+    worst = 0.0
+    for f in range(ref.shape[0]):
+        m = ref[f].max()
+        if m == 0.0:
+            assert (got[f] == 0).all(), f"{tag} frame {f}: empty frame not exactly zero"
+            continue
+        floor = 0.0
+        if counts is not None:
+            floor = counts[f] * 2.0 ** -24 / (2.0 * np.pi * sigma * sigma)
+        diff = np.abs(got[f].astype(np.float64) - ref[f]).max()
+        err = diff / m
+        worst = max(worst, err if diff > floor else 0.0)
+        assert diff <= DENSITY_RTOL_OF_MAX * m + floor, f"{tag} frame {f}: rel L-inf error {err:.3e}"
+    return worst
+
+
+# ---------------------------------------------------------------------------
+# clustering
+# ---------------------------------------------------------------------------
+
+def test_handbuilt_gpu(handbuilt):
+    for case in handbuilt:
+        xy, off = wl.pack([np.asarray(f, np.int32).reshape(-1, 2) for f in case["frames"]])
+        labels, kind, ncl = run_cluster(xy, off, case["eps_q"], case["min_pts"])
+        for f in range(len(case["frames"])):
+            assert labels[off[f]:off[f + 1]].tolist() == case["labels"][f], case["name"]
+            assert kind[off[f]:off[f + 1]].tolist() == case["kind"][f], case["name"]
+        assert ncl.tolist() == case["n_clusters"], case["name"]
+
+
+RANDOM_PARAMS = [(640, 4), (640, 1), (400, 6), (960, 5), (1, 2), (0, 2), (32766, 3), (100, 3)]
+
+
+@pytest.mark.parametrize("eps_q,min_pts", RANDOM_PARAMS)
+def test_random_batches_gpu(eps_q, min_pts):
+    for seed in range(3):
+        xy, off = wl.random_batch(1000 * eps_q + 10 * min_pts + seed, 24, 700)
+        got = run_cluster(xy, off, eps_q, min_pts)
+        assert_cluster_equal(got, xy, off, eps_q, min_pts, tag=f"seed {seed}")
+
+
+@pytest.mark.parametrize("max_fp", [8, 100])
+def test_inplace_path_gpu(max_fp):
+    """Frames above max_frame_points take the in-place path; results are identical."""
+    xy, off = wl.random_batch(77 + max_fp, 16, 600)
+    got = run_cluster(xy, off, 640, 4, max_fp=max_fp)
+    assert_cluster_equal(got, xy, off, 640, 4, tag=f"max_fp {max_fp}")
+
+
+def test_frame_above_lds_capacity_gpu():
+    rng = np.random.default_rng(5)
+    big = np.stack([rng.integers(0, 16 * 800, 12000), rng.integers(0, 16 * 600, 12000)], 1).astype(np.int32)
+    small = rng.integers(0, 16 * 500, (300, 2)).astype(np.int32)
+    xy, off = wl.pack([small, big, small[:50]])
+    got = run_cluster(xy, off, 160, 5, max_fp=0)
+    assert_cluster_equal(got, xy, off, 160, 5, tag="big frame")
+
+
+def test_lattice_ties_gpu():
+    frames = [wl.lattice_frame(30, 20, 640), wl.lattice_frame(25, 25, 452, 1000, 2000),
+              wl.lattice_frame(10, 10, 641), np.concatenate([wl.lattice_frame(12, 12, 384),
+                                                             wl.lattice_frame(12, 12, 512, 384, 0)])]
+    xy, off = wl.pack(frames)
+    for min_pts in (2, 3, 5, 6):
+        got = run_cluster(xy, off, 640, min_pts)
+        assert_cluster_equal(got, xy, off, 640, min_pts, tag=f"lattice minPts {min_pts}")
+
+
+def test_bad_offsets_do_not_fault_gpu():
+    xy = np.zeros((10, 2), np.int32)
+    off = np.array([0, 5, 3, 10, 12], np.int32)   # frame 1 negative, frame 3 past total
+    labels, kind, ncl = run_cluster(xy, off, 640, 2, max_fp=10)
+    assert ncl[1] == -1 and ncl[3] == -1
+    assert ncl[0] == 1
+
+
+def test_validate_mode_rejects_bad_offsets_gpu():
+    xy = np.zeros((10, 2), np.int32)
+    off = np.array([0, 5, 3, 10], np.int32)
+    os.environ["FLOCK_VALIDATE"] = "1"
+    try:
+        with pytest.raises(ValueError, match="decrease"):
+            run_cluster(xy, off, 640, 2)
+        xy2, off2 = wl.random_batch(3, 4, 50)
+        got = run_cluster(xy2, off2, 640, 3)
+        assert_cluster_equal(got, xy2, off2, 640, 3)
+    finally:
+        del os.environ["FLOCK_VALIDATE"]
+
+
+def test_determinism_and_batch_independence_gpu():
+    xy, off, w = wl.generate("batch64x2000_1080p", n_frames=8)
+    a = run_cluster(xy, off, w.eps_q, w.min_pts)
+    b = run_cluster(xy, off, w.eps_q, w.min_pts)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    # frame 3 alone gives the same labels as inside the batch
+    sxy, soff = sub_batch(xy, off, [3])
+    alone = run_cluster(sxy, soff, w.eps_q, w.min_pts)
+    assert np.array_equal(alone[0], a[0][off[3]:off[4]])
+    assert np.array_equal(alone[1], a[1][off[3]:off[4]])
+
+
+def test_permutation_invariance_gpu():
+    xy, off, w = wl.generate("batch64x2000_1080p", n_frames=1)
+    base_l, base_k, base_n = run_cluster(xy, off, w.eps_q, w.min_pts)
+    perm = np.random.default_rng(1).permutation(xy.shape[0])
+    pl, pk, pn = run_cluster(xy[perm], off, w.eps_q, w.min_pts)
+    inv = np.empty_like(perm)
+    inv[perm] = np.arange(len(perm))
+    assert np.array_equal(pk[inv], base_k) and pn[0] == base_n[0]
+    mapped = np.where(pl[inv] >= 0, perm[np.maximum(pl[inv], 0)], -1)
+    canon = {}
+    for i in np.nonzero(base_k == 2)[0]:
+        canon.setdefault(mapped[i], i)
+    assert np.array_equal(np.array([canon[m] if m >= 0 else -1 for m in mapped]), base_l)
+
+
+# ---------------------------------------------------------------------------
+# density
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("w,h,gx,gy,sigma", [
+    (1920, 1080, 64, 36, 30.0), (1920, 1080, 128, 72, 30.0), (3840, 2160, 256, 144, 45.0),
+    (1920, 1080, 1, 1, 30.0), (640, 480, 17, 5, 12.5), (1000, 700, 100, 37, 3.0),
+    (1920, 1080, 128, 72, 0.7), (1920, 1080, 33, 19, 2000.0),
+])
+def test_density_random_gpu(w, h, gx, gy, sigma):
+    xy, off = wl.random_batch(gx * 1000 + gy, 12, 400, width_px=w, height_px=h)
+    got = run_density(xy, off, w, h, gx, gy, sigma)
+    ref = oracle.density_frames(xy, off, w, h, gx, gy, sigma)
+    worst = assert_density_close(got, ref, np.diff(off), sigma, tag=f"{gx}x{gy} sigma {sigma}")
+    print(f"density {gx}x{gy} sigma {sigma}: worst rel err {worst:.2e}")
+
+
+def test_density_single_bird_peak_gpu():
+    sigma = 30.0
+    # bird exactly at the centre of cell (40, 30) of a 128 x 72 grid on 1920 x 1080
+    xy, off = wl.pack([np.array([[16 * 607 + 8, 16 * 457 + 8]], np.int32)])
+    got = run_density(xy, off, 1920, 1080, 128, 72, sigma)[0]
+    peak = 1.0 / (2.0 * np.pi * sigma * sigma)
+    assert np.unravel_index(np.argmax(got), got.shape) == (30, 40)
+    assert abs(got[30, 40] - peak) <= 1e-3 * peak
+
+
+def test_density_determinism_gpu():
+    xy, off, w = wl.generate("batch64x2000_1080p", n_frames=4)
+    a = run_density(xy, off, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px)
+    b = run_density(xy, off, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px)
+    assert np.array_equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# the five workloads at full size, in the launch configuration the bench uses
+# ---------------------------------------------------------------------------
+
+# frames compared against the oracle: all, or a spread sample of large batches
+CLUSTER_FRAMES = {"single500_1080p": None, "batch64x2000_1080p": None,
+                  "batch256xpoisson8000_4k": None, "house30000_4k": None,
+                  "stream1800x5000_1080p": list(range(0, 1800, 45)) + [1799]}
+DENSITY_FRAMES = {"single500_1080p": None, "batch64x2000_1080p": None,
+                  "batch256xpoisson8000_4k": [0, 1, 100, 255], "house30000_4k": None,
+                  "stream1800x5000_1080p": [0, 1, 900, 1799]}
+
+
+@pytest.mark.parametrize("name", wl.WORKLOAD_ORDER)
+def test_workload_parity_gpu(name):
+    xy, off, w = wl.generate(name)
+    print(f"{name}: {len(off) - 1} frames, {xy.shape[0]} birds", flush=True)
+    got = run_cluster(xy, off, w.eps_q, w.min_pts)
+    assert_cluster_equal(got, xy, off, w.eps_q, w.min_pts, frames=CLUSTER_FRAMES[name], tag=name)
+    dens = run_density(xy, off, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px)
+    frames = DENSITY_FRAMES[name] or list(range(len(off) - 1))
+    sxy, soff = sub_batch(xy, off, frames)
+    ref = oracle.density_frames(sxy, soff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px)
+    worst = assert_density_close(dens[frames], ref, tag=name)
+    print(f"{name}: clustering exact, density worst rel err {worst:.2e}", flush=True)
