@@ -1,0 +1,198 @@
+#!/usr/bin/env python3
+"""Benchmark: frames/s of the per-frame clustering + density hot path on one GPU.
+
+One step = cluster_frames + density_frames over one batch of synthetic frames
+(default: 64 frames x 2000 birds, 1920x1080 px, eps 40 px, minPts 4, density
+grid 128x72, sigma 30 px).  Inputs are resident in device memory before the
+timed region; W warm-up steps, then K timed steps bracketed by device
+synchronisation.  Per-kernel durations come from HIP events recorded on the
+stream the kernels run on, inside the timed region.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HEADLINE = "batch64x2000_1080p"
+METRIC = "frames/sec (cluster+density) at 2000 birds/frame"
+
+# MI355X published peaks
+HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0
+
+KERNEL_SOURCES = {
+    "cluster": "paper_2512_07009_amd/csrc/cluster.hip",
+    "density": "paper_2512_07009_amd/csrc/density.hip",
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_hash(rel: str) -> str:
+    with open(os.path.join(ROOT, rel), "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def committed_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    that summary was taken from the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_counters.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"source sha256\[:16\]:\s*`?([0-9a-f]{16})", text)
+    m_bytes = re.search(r"HBM bytes per launch \(scaled\):\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != source_hash(KERNEL_SOURCES[kernel]):
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(xy, off, w, budget_s: float):
+    """The CPU oracle on the host cores: whole frames, as many as fit ~budget_s."""
+    import oracle
+    threads = oracle.default_threads()
+    F = len(off) - 1
+    # probe one frame, then size the sample
+    t0 = time.perf_counter()
+    sx, so = xy[off[0]:off[1]], np.array([0, off[1] - off[0]], np.int32)
+    oracle.cluster_frames(sx, so, w.eps_q, w.min_pts, n_threads=threads)
+    oracle.density_frames(sx, so, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
+                          n_threads=threads)
+    per_frame = max(time.perf_counter() - t0, 1e-6)
+    # frames run concurrently across threads for clustering; density threads over rows
+    n = int(max(1, min(F, budget_s / per_frame)))
+    sxy, soff = xy[: off[n]], off[: n + 1]
+    t0 = time.perf_counter()
+    oracle.cluster_frames(sxy, soff, w.eps_q, w.min_pts, n_threads=threads)
+    oracle.density_frames(sxy, soff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
+                          n_threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "frames/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {n} of {F} frames of {w.name} (clustering + density), {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=2.0,
+                    help="target wall seconds for the oracle sample (all host cores)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(frames shard across GPUs with no collective; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2512_07009_amd as flock
+    from paper_2512_07009_amd import workloads as wl
+
+    w = wl.WORKLOADS[args.workload]
+    xy, off, _ = wl.generate(args.workload)
+    F, T = len(off) - 1, xy.shape[0]
+    max_fp = int(np.diff(off).max())
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dxy = torch.from_numpy(xy).to(dev)
+    doff = torch.from_numpy(off).to(dev)
+    labels = torch.empty(T, dtype=torch.int32, device=dev)
+    kind = torch.empty(T, dtype=torch.uint8, device=dev)
+    ncl = torch.empty(F, dtype=torch.int32, device=dev)
+    dens = torch.empty((F, w.grid_h, w.grid_w), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    log(f"workload {w.name}: {F} frames, {T} birds, max {max_fp}/frame; {flock.version()}")
+
+    def step():
+        flock.cluster_frames(dxy, doff, w.eps_px, w.min_pts, max_fp, out=(labels, kind, ncl),
+                             stream=stream)
+        flock.density_frames(dxy, doff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
+                             out=dens, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for k in range(K):
+        ev[k][0].record(stream)
+        flock.cluster_frames(dxy, doff, w.eps_px, w.min_pts, max_fp, out=(labels, kind, ncl),
+                             stream=stream)
+        ev[k][1].record(stream)
+        flock.density_frames(dxy, doff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
+                             out=dens, stream=stream)
+        ev[k][2].record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - t0
+
+    t_cluster = sum(e[0].elapsed_time(e[1]) for e in ev) / K * 1e-3   # s per launch
+    t_density = sum(e[1].elapsed_time(e[2]) for e in ev) / K * 1e-3
+    ms_per_step = wall / K * 1e3
+    value = F / (wall / K)
+
+    # algorithmic work per launch
+    cluster_bytes = 13 * T + 8 * F + 4          # xy 8 + labels 4 + kind 1 per bird; offsets, n_clusters
+    density_flops = 2.0 * w.grid_w * w.grid_h * T
+    cl = {"bound": "hbm", "achieved": cluster_bytes / t_cluster / 1e9, "peak": HBM_PEAK_GBS,
+          "unit": "GB/s", "per_launch_us": t_cluster * 1e6, "algorithmic_bytes": cluster_bytes}
+    cl["frac"] = cl["achieved"] / cl["peak"]
+    cl["traffic"] = committed_traffic("cluster", w.name)
+    de = {"bound": "mfma", "achieved": density_flops / t_density / 1e12, "peak": MFMA_F16_PEAK_TFLOPS,
+          "unit": "TFLOP/s", "per_launch_us": t_density * 1e6, "algorithmic_flops": density_flops}
+    de["frac"] = de["achieved"] / de["peak"]
+    de["traffic"] = committed_traffic("density", w.name)
+    dominant = ("cluster_frames", cl) if t_cluster >= t_density else ("density_frames", de)
+    roof = {k: dominant[1][k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")}
+    roof["kernel"] = dominant[0]
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i32+f16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "frames": F, "birds": T, "birds_per_frame_max": max_fp,
+                   "frame_px": [w.width_px, w.height_px], "eps_px": w.eps_px, "min_pts": w.min_pts,
+                   "grid": [w.grid_w, w.grid_h], "sigma_px": w.sigma_px, "parallelism": "single-gpu"},
+        "birds_per_s": T / (wall / K),
+        "roofline": roof,
+        "kernels": {"cluster_frames": cl, "density_frames": de},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        out["cpu_baseline"] = cpu_baseline(xy, off, w, args.cpu_budget_s)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

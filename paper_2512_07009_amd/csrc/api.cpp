@@ -120,9 +120,9 @@ ClusterPlan plan_cluster(int32_t max_frame_points, size_t lds_limit) {
     const int32_t limit = flock::cluster_max_cap_points(lds_limit);
     p.cap_points = (max_frame_points > 0 && max_frame_points < limit) ? max_frame_points : limit;
     const size_t reserve = 1024;  // static shared variables
-    const int64_t avail = (int64_t)lds_limit - (int64_t)reserve - 16 * (int64_t)p.cap_points;
+    const int64_t avail = (int64_t)lds_limit - (int64_t)reserve - 14 * (int64_t)p.cap_points - 4;
     int64_t cells = std::max<int64_t>(4096, 2 * (int64_t)p.cap_points);
-    cells = std::min<int64_t>(cells, avail / 4 - 1);
+    cells = std::min<int64_t>(cells, avail / 6);
     p.cap_cells = (int32_t)cells;
     p.lds_bytes = flock::cluster_lds_bytes(p.cap_points, p.cap_cells);
     return p;

@@ -40,7 +40,7 @@
 namespace flock {
 namespace {
 
-constexpr int kThreads = 512;
+constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kTile = 1024;  // points per LDS tile on the in-place path
 
@@ -167,31 +167,10 @@ __device__ int block_exclusive_scan(int v, int *wave_tot) {
     return base + inc - v;
 }
 
-// Cell geometry of one frame.
-struct Grid {
-    int32_t x0, y0;      // bbox origin (quanta)
-    int32_t side;        // cell side (quanta)
-    int32_t ncx, ncy;    // cells per axis
-    int32_t ncell;
-    int32_t reach;       // R: neighbour cells lie within +-R cells
-    int32_t dxmax[8];    // per |dy| <= R: widest |dx| whose cells can hold neighbours
-    bool dense_ok;       // side is the eps-diagonal side: same cell => neighbours
-};
-
+// Smallest per-axis distance between points of two cells |d| cells apart.
 __device__ __forceinline__ int64_t cell_gap(int32_t d, int32_t side) {
     d = d < 0 ? -d : d;
     return d == 0 ? 0 : (int64_t)(d - 1) * side + 1;
-}
-
-__device__ __forceinline__ int2 cell_of(int2 p, const Grid &g) {
-    uint32_t ux = (uint32_t)(p.x - g.x0);
-    uint32_t uy = (uint32_t)(p.y - g.y0);
-    int32_t cx = (int32_t)(ux / (uint32_t)g.side);
-    int32_t cy = (int32_t)(uy / (uint32_t)g.side);
-    // bbox-derived, so in range; clamp anyway so no index can leave the table
-    cx = min(max(cx, 0), g.ncx - 1);
-    cy = min(max(cy, 0), g.ncy - 1);
-    return make_int2(cx, cy);
 }
 
 // ---------------------------------------------------------------------------
@@ -316,14 +295,87 @@ __device__ void cluster_frame_inplace(const ClusterArgs &a, int f, int32_t b, in
 // Resident path: one frame per workgroup, all state in LDS
 // ---------------------------------------------------------------------------
 
+constexpr uint16_t kNone = 0xffff;
+constexpr int kMaxOffsets = 16;
+
+// Coordinates relative to the frame's bounding-box corner, packed as
+// x | y << 16 (the resident path takes frames whose extent fits 16 bits).
+__device__ __forceinline__ int32_t pk_x(uint32_t v) { return (int32_t)(v & 0xffffu); }
+__device__ __forceinline__ int32_t pk_y(uint32_t v) { return (int32_t)(v >> 16); }
+
+__device__ __forceinline__ int32_t sq_dist_pk(uint32_t a, uint32_t b, int32_t e1) {
+    const int32_t dx = clamp_abs(pk_x(a) - pk_x(b), e1);
+    const int32_t dy = clamp_abs(pk_y(a) - pk_y(b), e1);
+    return __mul24(dx, dx) + __mul24(dy, dy);
+}
+
+// Cell geometry of one frame (relative coordinates).
+struct Grid {
+    int32_t side;        // cell side (quanta)
+    float inv_side;
+    int32_t ncx, ncy;    // cells per axis
+    int32_t ncell;
+    int32_t reach;       // neighbour cells lie within +-reach cells
+    const int32_t *dxmax;  // [reach + 1] in LDS: per |dy|, widest |dx| whose cells can hold neighbours
+    bool dense_ok;       // side is the eps-diagonal side: same cell => neighbours
+};
+
+// floor(v / side) for 0 <= v < 2^16, via a float reciprocal and one correction.
+__device__ __forceinline__ int32_t cell_coord(int32_t v, const Grid &g, int32_t ncoord) {
+    int32_t c = (int32_t)((float)v * g.inv_side);
+    if (c * g.side > v) --c;
+    else if ((c + 1) * g.side <= v) ++c;
+    return min(max(c, 0), ncoord - 1);
+}
+
+__device__ __forceinline__ int32_t cell_id(uint32_t v, const Grid &g, int32_t *cx, int32_t *cy) {
+    *cx = cell_coord(pk_x(v), g, g.ncx);
+    *cy = cell_coord(pk_y(v), g, g.ncy);
+    return *cy * g.ncx + *cx;
+}
+
+// Neighbours of v among sorted points [q0, q1), stopping once `need` are seen.
+__device__ __forceinline__ int32_t count_span(const uint32_t *pxy, int32_t q0, int32_t q1, uint32_t v,
+                                              const Radius &r, int32_t need) {
+    int32_t cnt = 0;
+    int32_t q = q0;
+    for (; q + 4 <= q1; q += 4) {
+        const uint32_t w0 = pxy[q], w1 = pxy[q + 1], w2 = pxy[q + 2], w3 = pxy[q + 3];
+        cnt += (sq_dist_pk(v, w0, r.e1) <= r.e2) + (sq_dist_pk(v, w1, r.e1) <= r.e2) +
+               (sq_dist_pk(v, w2, r.e1) <= r.e2) + (sq_dist_pk(v, w3, r.e1) <= r.e2);
+        if (cnt >= need) return cnt;
+    }
+    for (; q < q1; ++q) cnt += sq_dist_pk(v, pxy[q], r.e1) <= r.e2;
+    return cnt;
+}
+
+// Append `flag` lanes' values to list[] (wave-uniform call: every lane of the
+// wave must reach it).
+__device__ __forceinline__ void wave_append(bool flag, uint16_t value, uint16_t *list, int *counter) {
+    const uint64_t m = __ballot(flag);
+    if (m == 0) return;
+    const int lane = threadIdx.x & 63;
+    int base = 0;
+    if (lane == 0) base = atomicAdd(counter, __popcll(m));
+    base = __shfl(base, 0, 64);
+    if (flag) list[base + __popcll(m & ((1ull << lane) - 1ull))] = value;
+}
+
 __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ int s_bbox[4];
     __shared__ int s_wave[kWaves];
     __shared__ int s_red;
+    __shared__ int s_nlist;
+    __shared__ int s_ncells;
+    __shared__ int s_noff[2];
+    __shared__ int s_odx[2][kMaxOffsets];
+    __shared__ int s_ody[2][kMaxOffsets];
+    __shared__ int s_dxmax[8];
 
     const int f = blockIdx.x;
     const int tid = threadIdx.x;
+    const int lane = tid & 63;
     const int32_t b = a.offsets[f];
     const int32_t e = a.offsets[f + 1];
     if (b < 0 || e < b || e > a.total) {
@@ -331,30 +383,24 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         return;
     }
     const int32_t n = e - b;
+    if (n == 0) {
+        if (tid == 0 && a.n_clusters) a.n_clusters[f] = 0;
+        return;
+    }
     if (tid == 0) {
         s_bbox[0] = INT_MAX;
         s_bbox[1] = INT_MAX;
         s_bbox[2] = INT_MIN;
         s_bbox[3] = INT_MIN;
         s_red = 0;
-    }
-    if (n == 0) {
-        if (tid == 0 && a.n_clusters) a.n_clusters[f] = 0;
-        return;
+        s_nlist = 0;
+        s_ncells = 0;
     }
     if (n > a.cap_points) {
         __syncthreads();
         cluster_frame_inplace(a, f, b, n, smem, &s_red);
         return;
     }
-
-    const int32_t cap = a.cap_points;
-    int2 *sxy = reinterpret_cast<int2 *>(smem);            // [cap] sorted coords
-    int32_t *parent = reinterpret_cast<int32_t *>(sxy + cap);  // [cap] by original index
-    int32_t *cstart = parent + cap;                          // [cap_cells + 1]
-    uint16_t *sid = reinterpret_cast<uint16_t *>(cstart + a.cap_cells + 1);  // [cap]
-    uint8_t *score = reinterpret_cast<uint8_t *>(sid + cap);  // [cap] core flag, sorted
-    uint8_t *kindo = score + cap;                             // [cap] kind, original order
 
     const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
     const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
@@ -363,7 +409,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     {
         int xmn = INT_MAX, ymn = INT_MAX, xmx = INT_MIN, ymx = INT_MIN;
         for (int32_t i = tid; i < n; i += kThreads) {
-            int2 p = P[i];
+            const int2 p = P[i];
             xmn = min(xmn, p.x);
             ymn = min(ymn, p.y);
             xmx = max(xmx, p.x);
@@ -374,7 +420,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         xmx = wave_max(xmx);
         ymx = wave_max(ymx);
         __syncthreads();  // s_bbox initialised
-        if ((tid & 63) == 0) {
+        if (lane == 0) {
             atomicMin(&s_bbox[0], xmn);
             atomicMin(&s_bbox[1], ymn);
             atomicMax(&s_bbox[2], xmx);
@@ -382,28 +428,59 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         }
         __syncthreads();
     }
+    const int32_t x0 = s_bbox[0], y0 = s_bbox[1];
+    const uint32_t wx = (uint32_t)(s_bbox[2] - x0), wy = (uint32_t)(s_bbox[3] - y0);
+    if (wx > 0xffffu || wy > 0xffffu) {  // extent beyond 16 bits: keep the data off chip
+        cluster_frame_inplace(a, f, b, n, smem, &s_red);
+        return;
+    }
+
+    // LDS layout (cap points, cc cells):
+    //   pxy    uint32[cap]   packed relative coordinates, sorted by cell
+    //   parent int32 [cap]   union-find forest, then labels (original index)
+    //   cell   uint32[cc+1]  first sorted position (low 16 bits) | smallest
+    //                        core index in the cell, 0xffff if none (high 16)
+    //   sid    uint16[cap]   original index of each sorted position
+    //   list   uint16[cap]   work list
+    //   clist  uint16[cc]    cells that hold a core
+    //   score  uint8 [cap]   core flag by sorted position
+    //   kindo  uint8 [cap]   kind by original index
+    const int32_t cap = a.cap_points, cc = a.cap_cells;
+    uint32_t *pxy = reinterpret_cast<uint32_t *>(smem);
+    int32_t *parent = reinterpret_cast<int32_t *>(pxy + cap);
+    uint32_t *cell = reinterpret_cast<uint32_t *>(parent + cap);
+    uint16_t *sid = reinterpret_cast<uint16_t *>(cell + cc + 1);
+    uint16_t *list = sid + cap;
+    uint16_t *clist = list + cap;
+    uint8_t *score = reinterpret_cast<uint8_t *>(clist + cc);
+    uint8_t *kindo = score + cap;
+    auto cstart = [cell](int32_t c) -> int32_t { return (int32_t)(cell[c] & 0xffffu); };
+    auto cnode = [cell](int32_t c) -> uint32_t { return cell[c] >> 16; };
 
     // 2. cell grid (every thread derives the same values)
     Grid g;
     {
-        g.x0 = s_bbox[0];
-        g.y0 = s_bbox[1];
-        const uint32_t wx = (uint32_t)(s_bbox[2] - s_bbox[0]);
-        const uint32_t wy = (uint32_t)(s_bbox[3] - s_bbox[1]);
         uint32_t side = (uint32_t)a.cell_side;
-        uint64_t ncx = wx / side + 1, ncy = wy / side + 1;
-        while (ncx * ncy > (uint64_t)a.cap_cells) {
+        uint32_t ncx = wx / side + 1, ncy = wy / side + 1;
+        while ((uint64_t)ncx * ncy > (uint64_t)cc) {
             side *= 2u;
             ncx = wx / side + 1;
             ncy = wy / side + 1;
         }
         g.side = (int32_t)side;
+        g.inv_side = 1.0f / (float)side;
         g.ncx = (int32_t)ncx;
         g.ncy = (int32_t)ncy;
         g.ncell = g.ncx * g.ncy;
         g.dense_ok = side == (uint32_t)a.cell_side;
-        g.reach = r.e == 0 ? 0 : 1 + (r.e - 1) / g.side;
-        if (g.reach > 7) g.reach = 7;  // side >= s >= E/2 when E >= 2, so reach <= 2
+        // side >= floor(E / sqrt 2) keeps reach <= 2 for every E
+        g.reach = r.e == 0 ? 0 : min(1 + (r.e - 1) / g.side, 7);
+        g.dxmax = s_dxmax;
+    }
+
+    // 3. counting sort by cell
+    for (int32_t c = tid; c <= g.ncell; c += kThreads) cell[c] = 0;
+    if (tid == 0) {
         for (int dy = 0; dy <= g.reach; ++dy) {
             const int64_t gy = cell_gap(dy, g.side);
             int dx = g.reach;
@@ -412,16 +489,29 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
                 if (gx * gx + gy * gy <= (int64_t)r.e2) break;
                 --dx;
             }
-            g.dxmax[dy] = dx;  // dx = 0 always qualifies for the rows kept below
+            s_dxmax[dy] = dx;
         }
+        // forward half of the neighbour-cell stencil (cells after this one in
+        // row-major order): adjacent cells in table 0, the rest in table 1
+        int k[2] = {0, 0};
+        for (int dy = 0; dy <= g.reach; ++dy)
+            for (int dx = (dy == 0 ? 1 : -s_dxmax[dy]); dx <= s_dxmax[dy]; ++dx) {
+                const int t = (dx >= -1 && dx <= 1 && dy <= 1) ? 0 : 1;
+                if (k[t] < kMaxOffsets) {
+                    s_odx[t][k[t]] = dx;
+                    s_ody[t][k[t]] = dy;
+                    ++k[t];
+                }
+            }
+        s_noff[0] = k[0];
+        s_noff[1] = k[1];
     }
-
-    // 3. counting sort by cell
-    for (int32_t c = tid; c <= g.ncell; c += kThreads) cstart[c] = 0;
     __syncthreads();
     for (int32_t i = tid; i < n; i += kThreads) {
-        const int2 c = cell_of(P[i], g);
-        parent[i] = atomicAdd(&cstart[c.y * g.ncx + c.x], 1);  // rank within cell
+        const int2 p = P[i];
+        const uint32_t v = (uint32_t)(p.x - x0) | ((uint32_t)(p.y - y0) << 16);
+        int32_t cx, cy;
+        list[i] = (uint16_t)atomicAdd(&cell[cell_id(v, g, &cx, &cy)], 1u);  // rank in cell
     }
     __syncthreads();
     {
@@ -429,138 +519,233 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         const int32_t c0 = min(tid * chunk, g.ncell);
         const int32_t c1 = min(c0 + chunk, g.ncell);
         int sum = 0;
-        for (int32_t c = c0; c < c1; ++c) sum += cstart[c];
+        for (int32_t c = c0; c < c1; ++c) sum += (int)cell[c];
         int run = block_exclusive_scan(sum, s_wave);
         for (int32_t c = c0; c < c1; ++c) {
-            const int v = cstart[c];
-            cstart[c] = run;
+            const int v = (int)cell[c];
+            cell[c] = (uint32_t)run | 0xffff0000u;
             run += v;
         }
-        if (tid == kThreads - 1) cstart[g.ncell] = run;
+        if (tid == kThreads - 1) cell[g.ncell] = (uint32_t)run | 0xffff0000u;
     }
     __syncthreads();
     for (int32_t i = tid; i < n; i += kThreads) {
         const int2 p = P[i];
-        const int2 c = cell_of(p, g);
-        const int32_t pos = cstart[c.y * g.ncx + c.x] + parent[i];
-        sxy[pos] = p;
+        const uint32_t v = (uint32_t)(p.x - x0) | ((uint32_t)(p.y - y0) << 16);
+        int32_t cx, cy;
+        const int32_t pos = cstart(cell_id(v, g, &cx, &cy)) + list[i];
+        pxy[pos] = v;
         sid[pos] = (uint16_t)i;
     }
     __syncthreads();
 
-    // 4. neighbour counts -> core flags
-    for (int32_t p = tid; p < n; p += kThreads) {
-        const int2 pp = sxy[p];
-        const int2 c = cell_of(pp, g);
-        const int32_t own = c.y * g.ncx + c.x;
-        int32_t cnt = 0;
-        if (g.dense_ok) cnt = cstart[own + 1] - cstart[own];
-        if (cnt < a.min_pts) {
-            cnt = 0;
-            for (int dy = -g.reach; dy <= g.reach && cnt < a.min_pts; ++dy) {
-                const int32_t cy = c.y + dy;
-                if (cy < 0 || cy >= g.ncy) continue;
-                const int dxm = g.dxmax[dy < 0 ? -dy : dy];
-                const int32_t cx0 = max(c.x - dxm, 0), cx1 = min(c.x + dxm, g.ncx - 1);
-                const int32_t q0 = cstart[cy * g.ncx + cx0], q1 = cstart[cy * g.ncx + cx1 + 1];
-                for (int32_t q = q0; q < q1; ++q) {
-                    cnt += within(pp, sxy[q], r) ? 1 : 0;
-                    if (cnt >= a.min_pts) break;
-                }
-            }
+    // 4a. a cell holding >= min_pts points is all core; list the other points
+    for (int32_t p0 = tid - lane; p0 < n; p0 += kThreads) {
+        const int32_t p = p0 + lane;
+        bool need = false;
+        if (p < n) {
+            int32_t cx, cy;
+            const int32_t c = cell_id(pxy[p], g, &cx, &cy);
+            const bool dense = g.dense_ok && cstart(c + 1) - cstart(c) >= a.min_pts;
+            score[p] = dense ? 1 : 0;
+            need = !dense;
         }
-        const bool core = cnt >= a.min_pts;
-        score[p] = core ? 1 : 0;
-        kindo[sid[p]] = core ? 2 : 0;
+        wave_append(need, (uint16_t)p, list, &s_nlist);
     }
-    for (int32_t i = tid; i < n; i += kThreads) parent[i] = i;
+    __syncthreads();
+    // 4b. count the listed points' neighbours, nearest rows first, stopping
+    //     at min_pts
+    {
+        const int32_t nl = s_nlist;
+        for (int32_t j = tid; j < nl; j += kThreads) {
+            const int32_t p = list[j];
+            const uint32_t v = pxy[p];
+            int32_t cx, cy;
+            cell_id(v, g, &cx, &cy);
+            int32_t cnt = 0;
+            for (int k = 0; k <= 2 * g.reach && cnt < a.min_pts; ++k) {
+                const int dy = (k & 1) ? -((k + 1) >> 1) : (k >> 1);  // 0, -1, 1, -2, 2, ...
+                const int32_t ry = cy + dy;
+                if (ry < 0 || ry >= g.ncy) continue;
+                const int dxm = g.dxmax[dy < 0 ? -dy : dy];
+                const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
+                cnt += count_span(pxy, cstart(ry * g.ncx + rx0), cstart(ry * g.ncx + rx1 + 1), v, r,
+                                  a.min_pts - cnt);
+            }
+            if (cnt >= a.min_pts) score[p] = 1;
+        }
+    }
     __syncthreads();
 
-    // 5. union-find over core points
+    // 5. kinds of cores, forest roots, and each cell's smallest core index
+    for (int32_t p = tid; p < n; p += kThreads) {
+        parent[p] = p;
+        const bool core = score[p];
+        kindo[sid[p]] = core ? 2 : 0;
+        if (core) {
+            int32_t cx, cy;
+            const int32_t c = cell_id(pxy[p], g, &cx, &cy);
+            atomicMin(&cell[c], (cell[c] & 0xffffu) | ((uint32_t)sid[p] << 16));
+        }
+    }
+    if (tid == 0) s_nlist = 0;
+    __syncthreads();
+    for (int32_t c0 = tid - lane; c0 < g.ncell; c0 += kThreads) {
+        const int32_t c = c0 + lane;
+        wave_append(c < g.ncell && cnode(c) != kNone, (uint16_t)c, clist, &s_ncells);
+    }
+    __syncthreads();
+
+    // 6. union-find over core points (the smaller index always becomes the root)
+    if (g.dense_ok) {
+        // All cores of a cell are neighbours, so a cell's cores form one node
+        // (its smallest core index).  Two nodes are joined when some core pair
+        // across the cells is within eps.  Adjacent cells go first; by the
+        // second pass most farther pairs are already in one tree.
+        const int32_t ncl = s_ncells;
+        for (int pass = 0; pass < 2; ++pass) {
+            const int noff = s_noff[pass];
+            for (int32_t item = tid; item < ncl * noff; item += kThreads) {
+                const int32_t j = item / noff;
+                const int o = item - j * noff;
+                const int32_t ca = clist[j];
+                const int32_t ay = ca / g.ncx, ax = ca - ay * g.ncx;
+                const int32_t bx = ax + s_odx[pass][o], by = ay + s_ody[pass][o];
+                if (bx < 0 || bx >= g.ncx || by >= g.ncy) continue;
+                const int32_t cb = by * g.ncx + bx;
+                const uint32_t nb = cnode(cb);
+                if (nb == kNone) continue;
+                const uint32_t na = cnode(ca);
+                if (uf_find<kGroup>(parent, (int32_t)na) == uf_find<kGroup>(parent, (int32_t)nb)) continue;
+                // B's rectangle, to skip points of A that cannot reach it
+                const int32_t bx0 = bx * g.side, bx1 = bx0 + g.side - 1;
+                const int32_t by0 = by * g.side, by1 = by0 + g.side - 1;
+                const int32_t a0 = cstart(ca), a1 = cstart(ca + 1);
+                const int32_t b0 = cstart(cb), b1 = cstart(cb + 1);
+                bool hit = false;
+                for (int32_t qa = a0; qa < a1 && !hit; ++qa) {
+                    if (!score[qa]) continue;
+                    const uint32_t va = pxy[qa];
+                    const int32_t ddx = min(max(max(bx0 - pk_x(va), pk_x(va) - bx1), 0), r.e1);
+                    const int32_t ddy = min(max(max(by0 - pk_y(va), pk_y(va) - by1), 0), r.e1);
+                    if (__mul24(ddx, ddx) + __mul24(ddy, ddy) > r.e2) continue;
+                    for (int32_t qb = b0; qb < b1; ++qb) {
+                        if (score[qb] && sq_dist_pk(va, pxy[qb], r.e1) <= r.e2) {
+                            hit = true;
+                            break;
+                        }
+                    }
+                }
+                if (hit) uf_unite<kGroup>(parent, (int32_t)na, (int32_t)nb);
+            }
+            __syncthreads();
+        }
+    } else {
+        // coarsened grid: point-level unions (each pair once: the later point
+        // of a cell, or the point in the earlier cell, does the work)
+        for (int32_t p = tid; p < n; p += kThreads) {
+            if (!score[p]) continue;
+            const uint32_t v = pxy[p];
+            const int32_t op = sid[p];
+            int32_t cx, cy;
+            const int32_t own = cell_id(v, g, &cx, &cy);
+            for (int32_t q = cstart(own); q < p; ++q)
+                if (score[q] && sq_dist_pk(v, pxy[q], r.e1) <= r.e2) uf_unite<kGroup>(parent, op, sid[q]);
+            for (int dy = 0; dy <= g.reach; ++dy) {
+                const int32_t ry = cy + dy;
+                if (ry >= g.ncy) break;
+                const int dxm = g.dxmax[dy];
+                const int32_t rx0 = dy == 0 ? cx + 1 : max(cx - dxm, 0);
+                const int32_t rx1 = min(cx + dxm, g.ncx - 1);
+                if (rx0 > rx1) continue;
+                const int32_t q1 = cstart(ry * g.ncx + rx1 + 1);
+                for (int32_t q = cstart(ry * g.ncx + rx0); q < q1; ++q)
+                    if (score[q] && sq_dist_pk(v, pxy[q], r.e1) <= r.e2) uf_unite<kGroup>(parent, op, sid[q]);
+            }
+        }
+        __syncthreads();
+    }
+
+    // 7. every core's label is its tree's root (read-only walks; each thread
+    //    writes only roots), and roots are counted once
+    int roots = 0;
     for (int32_t p = tid; p < n; p += kThreads) {
         if (!score[p]) continue;
-        const int2 pp = sxy[p];
-        const int32_t op = sid[p];
-        const int2 c = cell_of(pp, g);
-        const int32_t own = c.y * g.ncx + c.x;
-        // same cell
+        const int32_t o = sid[p];
+        int32_t node = o;
         if (g.dense_ok) {
-            int32_t q = cstart[own];
-            while (!score[q]) ++q;  // p itself is core, so this stops by p
-            if (q != p) uf_unite<kGroup>(parent, op, sid[q]);
-        } else {
-            for (int32_t q = cstart[own]; q < p; ++q)
-                if (score[q] && within(pp, sxy[q], r)) uf_unite<kGroup>(parent, op, sid[q]);
+            int32_t cx, cy;
+            node = (int32_t)cnode(cell_id(pxy[p], g, &cx, &cy));
         }
-        // cells after this one in row-major order
-        for (int dy = 0; dy <= g.reach; ++dy) {
-            const int32_t cy = c.y + dy;
-            if (cy >= g.ncy) break;
-            const int dxm = g.dxmax[dy];
-            const int32_t cx0 = dy == 0 ? c.x + 1 : max(c.x - dxm, 0);
-            const int32_t cx1 = min(c.x + dxm, g.ncx - 1);
-            for (int32_t cx = cx0; cx <= cx1; ++cx) {
-                const int32_t cc = cy * g.ncx + cx;
-                const int32_t q0 = cstart[cc], q1 = cstart[cc + 1];
-                for (int32_t q = q0; q < q1; ++q) {
-                    if (score[q] && within(pp, sxy[q], r)) {
-                        uf_unite<kGroup>(parent, op, sid[q]);
-                        if (g.dense_ok) break;  // the cell's cores are already one tree
+        const int32_t root = uf_root<kGroup>(parent, node);
+        st_rlx<kGroup>(parent + o, root);
+        roots += root == o;
+    }
+    __syncthreads();
+
+    // 8. border points: nearest core, ties by smaller (y, x)
+    for (int32_t p0 = tid - lane; p0 < n; p0 += kThreads) {
+        const int32_t p = p0 + lane;
+        wave_append(p < n && !score[p], (uint16_t)p, list, &s_nlist);
+    }
+    __syncthreads();
+    {
+        const int32_t nl = s_nlist;
+        for (int32_t j = tid; j < nl; j += kThreads) {
+            const int32_t p = list[j];
+            const uint32_t v = pxy[p];
+            const int32_t vx = pk_x(v), vy = pk_y(v);
+            int32_t cx, cy;
+            cell_id(v, g, &cx, &cy);
+            int32_t best = -1, best_d2 = 0;
+            uint32_t bestv = 0;
+            for (int dy = -g.reach; dy <= g.reach; ++dy) {
+                const int32_t ry = cy + dy;
+                if (ry < 0 || ry >= g.ncy) continue;
+                const int32_t y0c = ry * g.side;
+                const int32_t ddy = min(max(max(y0c - vy, vy - (y0c + g.side - 1)), 0), r.e1);
+                const int dxm = g.dxmax[dy < 0 ? -dy : dy];
+                const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
+                for (int32_t rx = rx0; rx <= rx1; ++rx) {
+                    const int32_t c = ry * g.ncx + rx;
+                    if (cnode(c) == kNone) continue;  // no core in this cell
+                    const int32_t x0c = rx * g.side;
+                    const int32_t ddx = min(max(max(x0c - vx, vx - (x0c + g.side - 1)), 0), r.e1);
+                    if (__mul24(ddx, ddx) + __mul24(ddy, ddy) > r.e2) continue;  // cell out of reach
+                    const int32_t q1 = cstart(c + 1);
+                    for (int32_t q = cstart(c); q < q1; ++q) {
+                        if (!score[q]) continue;
+                        const uint32_t w = pxy[q];
+                        const int32_t d2 = sq_dist_pk(v, w, r.e1);
+                        if (d2 > r.e2) continue;
+                        bool better = best < 0;
+                        if (!better) {
+                            if (d2 != best_d2) better = d2 < best_d2;
+                            else if (pk_y(w) != pk_y(bestv)) better = pk_y(w) < pk_y(bestv);
+                            else better = pk_x(w) < pk_x(bestv);
+                        }
+                        if (better) {
+                            best = q;
+                            best_d2 = d2;
+                            bestv = w;
+                        }
                     }
                 }
             }
-        }
-    }
-    __syncthreads();
-
-    // 6. flatten the core forest; count roots
-    int roots = 0;
-    for (int32_t i = tid; i < n; i += kThreads) {
-        if (kindo[i] != 2) continue;
-        const int32_t root = uf_root<kGroup>(parent, i);
-        st_rlx<kGroup>(parent + i, root);
-        roots += root == i;
-    }
-    __syncthreads();
-
-    // 7. border points: nearest core, ties by (y, x)
-    for (int32_t p = tid; p < n; p += kThreads) {
-        if (score[p]) continue;
-        const int2 pp = sxy[p];
-        const int2 c = cell_of(pp, g);
-        int32_t best = -1, best_d2 = 0;
-        int2 bestp = make_int2(0, 0);
-        for (int dy = -g.reach; dy <= g.reach; ++dy) {
-            const int32_t cy = c.y + dy;
-            if (cy < 0 || cy >= g.ncy) continue;
-            const int dxm = g.dxmax[dy < 0 ? -dy : dy];
-            const int32_t cx0 = max(c.x - dxm, 0), cx1 = min(c.x + dxm, g.ncx - 1);
-            const int32_t q0 = cstart[cy * g.ncx + cx0], q1 = cstart[cy * g.ncx + cx1 + 1];
-            for (int32_t q = q0; q < q1; ++q) {
-                if (!score[q]) continue;
-                const int2 qq = sxy[q];
-                const int32_t d2 = sq_dist_clamped(pp, qq, r);
-                if (d2 > r.e2) continue;
-                if (best < 0 || better_core(d2, qq, best_d2, bestp)) {
-                    best = q;
-                    best_d2 = d2;
-                    bestp = qq;
-                }
+            const int32_t o = sid[p];
+            if (best >= 0) {
+                parent[o] = parent[sid[best]];
+                kindo[o] = 1;
+            } else {
+                parent[o] = -1;
             }
-        }
-        const int32_t o = sid[p];
-        if (best >= 0) {
-            parent[o] = parent[sid[best]];
-            kindo[o] = 1;
-        } else {
-            parent[o] = -1;
         }
     }
     roots = wave_sum(roots);
-    if ((tid & 63) == 0) atomicAdd(&s_red, roots);
+    if (lane == 0) atomicAdd(&s_red, roots);
     __syncthreads();
 
-    // 8. outputs in original order (coalesced)
+    // 9. outputs in original order (coalesced)
     for (int32_t i = tid; i < n; i += kThreads) {
         a.labels[b + i] = parent[i];
         a.kind[b + i] = kindo[i];
@@ -571,7 +756,9 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
 }  // namespace
 
 size_t cluster_lds_bytes(int32_t cap_points, int32_t cap_cells) {
-    size_t bytes = (size_t)cap_points * (8 + 4 + 2 + 1 + 1) + ((size_t)cap_cells + 1) * 4;
+    // per point: packed coords 4, parent 4, sid 2, list 2, core 1, kind 1;
+    // per cell: start|node 4, cell list 2
+    size_t bytes = (size_t)cap_points * 14 + (size_t)cap_cells * 6 + 4;
     const size_t inplace = (size_t)kTile * (8 + 1);
     if (bytes < inplace) bytes = inplace;
     return (bytes + 15) & ~(size_t)15;
@@ -579,9 +766,9 @@ size_t cluster_lds_bytes(int32_t cap_points, int32_t cap_cells) {
 
 int32_t cluster_max_cap_points(size_t lds_limit) {
     // reserve room for the static shared variables and a 4096-entry cell table
-    const size_t reserve = 1024 + 4097 * 4;
+    const size_t reserve = 1024 + 4096 * 6 + 4;
     if (lds_limit <= reserve) return 0;
-    size_t cap = (lds_limit - reserve) / 16;
+    size_t cap = (lds_limit - reserve) / 14;
     if (cap > 65535) cap = 65535;  // original indices are kept as uint16
     return (int32_t)cap;
 }
