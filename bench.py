@@ -127,7 +127,7 @@ def main():
         flock.cluster_frames(dxy, doff, w.eps_px, w.min_pts, max_fp, out=(labels, kind, ncl),
                              stream=stream)
         flock.density_frames(dxy, doff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
-                             out=dens, stream=stream)
+                             max_fp, out=dens, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -143,7 +143,7 @@ def main():
                              stream=stream)
         ev[k][1].record(stream)
         flock.density_frames(dxy, doff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
-                             out=dens, stream=stream)
+                             max_fp, out=dens, stream=stream)
         ev[k][2].record(stream)
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0

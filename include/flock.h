@@ -116,6 +116,9 @@ size_t cluster_frames_workspace(int32_t n_frames, int32_t total, int32_t max_fra
  * 2^-10); an empty frame gives exact zeros.
  *
  * Arguments:
+ *   max_frame_points      host: an upper bound on the birds in any one frame,
+ *                         or 0 if unknown (a planning hint; every value >= 0
+ *                         gives the same result).
  *   width_px, height_px   frame extent, >= 1.
  *   grid_w, grid_h        grid size, 1 .. 4096 each.
  *   sigma_px              bandwidth, finite, > 0.
@@ -125,9 +128,9 @@ size_t cluster_frames_workspace(int32_t n_frames, int32_t total, int32_t max_fra
  * The result is deterministic (fixed summation order).
  */
 flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
-                            int32_t total, int32_t width_px, int32_t height_px, int32_t grid_w,
-                            int32_t grid_h, float sigma_px, float *density, void *workspace,
-                            size_t workspace_bytes, void *stream);
+                            int32_t total, int32_t max_frame_points, int32_t width_px,
+                            int32_t height_px, int32_t grid_w, int32_t grid_h, float sigma_px,
+                            float *density, void *workspace, size_t workspace_bytes, void *stream);
 
 /* Bytes of workspace density_frames needs for this batch shape (may be 0). */
 size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h);

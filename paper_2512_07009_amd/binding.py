@@ -44,7 +44,7 @@ def lib() -> ctypes.CDLL:
         p, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
         L.cluster_frames.argtypes = [p, p, i32, i32, i32, i32, i32, p, p, p, p, sz, p]
         L.cluster_frames.restype = i32
-        L.density_frames.argtypes = [p, p, i32, i32, i32, i32, i32, i32, ctypes.c_float, p, p, sz, p]
+        L.density_frames.argtypes = [p, p, i32, i32, i32, i32, i32, i32, i32, ctypes.c_float, p, p, sz, p]
         L.density_frames.restype = i32
         L.cluster_frames_workspace.argtypes = [i32, i32, i32]
         L.cluster_frames_workspace.restype = sz
@@ -122,8 +122,12 @@ def cluster_frames(xy: torch.Tensor, offsets: torch.Tensor, eps_px: float, min_p
 
 
 def density_frames(xy: torch.Tensor, offsets: torch.Tensor, width_px: int, height_px: int,
-                   grid_w: int, grid_h: int, sigma_px: float, out=None, stream=None):
-    """Gaussian density grid of every frame: float32[F, grid_h, grid_w] (birds / px^2)."""
+                   grid_w: int, grid_h: int, sigma_px: float, max_frame_points: int = 0, out=None,
+                   stream=None):
+    """Gaussian density grid of every frame: float32[F, grid_h, grid_w] (birds / px^2).
+
+    max_frame_points: an upper bound on birds per frame, or 0 (a planning hint).
+    """
     F, T = _batch(xy, offsets)
     dev = xy.device
     dens = out if out is not None else torch.empty((max(F, 0), grid_h, grid_w), dtype=torch.float32,
@@ -131,7 +135,8 @@ def density_frames(xy: torch.Tensor, offsets: torch.Tensor, width_px: int, heigh
     ws_bytes = lib().density_frames_workspace(F, T, int(grid_w), int(grid_h))
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
     with torch.cuda.device(dev):
-        st = lib().density_frames(_ptr(xy), _ptr(offsets), F, T, int(width_px), int(height_px),
+        st = lib().density_frames(_ptr(xy), _ptr(offsets), F, T, int(max_frame_points),
+                                  int(width_px), int(height_px),
                                   int(grid_w), int(grid_h), float(sigma_px), _ptr(dens), _ptr(ws),
                                   ws_bytes, _stream(stream))
     _check(st)

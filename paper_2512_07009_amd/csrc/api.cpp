@@ -201,7 +201,8 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
 }
 
 flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
-                            int32_t width_px, int32_t height_px, int32_t grid_w, int32_t grid_h,
+                            int32_t max_frame_points, int32_t width_px, int32_t height_px,
+                            int32_t grid_w, int32_t grid_h,
                             float sigma_px, float *density, void *workspace, size_t workspace_bytes,
                             void *stream) {
     g_error.clear();
@@ -209,6 +210,7 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     (void)workspace_bytes;
     if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
     if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
+    if (max_frame_points < 0) return fail(FLOCK_EINVAL, "max_frame_points = %d < 0", max_frame_points);
     if (width_px < 1 || height_px < 1)
         return fail(FLOCK_EINVAL, "frame extent %d x %d px must be >= 1", width_px, height_px);
     if (grid_w < 1 || grid_h < 1 || grid_w > 4096 || grid_h > 4096)
@@ -236,6 +238,7 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     a.offsets = offsets;
     a.n_frames = n_frames;
     a.total = total;
+    a.max_frame_points = max_frame_points;
     a.width_px = width_px;
     a.height_px = height_px;
     a.grid_w = grid_w;
@@ -245,7 +248,7 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     const flock::DensityPlan plan = flock::plan_density(a, dev->n_cus);
     const long long blocks = (long long)n_frames * plan.regions_y * plan.regions_x;
     if (blocks > 0x7fffffffLL) return fail(FLOCK_EUNSUPPORTED, "batch too large for one launch");
-    hipError_t err = flock::launch_density(a, plan, s);
+    hipError_t err = flock::launch_density(a, plan, dev->lds_per_block, s);
     if (err != hipSuccess) return hip_fail(err, "density kernel launch");
     return FLOCK_OK;
 }

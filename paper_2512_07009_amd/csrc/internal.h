@@ -43,6 +43,7 @@ struct DensityArgs {
     const int32_t *offsets;
     int32_t n_frames;
     int32_t total;
+    int32_t max_frame_points; // bound used to size the per-frame sort (0: no sort)
     int32_t width_px, height_px;
     int32_t grid_w, grid_h;
     float sigma_px;
@@ -50,12 +51,13 @@ struct DensityArgs {
 };
 
 struct DensityPlan {
-    int tm;                   // 16-row gy tiles per workgroup region
-    int tnw;                  // 16-col gx tiles per wave (4 waves per region)
+    int rm;                   // 32-row gy tiles per workgroup region
+    int rn;                   // 32-column gx tiles per workgroup region
     int regions_y, regions_x; // regions per frame
 };
 
 DensityPlan plan_density(const DensityArgs &a, int n_cus);
-hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, hipStream_t stream);
+hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, size_t lds_limit,
+                          hipStream_t stream);
 
 }  // namespace flock

@@ -39,10 +39,10 @@ def _cluster(n_frames=1, total=4, max_fp=0, eps_q=640, min_pts=4, xy=FAKE, offse
                                         labels, kind, ncl, None, 0, None)
 
 
-def _density(n_frames=1, total=4, w=1920, h=1080, gx=128, gy=72, sigma=30.0, xy=FAKE,
+def _density(n_frames=1, total=4, max_fp=0, w=1920, h=1080, gx=128, gy=72, sigma=30.0, xy=FAKE,
              offsets=FAKE, out=FAKE):
-    return binding.lib().density_frames(xy, offsets, n_frames, total, w, h, gx, gy, sigma, out,
-                                        None, 0, None)
+    return binding.lib().density_frames(xy, offsets, n_frames, total, max_fp, w, h, gx, gy, sigma,
+                                        out, None, 0, None)
 
 
 @pytest.mark.parametrize("kwargs,needle", [
@@ -64,6 +64,7 @@ def test_cluster_rejects_bad_arguments(kwargs, needle):
 
 @pytest.mark.parametrize("kwargs,needle", [
     (dict(n_frames=-1), "n_frames"),
+    (dict(max_fp=-2), "max_frame_points"),
     (dict(w=0), "extent"),
     (dict(h=-3), "extent"),
     (dict(gx=0), "grid"),

@@ -36,9 +36,10 @@ def run_cluster(xy, off, eps_q, min_pts, max_fp=None):
     return labels.cpu().numpy(), kind.cpu().numpy(), ncl.cpu().numpy()
 
 
-def run_density(xy, off, w, h, gx, gy, sigma):
+def run_density(xy, off, w, h, gx, gy, sigma, max_fp=None):
     dxy, doff = dev_batch(xy, off)
-    d = flock.density_frames(dxy, doff, w, h, gx, gy, sigma)
+    d = flock.density_frames(dxy, doff, w, h, gx, gy, sigma,
+                             max_count(off) if max_fp is None else max_fp)
     torch.cuda.synchronize()
     return d.cpu().numpy()
 
@@ -209,6 +210,15 @@ def test_density_random_gpu(w, h, gx, gy, sigma):
     ref = oracle.density_frames(xy, off, w, h, gx, gy, sigma)
     worst = assert_density_close(got, ref, np.diff(off), sigma, tag=f"{gx}x{gy} sigma {sigma}")
     print(f"density {gx}x{gy} sigma {sigma}: worst rel err {worst:.2e}")
+
+
+@pytest.mark.parametrize("max_fp", [0, 50])
+def test_density_input_order_path_gpu(max_fp):
+    """Frames above max_frame_points (all of them for 0) keep their input order."""
+    xy, off = wl.random_batch(4242 + max_fp, 10, 300)
+    got = run_density(xy, off, 1920, 1080, 128, 72, 30.0, max_fp=max_fp)
+    ref = oracle.density_frames(xy, off, 1920, 1080, 128, 72, 30.0)
+    assert_density_close(got, ref, np.diff(off), 30.0, tag=f"max_fp {max_fp}")
 
 
 def test_density_single_bird_peak_gpu():
