@@ -3,10 +3,13 @@
 
 One step = cluster_frames + density_frames over one batch of synthetic frames
 (default: 64 frames x 2000 birds, 1920x1080 px, eps 40 px, minPts 4, density
-grid 128x72, sigma 30 px).  Inputs are resident in device memory before the
+grid 128x72, sigma 30 px).  The two calls are independent analytics of the
+same batch, so a step issues them on two streams (default priority) and joins;
+the same steps issued back to back on one stream are reported as
+sequential_frames_per_s.  Inputs are resident in device memory before the
 timed region; W warm-up steps, then K timed steps bracketed by device
 synchronisation.  Per-kernel durations come from HIP events recorded on the
-stream the kernels run on, inside the timed region.
+stream each kernel runs on, inside the timed region.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -96,6 +99,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=2.0,
                     help="target wall seconds for the oracle sample (all host cores)")
+    ap.add_argument("--calibrate-copy-mb", type=float, default=0,
+                    help="also run one plain device copy of this many MiB (counter scaling)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -123,33 +128,62 @@ def main():
     stream = torch.cuda.current_stream(dev)
     log(f"workload {w.name}: {F} frames, {T} birds, max {max_fp}/frame; {flock.version()}")
 
-    def step():
+    side = torch.cuda.Stream(dev)  # default priority
+
+    def run_pair(k, concurrent, evs=None):
+        """cluster_frames on `stream`, density_frames on `side` (or also on
+        `stream` when not concurrent), with the join back on `stream`."""
+        ds = side if concurrent else stream
+        if concurrent:
+            fork = torch.cuda.Event()
+            fork.record(stream)
+            side.wait_event(fork)
+        if evs is not None:
+            evs[0].record(stream)
         flock.cluster_frames(dxy, doff, w.eps_px, w.min_pts, max_fp, out=(labels, kind, ncl),
                              stream=stream)
+        if evs is not None:
+            evs[1].record(stream)
+            evs[2].record(ds)
         flock.density_frames(dxy, doff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
-                             max_fp, out=dens, stream=stream)
+                             max_fp, out=dens, stream=ds)
+        if evs is not None:
+            evs[3].record(ds)
+        if concurrent:
+            join = torch.cuda.Event()
+            join.record(side)
+            stream.wait_event(join)
 
-    for _ in range(args.warmup):
-        step()
+    def timed(concurrent, K):
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+        torch.cuda.synchronize(dev)
+        t0 = time.perf_counter()
+        for k in range(K):
+            run_pair(k, concurrent, evs[k])
+        torch.cuda.synchronize(dev)
+        wall = time.perf_counter() - t0
+        t_c = sum(e[0].elapsed_time(e[1]) for e in evs) / K * 1e-3   # s per launch
+        t_d = sum(e[2].elapsed_time(e[3]) for e in evs) / K * 1e-3
+        return wall, t_c, t_d
+
+    if args.calibrate_copy_mb > 0:
+        # a plain device copy of known size, for scaling HBM byte counters
+        nbytes = int(args.calibrate_copy_mb) << 20
+        src = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize(dev)
+        log(f"calibration copy: {nbytes} bytes read and written")
+        del src, dst
+
+    for k in range(args.warmup):
+        run_pair(k, True)
+        run_pair(k, False)
     torch.cuda.synchronize(dev)
 
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
-    torch.cuda.synchronize(dev)
-    t0 = time.perf_counter()
-    for k in range(K):
-        ev[k][0].record(stream)
-        flock.cluster_frames(dxy, doff, w.eps_px, w.min_pts, max_fp, out=(labels, kind, ncl),
-                             stream=stream)
-        ev[k][1].record(stream)
-        flock.density_frames(dxy, doff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
-                             max_fp, out=dens, stream=stream)
-        ev[k][2].record(stream)
-    torch.cuda.synchronize(dev)
-    wall = time.perf_counter() - t0
-
-    t_cluster = sum(e[0].elapsed_time(e[1]) for e in ev) / K * 1e-3   # s per launch
-    t_density = sum(e[1].elapsed_time(e[2]) for e in ev) / K * 1e-3
+    wall_seq, _, _ = timed(False, K)
+    wall, t_cluster, t_density = timed(True, K)
     ms_per_step = wall / K * 1e3
     value = F / (wall / K)
 
@@ -185,6 +219,7 @@ def main():
                    "frame_px": [w.width_px, w.height_px], "eps_px": w.eps_px, "min_pts": w.min_pts,
                    "grid": [w.grid_w, w.grid_h], "sigma_px": w.sigma_px, "parallelism": "single-gpu"},
         "birds_per_s": T / (wall / K),
+        "sequential_frames_per_s": F / (wall_seq / K),
         "roofline": roof,
         "kernels": {"cluster_frames": cl, "density_frames": de},
     }
