@@ -137,10 +137,14 @@ const char *flock_last_error(void) { return g_error.c_str(); }
 const char *flock_version(void) { return "flock 0.1.0 gfx950"; }
 
 size_t cluster_frames_workspace(int32_t n_frames, int32_t total, int32_t max_frame_points) {
-    (void)n_frames;
-    (void)total;
-    (void)max_frame_points;
-    return 0;
+    if (n_frames <= 0 || total <= 0 || max_frame_points < 0) return 0;
+    const DeviceInfo *dev = nullptr;
+    size_t lds = 160 * 1024;
+    if (device_info(&dev) == FLOCK_OK) lds = dev->lds_per_block;
+    g_error.clear();
+    const ClusterPlan plan = plan_cluster(max_frame_points, lds);
+    const bool big = max_frame_points == 0 || max_frame_points > plan.cap_points;
+    return big ? flock::cluster_big_workspace(n_frames, total) : 0;
 }
 
 size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h) {
@@ -156,8 +160,6 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
                             uint8_t *kind, int32_t *n_clusters, void *workspace, size_t workspace_bytes,
                             void *stream) {
     g_error.clear();
-    (void)workspace;
-    (void)workspace_bytes;
     if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
     if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
     if (max_frame_points < 0) return fail(FLOCK_EINVAL, "max_frame_points = %d < 0", max_frame_points);
@@ -182,6 +184,11 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     }
 
     const ClusterPlan plan = plan_cluster(max_frame_points, dev->lds_per_block);
+    const bool big = max_frame_points == 0 || max_frame_points > plan.cap_points;
+    const size_t ws_need = big ? flock::cluster_big_workspace(n_frames, total) : 0;
+    if (workspace && workspace_bytes < ws_need)
+        return fail(FLOCK_ENOMEM, "workspace of %zu bytes, %zu needed", workspace_bytes, ws_need);
+    if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
     flock::ClusterArgs a;
     a.xy = xy;
     a.offsets = offsets;
@@ -195,8 +202,23 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     a.labels = labels;
     a.kind = kind;
     a.n_clusters = n_clusters;
+    a.big_path = big ? 1 : 0;
     hipError_t err = flock::launch_cluster_resident(a, plan.lds_bytes, s);
     if (err != hipSuccess) return hip_fail(err, "cluster kernel launch");
+    if (big && total > 0) {
+        void *ws = workspace;
+        if (!ws) {
+            err = hipMallocAsync(&ws, ws_need, s);
+            if (err != hipSuccess) return fail(FLOCK_ENOMEM, "hipMallocAsync(%zu): %s", ws_need,
+                                               hipGetErrorString(err));
+        }
+        err = flock::launch_cluster_big(a, ws, s);
+        if (!workspace) {
+            const hipError_t ferr = hipFreeAsync(ws, s);
+            if (err == hipSuccess) err = ferr;
+        }
+        if (err != hipSuccess) return hip_fail(err, "large-frame cluster kernels");
+    }
     return FLOCK_OK;
 }
 

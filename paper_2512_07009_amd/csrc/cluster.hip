@@ -25,8 +25,10 @@
 //      ever hooked under a smaller index, so every component's final root is
 //      its smallest core index whatever the order of the atomic operations;
 //   5. flatten, nearest-core border assignment, coalesced output writes.
-// Frames with more points than the on-chip capacity take an in-place path
-// that keeps the union-find forest in the caller's labels array and runs
+// Frames with more points than the on-chip capacity go to the multi-workgroup
+// path (cluster_big.hip) when the caller's plan provides its workspace;
+// otherwise, and for frames wider than 16-bit coordinates, an in-place path
+// keeps the union-find forest in the caller's labels array and runs
 // brute-force pair tests through LDS tiles (correct for any size, slow).
 //
 // All results are independent of the order of points within a cell, so the
@@ -35,150 +37,21 @@
 
 #include <climits>
 
+#include "cluster_common.h"
 #include "internal.h"
 
 namespace flock {
 namespace {
+
+using namespace cl;
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / 64;
 constexpr int kTile = 1024;  // points per LDS tile on the in-place path
 
 // ---------------------------------------------------------------------------
-// small helpers
-// ---------------------------------------------------------------------------
-
-template <int Scope>
-__device__ __forceinline__ int32_t ld_rlx(const int32_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, Scope);
-}
-template <int Scope>
-__device__ __forceinline__ void st_rlx(int32_t *p, int32_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, Scope);
-}
-
-// Root of x with path halving.  Invariant kept by every writer:
-// parent[x] <= x, and parent[x] is an ancestor of x.
-template <int Scope>
-__device__ int32_t uf_find(int32_t *parent, int32_t x) {
-    for (;;) {
-        int32_t p = ld_rlx<Scope>(parent + x);
-        if (p == x) return x;
-        int32_t gp = ld_rlx<Scope>(parent + p);
-        if (gp == p) return p;
-        st_rlx<Scope>(parent + x, gp);
-        x = gp;
-    }
-}
-
-// Root of x without writes (safe while other threads set parent[i] = root).
-template <int Scope>
-__device__ int32_t uf_root(const int32_t *parent, int32_t x) {
-    for (;;) {
-        int32_t p = ld_rlx<Scope>(parent + x);
-        if (p == x) return x;
-        x = p;
-    }
-}
-
-// Merge the trees of a and b, hooking the larger root under the smaller.
-template <int Scope>
-__device__ void uf_unite(int32_t *parent, int32_t a, int32_t b) {
-    for (;;) {
-        a = uf_find<Scope>(parent, a);
-        b = uf_find<Scope>(parent, b);
-        if (a == b) return;
-        if (a < b) {
-            int32_t t = a;
-            a = b;
-            b = t;
-        }
-        int32_t expected = a;
-        if (__hip_atomic_compare_exchange_strong(parent + a, &expected, b, __ATOMIC_RELAXED,
-                                                 __ATOMIC_RELAXED, Scope))
-            return;
-    }
-}
-
-// Exact neighbour test.  Per axis the distance is clamped to E + 1, which
-// cannot change the outcome and keeps dx^2 + dy^2 below 2^31 (E <= 32766).
-struct Radius {
-    int32_t e;       // E
-    int32_t e1;      // E + 1
-    int32_t e2;      // E^2
-};
-
-__device__ __forceinline__ int32_t clamp_abs(int32_t d, int32_t e1) {
-    d = d < 0 ? -d : d;
-    return d < e1 ? d : e1;
-}
-
-__device__ __forceinline__ int32_t sq_dist_clamped(int2 a, int2 b, const Radius &r) {
-    int32_t dx = clamp_abs(a.x - b.x, r.e1);
-    int32_t dy = clamp_abs(a.y - b.y, r.e1);
-    return __mul24(dx, dx) + __mul24(dy, dy);
-}
-
-__device__ __forceinline__ bool within(int2 a, int2 b, const Radius &r) {
-    return sq_dist_clamped(a, b, r) <= r.e2;
-}
-
-// true if core q beats the current best core for a border point:
-// key (d^2, y, x) ascending.
-__device__ __forceinline__ bool better_core(int32_t d2, int2 q, int32_t best_d2, int2 best) {
-    if (d2 != best_d2) return d2 < best_d2;
-    if (q.y != best.y) return q.y < best.y;
-    return q.x < best.x;
-}
-
-__device__ __forceinline__ int wave_sum(int v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
-}
-
-__device__ __forceinline__ int wave_min(int v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
-    return v;
-}
-
-__device__ __forceinline__ int wave_max(int v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
-    return v;
-}
-
-// Exclusive scan of one int per thread across the workgroup.
-__device__ int block_exclusive_scan(int v, int *wave_tot) {
-    const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    int inc = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        int t = __shfl_up(inc, o, 64);
-        if (lane >= o) inc += t;
-    }
-    if (lane == 63) wave_tot[wave] = inc;
-    __syncthreads();
-    int base = 0;
-    for (int w = 0; w < wave; ++w) base += wave_tot[w];
-    __syncthreads();
-    return base + inc - v;
-}
-
-// Smallest per-axis distance between points of two cells |d| cells apart.
-__device__ __forceinline__ int64_t cell_gap(int32_t d, int32_t side) {
-    d = d < 0 ? -d : d;
-    return d == 0 ? 0 : (int64_t)(d - 1) * side + 1;
-}
-
-// ---------------------------------------------------------------------------
 // In-place path for frames above the on-chip capacity
 // ---------------------------------------------------------------------------
-
-constexpr int kAgent = __HIP_MEMORY_SCOPE_AGENT;
-constexpr int kGroup = __HIP_MEMORY_SCOPE_WORKGROUP;
 
 __device__ void cluster_frame_inplace(const ClusterArgs &a, int f, int32_t b, int32_t n,
                                       unsigned char *smem, int *red) {
@@ -248,8 +121,7 @@ __device__ void cluster_frame_inplace(const ClusterArgs &a, int f, int32_t b, in
         const int32_t i = base + tid;
         const bool valid = i < n && knd[i] != 2;
         const int2 pi = i < n ? P[i] : make_int2(0, 0);
-        int32_t best = -1, best_d2 = 0;
-        int2 bestp = make_int2(0, 0);
+        int32_t best = -1, best_d2 = INT32_MAX, by = 0, bx = 0;
         for (int32_t t0 = 0; t0 < n; t0 += kTile) {
             const int32_t tn = min(kTile, n - t0);
             __syncthreads();
@@ -264,11 +136,11 @@ __device__ void cluster_frame_inplace(const ClusterArgs &a, int f, int32_t b, in
                     const int2 q = tile[j];
                     const int32_t d2 = sq_dist_clamped(pi, q, r);
                     if (d2 > r.e2) continue;
-                    if (best < 0 || better_core(d2, q, best_d2, bestp)) {
-                        best = t0 + j;
-                        best_d2 = d2;
-                        bestp = q;
-                    }
+                    const bool take = core_before(d2, q.y, q.x, best_d2, by, bx);
+                    best = take ? t0 + j : best;
+                    best_d2 = take ? d2 : best_d2;
+                    by = take ? q.y : by;
+                    bx = take ? q.x : bx;
                 }
             }
         }
@@ -397,6 +269,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         s_ncells = 0;
     }
     if (n > a.cap_points) {
+        if (a.big_path) return;  // the multi-workgroup path owns this frame
         __syncthreads();
         cluster_frame_inplace(a, f, b, n, smem, &s_red);
         return;
@@ -697,7 +570,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
             const int32_t vx = pk_x(v), vy = pk_y(v);
             int32_t cx, cy;
             cell_id(v, g, &cx, &cy);
-            int32_t best = -1, best_d2 = 0;
+            int32_t best = -1, best_d2 = INT32_MAX;
             uint32_t bestv = 0;
             for (int dy = -g.reach; dy <= g.reach; ++dy) {
                 const int32_t ry = cy + dy;
@@ -718,17 +591,11 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
                         const uint32_t w = pxy[q];
                         const int32_t d2 = sq_dist_pk(v, w, r.e1);
                         if (d2 > r.e2) continue;
-                        bool better = best < 0;
-                        if (!better) {
-                            if (d2 != best_d2) better = d2 < best_d2;
-                            else if (pk_y(w) != pk_y(bestv)) better = pk_y(w) < pk_y(bestv);
-                            else better = pk_x(w) < pk_x(bestv);
-                        }
-                        if (better) {
-                            best = q;
-                            best_d2 = d2;
-                            bestv = w;
-                        }
+                        // packed y<<16|x orders as (y, x)
+                        const bool take = (d2 < best_d2) | ((d2 == best_d2) & (w < bestv));
+                        best = take ? q : best;
+                        best_d2 = take ? d2 : best_d2;
+                        bestv = take ? w : bestv;
                     }
                 }
             }

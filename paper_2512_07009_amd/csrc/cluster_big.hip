@@ -1,0 +1,522 @@
+// cluster_big.hip - radius-neighbour clustering of frames too large for one
+// workgroup's LDS, spread over many workgroups.
+//
+// Same definition and conventions as cluster.hip (standard DBSCAN with the
+// nearest-core border rule and smallest-core-index labels; the paper's
+// clustering module, Section 2.3).  Frames with more points than the on-chip
+// capacity are processed by a sequence of grid-wide kernels over the whole
+// batch; each thread first finds its frame and skips frames that the on-chip
+// kernel handles.  All intermediate state is in the workspace:
+//
+//   frame records  int32[F][16]        bbox, cell grid, stencil
+//   rank           int32[T]            rank of a point within its cell
+//   spos, ssid     int2[T], int32[T]   points sorted by cell; frame-local index
+//   score          uint8[T]            core flag by sorted position
+//   cstart, cnode  int32[2T + 2F]      per frame f, entries 2*offsets[f] + 2f
+//                                      .. + ncell: cell start (and end
+//                                      sentinel); the cell's smallest core index
+//
+// A frame of n points gets a cell table of at most 2n + 1 cells (the cell
+// side doubles from the eps-diagonal side until the grid fits; the same-cell
+// shortcut holds only at the undoubled side), so the table never depends on
+// anything the host does not know.  The union-find forest lives in the
+// caller's labels array (frame-local indices), with agent-scope atomics.
+//
+// Kernels, in stream order: prep (one workgroup per frame: bounding box,
+// grid, clearing), hist (cell counts and ranks), scan (one workgroup per
+// frame), scatter, core (neighbour counts with early exit), nodes (each
+// cell's smallest core index), union (cell pairs, or point pairs when the
+// grid was coarsened), flatten (labels of cores, cluster counts), border.
+
+#include <climits>
+
+#include "cluster_common.h"
+#include "internal.h"
+
+namespace flock {
+namespace {
+
+using namespace cl;
+
+constexpr int kBlock = 256;
+constexpr int kScanThreads = 1024;
+constexpr int kRec = 16;  // int32 fields per frame record
+
+enum RecField {
+    kXmin = 0, kYmin, kXmax, kYmax, kSide, kNcx, kNcy, kDense, kReach, kDx0, kDx1, kDx2, kNcell, kBig
+};
+
+struct BigWs {
+    int32_t *rec;
+    int32_t *rank;
+    int2 *spos;
+    int32_t *ssid;
+    uint8_t *score;
+    int32_t *cstart;
+    int32_t *cnode;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+BigWs carve(void *base, int32_t n_frames, int32_t total) {
+    char *p = static_cast<char *>(base);
+    BigWs w;
+    const size_t cells = 2 * (size_t)total + 2 * (size_t)n_frames;
+    w.rec = reinterpret_cast<int32_t *>(p);
+    p += align256(sizeof(int32_t) * kRec * (size_t)n_frames);
+    w.rank = reinterpret_cast<int32_t *>(p);
+    p += align256(sizeof(int32_t) * (size_t)total);
+    w.spos = reinterpret_cast<int2 *>(p);
+    p += align256(sizeof(int2) * (size_t)total);
+    w.ssid = reinterpret_cast<int32_t *>(p);
+    p += align256(sizeof(int32_t) * (size_t)total);
+    w.score = reinterpret_cast<uint8_t *>(p);
+    p += align256((size_t)total);
+    w.cstart = reinterpret_cast<int32_t *>(p);
+    p += align256(sizeof(int32_t) * cells);
+    w.cnode = reinterpret_cast<int32_t *>(p);
+    return w;
+}
+
+__device__ __forceinline__ bool frame_ok(const ClusterArgs &a, int f, int32_t *b, int32_t *e) {
+    *b = a.offsets[f];
+    *e = a.offsets[f + 1];
+    return !(*b < 0 || *e < *b || *e > a.total);
+}
+
+// Frame holding global point index i: the last f with offsets[f] <= i.
+__device__ __forceinline__ int frame_of_point(const int32_t *offsets, int n_frames, int32_t i) {
+    int lo = 0, hi = n_frames - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (offsets[mid] <= i) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+// Frame owning cell-table entry c: the last f with 2 offsets[f] + 2 f <= c.
+__device__ __forceinline__ int frame_of_cell(const int32_t *offsets, int n_frames, int64_t c) {
+    int lo = 0, hi = n_frames - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (2 * (int64_t)offsets[mid] + 2 * (int64_t)mid <= c) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int64_t cell_base(const int32_t *offsets, int f) {
+    return 2 * (int64_t)offsets[f] + 2 * (int64_t)f;
+}
+
+struct BigGrid {
+    int32_t x0, y0, side, ncx, ncy, dense, reach, dx[3], ncell;
+};
+
+__device__ __forceinline__ BigGrid load_grid(const int32_t *rec) {
+    BigGrid g;
+    g.x0 = rec[kXmin];
+    g.y0 = rec[kYmin];
+    g.side = rec[kSide];
+    g.ncx = rec[kNcx];
+    g.ncy = rec[kNcy];
+    g.dense = rec[kDense];
+    g.reach = rec[kReach];
+    g.dx[0] = rec[kDx0];
+    g.dx[1] = rec[kDx1];
+    g.dx[2] = rec[kDx2];
+    g.ncell = rec[kNcell];
+    return g;
+}
+
+__device__ __forceinline__ void cell_xy(int2 p, const BigGrid &g, int32_t *cx, int32_t *cy) {
+    const uint32_t ux = (uint32_t)(p.x - g.x0), uy = (uint32_t)(p.y - g.y0);
+    *cx = min((int32_t)(ux / (uint32_t)g.side), g.ncx - 1);
+    *cy = min((int32_t)(uy / (uint32_t)g.side), g.ncy - 1);
+}
+
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kBlock) void big_prep(ClusterArgs a, BigWs w) {
+    __shared__ int s_bbox[4];
+    const int f = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+    int32_t *rec = w.rec + (size_t)f * kRec;
+    int32_t b, e;
+    const bool ok = frame_ok(a, f, &b, &e);
+    const int32_t n = ok ? e - b : 0;
+    if (!ok || n <= a.cap_points) {
+        if (tid == 0) rec[kBig] = 0;
+        return;
+    }
+    if (tid == 0) {
+        s_bbox[0] = INT_MAX;
+        s_bbox[1] = INT_MAX;
+        s_bbox[2] = INT_MIN;
+        s_bbox[3] = INT_MIN;
+    }
+    __syncthreads();
+    const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
+    int xmn = INT_MAX, ymn = INT_MAX, xmx = INT_MIN, ymx = INT_MIN;
+    for (int32_t i = tid; i < n; i += kBlock) {
+        const int2 p = P[i];
+        xmn = min(xmn, p.x);
+        ymn = min(ymn, p.y);
+        xmx = max(xmx, p.x);
+        ymx = max(ymx, p.y);
+    }
+    xmn = wave_min(xmn);
+    ymn = wave_min(ymn);
+    xmx = wave_max(xmx);
+    ymx = wave_max(ymx);
+    if (lane == 0) {
+        atomicMin(&s_bbox[0], xmn);
+        atomicMin(&s_bbox[1], ymn);
+        atomicMax(&s_bbox[2], xmx);
+        atomicMax(&s_bbox[3], ymx);
+    }
+    __syncthreads();
+    // grid: at most 2n + 1 cells
+    const uint32_t wx = (uint32_t)(s_bbox[2] - s_bbox[0]), wy = (uint32_t)(s_bbox[3] - s_bbox[1]);
+    uint32_t side = (uint32_t)a.cell_side;
+    uint64_t ncx = wx / side + 1, ncy = wy / side + 1;
+    while (ncx * ncy > 2 * (uint64_t)n + 1) {
+        side *= 2u;
+        ncx = wx / side + 1;
+        ncy = wy / side + 1;
+    }
+    const int32_t ncell = (int32_t)(ncx * ncy);
+    const int32_t reach = a.eps_q == 0 ? 0 : min(1 + (a.eps_q - 1) / (int32_t)side, 2);
+    if (tid == 0) {
+        rec[kXmin] = s_bbox[0];
+        rec[kYmin] = s_bbox[1];
+        rec[kXmax] = s_bbox[2];
+        rec[kYmax] = s_bbox[3];
+        rec[kSide] = (int32_t)side;
+        rec[kNcx] = (int32_t)ncx;
+        rec[kNcy] = (int32_t)ncy;
+        rec[kDense] = side == (uint32_t)a.cell_side;
+        rec[kReach] = reach;
+        const int64_t e2 = (int64_t)a.eps_q * a.eps_q;
+        for (int dy = 0; dy < 3; ++dy) {
+            int dx = 0;
+            if (dy <= reach) {
+                const int64_t gy = cell_gap(dy, (int32_t)side);
+                dx = reach;
+                while (dx > 0) {
+                    const int64_t gx = cell_gap(dx, (int32_t)side);
+                    if (gx * gx + gy * gy <= e2) break;
+                    --dx;
+                }
+            }
+            rec[kDx0 + dy] = dx;
+        }
+        rec[kNcell] = ncell;
+        rec[kBig] = 1;
+        if (a.n_clusters) a.n_clusters[f] = 0;
+    }
+    const int64_t base = cell_base(a.offsets, f);
+    for (int32_t c = tid; c <= ncell; c += kBlock) {
+        w.cstart[base + c] = 0;
+        w.cnode[base + c] = INT_MAX;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void big_hist(ClusterArgs a, BigWs w) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= a.total) return;
+    const int f = frame_of_point(a.offsets, a.n_frames, i);
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig]) return;
+    const BigGrid g = load_grid(rec);
+    const int2 p = reinterpret_cast<const int2 *>(a.xy)[i];
+    int32_t cx, cy;
+    cell_xy(p, g, &cx, &cy);
+    w.rank[i] = atomicAdd(&w.cstart[cell_base(a.offsets, f) + (int64_t)cy * g.ncx + cx], 1);
+}
+
+__global__ __launch_bounds__(kScanThreads) void big_scan(ClusterArgs a, BigWs w) {
+    __shared__ int s_wave[kScanThreads / 64];
+    const int f = blockIdx.x, tid = threadIdx.x;
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig]) return;
+    const int32_t ncell = rec[kNcell];
+    int32_t *cs = w.cstart + cell_base(a.offsets, f);
+    const int32_t chunk = (ncell + kScanThreads - 1) / kScanThreads;
+    const int32_t c0 = min(tid * chunk, ncell), c1 = min(c0 + chunk, ncell);
+    int sum = 0;
+    for (int32_t c = c0; c < c1; ++c) sum += cs[c];
+    int run = block_exclusive_scan(sum, s_wave);
+    for (int32_t c = c0; c < c1; ++c) {
+        const int v = cs[c];
+        cs[c] = run;
+        run += v;
+    }
+    if (tid == kScanThreads - 1) cs[ncell] = run;
+}
+
+__global__ __launch_bounds__(kBlock) void big_scatter(ClusterArgs a, BigWs w) {
+    const int32_t i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= a.total) return;
+    const int f = frame_of_point(a.offsets, a.n_frames, i);
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig]) return;
+    const BigGrid g = load_grid(rec);
+    const int2 p = reinterpret_cast<const int2 *>(a.xy)[i];
+    int32_t cx, cy;
+    cell_xy(p, g, &cx, &cy);
+    const int32_t b = a.offsets[f];
+    const int32_t pos = b + w.cstart[cell_base(a.offsets, f) + (int64_t)cy * g.ncx + cx] + w.rank[i];
+    w.spos[pos] = p;
+    w.ssid[pos] = i - b;
+}
+
+__global__ __launch_bounds__(kBlock) void big_core(ClusterArgs a, BigWs w) {
+    const int32_t p = blockIdx.x * kBlock + threadIdx.x;
+    if (p >= a.total) return;
+    const int f = frame_of_point(a.offsets, a.n_frames, p);
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig]) return;
+    const BigGrid g = load_grid(rec);
+    const int32_t b = a.offsets[f];
+    const int32_t *cs = w.cstart + cell_base(a.offsets, f);
+    const int2 *S = w.spos + b;
+    const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
+    const int2 v = w.spos[p];
+    int32_t cx, cy;
+    cell_xy(v, g, &cx, &cy);
+    const int32_t own = cy * g.ncx + cx;
+    int32_t cnt = g.dense ? cs[own + 1] - cs[own] : 0;
+    if (cnt < a.min_pts) {
+        cnt = 0;
+        for (int k = 0; k <= 2 * g.reach && cnt < a.min_pts; ++k) {
+            const int dy = (k & 1) ? -((k + 1) >> 1) : (k >> 1);  // 0, -1, 1, -2, 2
+            const int32_t ry = cy + dy;
+            if (ry < 0 || ry >= g.ncy) continue;
+            const int dxm = g.dx[dy < 0 ? -dy : dy];
+            const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
+            const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
+            for (int32_t q = cs[ry * g.ncx + rx0]; q < q1 && cnt < a.min_pts; ++q)
+                cnt += within(v, S[q], r) ? 1 : 0;
+        }
+    }
+    const bool core = cnt >= a.min_pts;
+    w.score[p] = core ? 1 : 0;
+    const int32_t o = w.ssid[p];
+    a.labels[b + o] = o;  // union-find parent
+    a.kind[b + o] = core ? 2 : 0;
+}
+
+__global__ __launch_bounds__(kBlock) void big_nodes(ClusterArgs a, BigWs w) {
+    const int32_t p = blockIdx.x * kBlock + threadIdx.x;
+    if (p >= a.total || !w.score[p]) return;
+    const int f = frame_of_point(a.offsets, a.n_frames, p);
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig] || !rec[kDense]) return;
+    const BigGrid g = load_grid(rec);
+    int32_t cx, cy;
+    cell_xy(w.spos[p], g, &cx, &cy);
+    atomicMin(&w.cnode[cell_base(a.offsets, f) + (int64_t)cy * g.ncx + cx], w.ssid[p]);
+}
+
+// k-th forward stencil offset (cells after this one in row-major order).
+__device__ __forceinline__ bool forward_offset(const BigGrid &g, int k, int *odx, int *ody) {
+    for (int dy = 0; dy <= g.reach; ++dy) {
+        const int lo = dy == 0 ? 1 : -g.dx[dy];
+        const int cnt = g.dx[dy] - lo + 1;
+        if (cnt > 0 && k < cnt) {
+            *odx = lo + k;
+            *ody = dy;
+            return true;
+        }
+        k -= max(cnt, 0);
+    }
+    return false;
+}
+
+constexpr int kMaxForward = 12;
+
+// Cell-pair unions for frames with the eps-diagonal grid: the cores of a
+// cell are one node (its smallest core index).
+__global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w, int64_t n_items) {
+    const int64_t item = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (item >= n_items) return;
+    const int64_t c = item / kMaxForward;
+    const int k = (int)(item - c * kMaxForward);
+    const int f = frame_of_cell(a.offsets, a.n_frames, c);
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig] || !rec[kDense]) return;
+    const BigGrid g = load_grid(rec);
+    const int64_t base = cell_base(a.offsets, f);
+    const int32_t ca = (int32_t)(c - base);
+    if (ca >= g.ncell) return;
+    const int32_t na = w.cnode[base + ca];
+    if (na == INT_MAX) return;
+    int odx, ody;
+    if (!forward_offset(g, k, &odx, &ody)) return;
+    const int32_t ay = ca / g.ncx, ax = ca - ay * g.ncx;
+    const int32_t bx = ax + odx, by = ay + ody;
+    if (bx < 0 || bx >= g.ncx || by >= g.ncy) return;
+    const int32_t cb = by * g.ncx + bx;
+    const int32_t nb = w.cnode[base + cb];
+    if (nb == INT_MAX) return;
+    const int32_t b = a.offsets[f];
+    int32_t *parent = a.labels + b;
+    if (uf_find<kAgent>(parent, na) == uf_find<kAgent>(parent, nb)) return;
+    const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
+    const int32_t *cs = w.cstart + base;
+    const int32_t a0 = cs[ca], a1 = cs[ca + 1], b0 = cs[cb], b1 = cs[cb + 1];
+    const int2 *S = w.spos + b;
+    const uint8_t *core = w.score + b;
+    const int32_t rx0 = g.x0 + bx * g.side, rx1 = rx0 + g.side - 1;
+    const int32_t ry0 = g.y0 + by * g.side, ry1 = ry0 + g.side - 1;
+    for (int32_t qa = a0; qa < a1; ++qa) {
+        if (!core[qa]) continue;
+        const int2 va = S[qa];
+        const int32_t ddx = min(max(max(rx0 - va.x, va.x - rx1), 0), r.e1);
+        const int32_t ddy = min(max(max(ry0 - va.y, va.y - ry1), 0), r.e1);
+        if (__mul24(ddx, ddx) + __mul24(ddy, ddy) > r.e2) continue;
+        for (int32_t qb = b0; qb < b1; ++qb) {
+            if (core[qb] && within(va, S[qb], r)) {
+                uf_unite<kAgent>(parent, na, nb);
+                return;
+            }
+        }
+    }
+}
+
+// Point-pair unions for frames whose grid was coarsened.
+__global__ __launch_bounds__(kBlock) void big_union_points(ClusterArgs a, BigWs w) {
+    const int32_t p = blockIdx.x * kBlock + threadIdx.x;
+    if (p >= a.total || !w.score[p]) return;
+    const int f = frame_of_point(a.offsets, a.n_frames, p);
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig] || rec[kDense]) return;
+    const BigGrid g = load_grid(rec);
+    const int32_t b = a.offsets[f];
+    const int32_t *cs = w.cstart + cell_base(a.offsets, f);
+    const int2 *S = w.spos + b;
+    const uint8_t *core = w.score + b;
+    int32_t *parent = a.labels + b;
+    const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
+    const int32_t lp = p - b;
+    const int2 v = S[lp];
+    const int32_t op = w.ssid[p];
+    int32_t cx, cy;
+    cell_xy(v, g, &cx, &cy);
+    const int32_t own = cy * g.ncx + cx;
+    for (int32_t q = cs[own]; q < lp; ++q)
+        if (core[q] && within(v, S[q], r)) uf_unite<kAgent>(parent, op, w.ssid[b + q]);
+    for (int dy = 0; dy <= g.reach; ++dy) {
+        const int32_t ry = cy + dy;
+        if (ry >= g.ncy) break;
+        const int32_t rx0 = dy == 0 ? cx + 1 : max(cx - g.dx[dy], 0);
+        const int32_t rx1 = min(cx + g.dx[dy], g.ncx - 1);
+        if (rx0 > rx1) continue;
+        const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
+        for (int32_t q = cs[ry * g.ncx + rx0]; q < q1; ++q)
+            if (core[q] && within(v, S[q], r)) uf_unite<kAgent>(parent, op, w.ssid[b + q]);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void big_flatten(ClusterArgs a, BigWs w) {
+    const int32_t p = blockIdx.x * kBlock + threadIdx.x;
+    bool counted = false;
+    int f = 0;
+    if (p < a.total && w.score[p]) {
+        f = frame_of_point(a.offsets, a.n_frames, p);
+        const int32_t *rec = w.rec + (size_t)f * kRec;
+        if (rec[kBig]) {
+            const BigGrid g = load_grid(rec);
+            const int32_t b = a.offsets[f];
+            const int32_t o = w.ssid[p];
+            int32_t node = o;
+            if (g.dense) {
+                int32_t cx, cy;
+                cell_xy(w.spos[p], g, &cx, &cy);
+                node = w.cnode[cell_base(a.offsets, f) + (int64_t)cy * g.ncx + cx];
+            }
+            const int32_t root = uf_root<kAgent>(a.labels + b, node);
+            st_rlx<kAgent>(a.labels + b + o, root);
+            counted = root == o;
+        }
+    }
+    if (counted && a.n_clusters) atomicAdd(&a.n_clusters[f], 1);
+}
+
+__global__ __launch_bounds__(kBlock) void big_border(ClusterArgs a, BigWs w) {
+    const int32_t p = blockIdx.x * kBlock + threadIdx.x;
+    if (p >= a.total || w.score[p]) return;
+    const int f = frame_of_point(a.offsets, a.n_frames, p);
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig]) return;
+    const BigGrid g = load_grid(rec);
+    const int32_t b = a.offsets[f];
+    const int64_t base = cell_base(a.offsets, f);
+    const int32_t *cs = w.cstart + base;
+    const int2 *S = w.spos + b;
+    const uint8_t *core = w.score + b;
+    const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
+    const int2 v = w.spos[p];
+    int32_t cx, cy;
+    cell_xy(v, g, &cx, &cy);
+    int32_t best = -1, best_d2 = INT32_MAX, by = 0, bx = 0;
+    for (int dy = -g.reach; dy <= g.reach; ++dy) {
+        const int32_t ry = cy + dy;
+        if (ry < 0 || ry >= g.ncy) continue;
+        const int dxm = g.dx[dy < 0 ? -dy : dy];
+        const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
+        const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
+        for (int32_t q = cs[ry * g.ncx + rx0]; q < q1; ++q) {
+            if (!core[q]) continue;
+            const int2 qq = S[q];
+            const int32_t d2 = sq_dist_clamped(v, qq, r);
+            if (d2 > r.e2) continue;
+            const bool take = core_before(d2, qq.y, qq.x, best_d2, by, bx);
+            best = take ? q : best;
+            best_d2 = take ? d2 : best_d2;
+            by = take ? qq.y : by;
+            bx = take ? qq.x : bx;
+        }
+    }
+    const int32_t o = w.ssid[p];
+    if (best >= 0) {
+        a.labels[b + o] = a.labels[b + w.ssid[b + best]];
+        a.kind[b + o] = 1;
+    } else {
+        a.labels[b + o] = -1;
+    }
+}
+
+unsigned blocks_for(int64_t n) { return (unsigned)((n + kBlock - 1) / kBlock); }
+
+}  // namespace
+
+size_t cluster_big_workspace(int32_t n_frames, int32_t total) {
+    const size_t cells = 2 * (size_t)total + 2 * (size_t)n_frames;
+    return align256(sizeof(int32_t) * kRec * (size_t)n_frames) + align256(sizeof(int32_t) * (size_t)total) +
+           align256(sizeof(int2) * (size_t)total) + align256(sizeof(int32_t) * (size_t)total) +
+           align256((size_t)total) + 2 * align256(sizeof(int32_t) * cells) + 256;
+}
+
+hipError_t launch_cluster_big(const ClusterArgs &a, void *workspace, hipStream_t stream) {
+    const BigWs w = carve(workspace, a.n_frames, a.total);
+    const int64_t cells = 2 * (int64_t)a.total + 2 * (int64_t)a.n_frames;
+    const unsigned pts = blocks_for(a.total);
+    hipLaunchKernelGGL(big_prep, dim3(a.n_frames), dim3(kBlock), 0, stream, a, w);
+    if (a.total > 0) {
+        hipLaunchKernelGGL(big_hist, dim3(pts), dim3(kBlock), 0, stream, a, w);
+        hipLaunchKernelGGL(big_scan, dim3(a.n_frames), dim3(kScanThreads), 0, stream, a, w);
+        hipLaunchKernelGGL(big_scatter, dim3(pts), dim3(kBlock), 0, stream, a, w);
+        hipLaunchKernelGGL(big_core, dim3(pts), dim3(kBlock), 0, stream, a, w);
+        hipLaunchKernelGGL(big_nodes, dim3(pts), dim3(kBlock), 0, stream, a, w);
+        const int64_t items = cells * kMaxForward;
+        hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items);
+        hipLaunchKernelGGL(big_union_points, dim3(pts), dim3(kBlock), 0, stream, a, w);
+        hipLaunchKernelGGL(big_flatten, dim3(pts), dim3(kBlock), 0, stream, a, w);
+        hipLaunchKernelGGL(big_border, dim3(pts), dim3(kBlock), 0, stream, a, w);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace flock

@@ -20,8 +20,10 @@ struct ClusterArgs {
     int32_t eps_q;            // radius in quanta
     int32_t min_pts;
     int32_t cell_side;        // largest s >= 1 with 2 s^2 <= eps_q^2
-    int32_t cap_points;       // frames with more points take the in-place path
+    int32_t cap_points;       // frames with more points leave the on-chip kernel
     int32_t cap_cells;        // cell-table entries available on chip
+    int32_t big_path;         // 1: frames above cap_points go to the multi-workgroup
+                              // path; 0: the on-chip kernel clusters them in place
     int32_t *labels;          // [total]
     uint8_t *kind;            // [total]
     int32_t *n_clusters;      // [n_frames] or nullptr
@@ -34,6 +36,10 @@ size_t cluster_lds_bytes(int32_t cap_points, int32_t cap_cells);
 int32_t cluster_max_cap_points(size_t lds_limit);
 
 hipError_t launch_cluster_resident(const ClusterArgs &a, size_t lds_bytes, hipStream_t stream);
+
+// Multi-workgroup path for frames above cap_points (cluster_big.hip).
+size_t cluster_big_workspace(int32_t n_frames, int32_t total);
+hipError_t launch_cluster_big(const ClusterArgs &a, void *workspace, hipStream_t stream);
 
 // ----------------------------------------------------------------------------
 // Density

@@ -135,6 +135,49 @@ def test_frame_above_lds_capacity_gpu():
     assert_cluster_equal(got, xy, off, 160, 5, tag="big frame")
 
 
+@pytest.mark.parametrize("max_fp", [0, 20000])
+def test_large_frame_path_gpu(max_fp):
+    """Frames above the on-chip capacity use the multi-workgroup path: dense
+    frames, a frame whose cell grid is coarsened (huge spread, small eps),
+    and small frames around them."""
+    rng = np.random.default_rng(11)
+    dense = np.stack([rng.normal(20000, 3000, 15000), rng.normal(15000, 2500, 15000)], 1)
+    dense = np.clip(np.round(dense), 0, 60000).astype(np.int32)
+    spread = rng.integers(0, 1 << 20, (12000, 2)).astype(np.int32)
+    spread[:3000] = spread[3000:6000] + rng.integers(-8, 9, (3000, 2)).astype(np.int32)
+    spread = np.clip(spread, 0, None)
+    small = rng.integers(0, 16 * 300, (500, 2)).astype(np.int32)
+    xy, off = wl.pack([small, dense, np.zeros((0, 2), np.int32), spread, small[:40]])
+    for eps_q, min_pts in ((160, 5), (16, 2)):
+        got = run_cluster(xy, off, eps_q, min_pts, max_fp=max_fp)
+        assert_cluster_equal(got, xy, off, eps_q, min_pts, tag=f"large eps {eps_q} max_fp {max_fp}")
+
+
+def test_workspace_too_small_gpu():
+    xy, off = wl.random_batch(1, 3, 50)
+    dxy, doff = dev_batch(xy, off)
+    lib = flock.lib()
+    need = lib.cluster_frames_workspace(3, xy.shape[0], 0)
+    assert need > 0
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    labels = torch.empty(xy.shape[0], dtype=torch.int32, device="cuda")
+    kind = torch.empty(xy.shape[0], dtype=torch.uint8, device="cuda")
+    import ctypes
+    st = lib.cluster_frames(ctypes.c_void_p(dxy.data_ptr()), ctypes.c_void_p(doff.data_ptr()), 3,
+                            xy.shape[0], 0, 640, 4, ctypes.c_void_p(labels.data_ptr()),
+                            ctypes.c_void_p(kind.data_ptr()), None, ctypes.c_void_p(ws.data_ptr()),
+                            need - 1, None)
+    assert st == flock.binding.FLOCK_ENOMEM
+    # and with NULL workspace the library allocates stream-ordered scratch itself
+    st = lib.cluster_frames(ctypes.c_void_p(dxy.data_ptr()), ctypes.c_void_p(doff.data_ptr()), 3,
+                            xy.shape[0], 0, 640, 4, ctypes.c_void_p(labels.data_ptr()),
+                            ctypes.c_void_p(kind.data_ptr()), None, None, 0, None)
+    assert st == 0
+    torch.cuda.synchronize()
+    rl, rk, _ = oracle.cluster_frames(xy, off, 640, 4)
+    assert np.array_equal(labels.cpu().numpy(), rl) and np.array_equal(kind.cpu().numpy(), rk)
+
+
 def test_lattice_ties_gpu():
     frames = [wl.lattice_frame(30, 20, 640), wl.lattice_frame(25, 25, 452, 1000, 2000),
               wl.lattice_frame(10, 10, 641), np.concatenate([wl.lattice_frame(12, 12, 384),
