@@ -148,11 +148,7 @@ size_t cluster_frames_workspace(int32_t n_frames, int32_t total, int32_t max_fra
 }
 
 size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h) {
-    (void)n_frames;
-    (void)total;
-    (void)grid_w;
-    (void)grid_h;
-    return 0;
+    return flock::density_workspace_bytes(n_frames, total, grid_w, grid_h);
 }
 
 flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
@@ -228,8 +224,6 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
                             float sigma_px, float *density, void *workspace, size_t workspace_bytes,
                             void *stream) {
     g_error.clear();
-    (void)workspace;
-    (void)workspace_bytes;
     if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
     if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
     if (max_frame_points < 0) return fail(FLOCK_EINVAL, "max_frame_points = %d < 0", max_frame_points);
@@ -267,10 +261,25 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     a.grid_h = grid_h;
     a.sigma_px = sigma_px;
     a.density = density;
-    const flock::DensityPlan plan = flock::plan_density(a, dev->n_cus);
-    const long long blocks = (long long)n_frames * plan.regions_y * plan.regions_x;
+    const flock::DensityPlan plan = flock::plan_density(a, dev->n_cus, dev->lds_per_block);
+    const long long blocks = (long long)n_frames * plan.regions_y * plan.regions_x * plan.split;
     if (blocks > 0x7fffffffLL) return fail(FLOCK_EUNSUPPORTED, "batch too large for one launch");
-    hipError_t err = flock::launch_density(a, plan, dev->lds_per_block, s);
+    // a split launch keeps partial grids in the workspace
+    const size_t need = plan.split > 1 ? flock::density_workspace_bytes(n_frames, total, grid_w, grid_h) : 0;
+    if (workspace && workspace_bytes < need)
+        return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
+    if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
+    void *ws = workspace;
+    hipError_t err = hipSuccess;
+    if (need > 0 && !ws) {
+        err = hipMallocAsync(&ws, need, s);
+        if (err != hipSuccess) return hip_fail(err, "workspace allocation");
+    }
+    err = flock::launch_density(a, plan, dev->lds_per_block, static_cast<float *>(ws), s);
+    if (need > 0 && !workspace) {
+        const hipError_t ferr = hipFreeAsync(ws, s);
+        if (err == hipSuccess) err = ferr;
+    }
     if (err != hipSuccess) return hip_fail(err, "density kernel launch");
     return FLOCK_OK;
 }

@@ -169,6 +169,15 @@ __device__ void cluster_frame_inplace(const ClusterArgs &a, int f, int32_t b, in
 
 constexpr uint16_t kNone = 0xffff;
 constexpr int kMaxOffsets = 16;
+// Neighbour cells lie within +-reach cells, and reach <= 2 for every eps:
+// reach = 1 + (E - 1) / side with side >= max(1, floor(E / sqrt 2)) > (E - 1) / 2.
+// So the full stencil has at most 5 x 5 cells.
+constexpr int kMaxStencil = 25;
+constexpr int kMaxFar = 8;  // forward stencil cells beyond the adjacent four (reach <= 2)
+constexpr int kBorderLanes = 8;  // lanes that share one border candidate
+// Points per thread held in registers during the sort: the planner keeps a
+// resident frame at <= kThreads * kPtsPerThread points.
+constexpr int kPtsPerThread = 10;
 
 // Coordinates relative to the frame's bounding-box corner, packed as
 // x | y << 16 (the resident path takes frames whose extent fits 16 bits).
@@ -221,6 +230,140 @@ __device__ __forceinline__ int32_t count_span(const uint32_t *pxy, int32_t q0, i
     return cnt;
 }
 
+// floor(x / d) for 0 <= x < 2^22, 1 <= d, from a float reciprocal and one
+// correction step.
+__device__ __forceinline__ int32_t div_small(int32_t x, int32_t d, float inv_d) {
+    int32_t q = (int32_t)((float)x * inv_d);
+    if (q * d > x) --q;
+    else if ((q + 1) * d <= x) ++q;
+    return q;
+}
+
+// Squared distance from v to the nearest point of the cell
+// rectangle [x0, x0 + side) x [y0, y0 + side), per axis clamped to E + 1.
+__device__ __forceinline__ int32_t rect_near2(int32_t vx, int32_t vy, int32_t x0, int32_t y0, int32_t side,
+                                              int32_t e1) {
+    const int32_t dx = min(max(max(x0 - vx, vx - (x0 + side - 1)), 0), e1);
+    const int32_t dy = min(max(max(y0 - vy, vy - (y0 + side - 1)), 0), e1);
+    return __mul24(dx, dx) + __mul24(dy, dy);
+}
+
+// Neighbour-cell tables of one frame, built by the 64 lanes of one wave.
+// Cell offset (dx, dy), |dx|, |dy| <= reach <= 2, can hold a neighbour iff the
+// gap between the two cells, gap(|dx|)^2 + gap(|dy|)^2, is <= E^2.
+//   sdx/sdy   the whole stencil, nearest cells first (ties in lane order)
+//   odx/ody   its forward half (cells later in row-major order): adjacent
+//             cells in table 0, the others in table 1
+//   dxmax[k]  the widest |dx| in row |dy| = k
+__device__ void build_stencil(int32_t reach, int32_t side, const Radius &r, int lane, int *dxmax, int *sdx,
+                              int *sdy, int *nsten, int (*odx)[kMaxOffsets], int (*ody)[kMaxOffsets],
+                              int *noff) {
+    const int dx = lane % 5 - 2, dy = lane / 5 - 2;
+    const int adx = dx < 0 ? -dx : dx, ady = dy < 0 ? -dy : dy;
+    bool valid = false;
+    uint32_t key = 0xffffffffu;
+    if (lane < kMaxStencil && adx <= reach && ady <= reach) {
+        const int64_t gx = cell_gap(adx, side), gy = cell_gap(ady, side);
+        const int64_t d = gx * gx + gy * gy;
+        valid = d <= (int64_t)r.e2;
+        key = valid ? (uint32_t)d : key;
+    }
+    int rank = 0;
+    for (int u = 0; u < kMaxStencil; ++u) {
+        const uint32_t ku = __shfl(key, u, 64);
+        rank += (ku < key) | ((ku == key) & (u < lane));
+    }
+    const uint64_t vm = __ballot(valid);
+    if (valid) {
+        sdx[rank] = dx;
+        sdy[rank] = dy;
+    }
+    const bool fwd = valid && (dy > 0 || (dy == 0 && dx > 0));
+    const bool adj = adx <= 1 && ady <= 1;
+    const uint64_t m0 = __ballot(fwd && adj), m1 = __ballot(fwd && !adj);
+    const uint64_t below = (1ull << lane) - 1ull;
+    if (fwd && adj) {
+        odx[0][__popcll(m0 & below)] = dx;
+        ody[0][__popcll(m0 & below)] = dy;
+    }
+    if (fwd && !adj) {
+        odx[1][__popcll(m1 & below)] = dx;
+        ody[1][__popcll(m1 & below)] = dy;
+    }
+    if (lane <= 2) {  // row dy = lane: valid cells are |dx| <= dxmax, a symmetric run
+        const int cnt = __popcll((vm >> ((lane + 2) * 5)) & 31ull);
+        dxmax[lane] = cnt > 0 ? (cnt - 1) / 2 : 0;
+    }
+    if (lane == 0) {
+        *nsten = __popcll(vm);
+        noff[0] = __popcll(m0);
+        noff[1] = __popcll(m1);
+    }
+}
+
+// Join core cell clist[j] with its forward neighbours (odx/ody, noff <= K
+// of them): a neighbour holding a core is joined when some core pair across
+// the two cells is within eps.  All cores of a cell form one node (its
+// smallest core index), since any two points of a cell are neighbours.
+// The neighbour cell words and the first step of each neighbour's find are
+// loaded together, so one thread keeps several LDS reads in flight.
+template <int K>
+__device__ __forceinline__ void union_cell(int32_t j, const uint16_t *clist, const uint32_t *cell,
+                                           int32_t *parent, const uint32_t *pxy, const uint8_t *score,
+                                           const Grid &g, const Radius &r, const int *odx, const int *ody,
+                                           int noff, float inv_ncx) {
+    const int32_t ca = clist[j];
+    const int32_t ay = div_small(ca, g.ncx, inv_ncx), ax = ca - ay * g.ncx;
+    const uint32_t wa = cell[ca];
+    const int32_t a0 = (int32_t)(wa & 0xffffu), a1 = (int32_t)(cell[ca + 1] & 0xffffu);
+    int32_t cb[K], bxs[K], bys[K];
+    uint32_t wb[K], wb1[K];
+#pragma unroll
+    for (int o = 0; o < K; ++o) {
+        const int32_t bx = ax + odx[o < noff ? o : 0], by = ay + ody[o < noff ? o : 0];
+        const bool ok = o < noff && bx >= 0 && bx < g.ncx && by < g.ncy;
+        bxs[o] = bx;
+        bys[o] = by;
+        cb[o] = ok ? by * g.ncx + bx : -1;
+        const int32_t c = ok ? cb[o] : ca;
+        wb[o] = cell[c];
+        wb1[o] = cell[c + 1];
+    }
+    int32_t pb[K];
+#pragma unroll
+    for (int o = 0; o < K; ++o) {
+        const int32_t nb = (int32_t)(wb[o] >> 16);
+        const bool has = cb[o] >= 0 && nb != (int32_t)kNone;
+        cb[o] = has ? cb[o] : -1;
+        pb[o] = has ? ld_rlx<kGroup>(parent + nb) : 0;
+    }
+    int32_t ra = uf_find<kGroup>(parent, (int32_t)(wa >> 16));
+#pragma unroll
+    for (int o = 0; o < K; ++o) {
+        if (cb[o] < 0) continue;
+        // pb is an ancestor of the neighbour's node: its root is the node's root
+        const int32_t rb = uf_find<kGroup>(parent, pb[o]);
+        ra = uf_find<kGroup>(parent, ra);
+        if (ra == rb) continue;  // already one tree
+        // B's rectangle, to skip cores of A that cannot reach it
+        const int32_t bx0 = bxs[o] * g.side, by0 = bys[o] * g.side;
+        const int32_t b0 = (int32_t)(wb[o] & 0xffffu), b1 = (int32_t)(wb1[o] & 0xffffu);
+        bool hit = false;
+        for (int32_t qa = a0; qa < a1 && !hit; ++qa) {
+            if (!score[qa]) continue;
+            const uint32_t va = pxy[qa];
+            if (rect_near2(pk_x(va), pk_y(va), bx0, by0, g.side, r.e1) > r.e2) continue;
+            for (int32_t qb = b0; qb < b1; ++qb) {
+                if (score[qb] && sq_dist_pk(va, pxy[qb], r.e1) <= r.e2) {
+                    hit = true;
+                    break;
+                }
+            }
+        }
+        if (hit) uf_unite<kGroup>(parent, ra, rb);
+    }
+}
+
 // Append `flag` lanes' values to list[] (wave-uniform call: every lane of the
 // wave must reach it).
 __device__ __forceinline__ void wave_append(bool flag, uint16_t value, uint16_t *list, int *counter) {
@@ -243,6 +386,9 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     __shared__ int s_noff[2];
     __shared__ int s_odx[2][kMaxOffsets];
     __shared__ int s_ody[2][kMaxOffsets];
+    __shared__ int s_nsten;
+    __shared__ int s_sdx[kMaxStencil];
+    __shared__ int s_sdy[kMaxStencil];
     __shared__ int s_dxmax[8];
 
     const int f = blockIdx.x;
@@ -278,15 +424,23 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
     const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
 
-    // 1. bounding box
+    // 1. bounding box; each thread keeps its points (i = tid + k * kThreads)
+    //    in registers for the sort
+    int2 pt[kPtsPerThread];
+#pragma unroll
+    for (int k = 0; k < kPtsPerThread; ++k) {
+        const int32_t i = tid + k * kThreads;
+        pt[k] = i < n ? P[i] : make_int2(0, 0);
+    }
     {
         int xmn = INT_MAX, ymn = INT_MAX, xmx = INT_MIN, ymx = INT_MIN;
-        for (int32_t i = tid; i < n; i += kThreads) {
-            const int2 p = P[i];
-            xmn = min(xmn, p.x);
-            ymn = min(ymn, p.y);
-            xmx = max(xmx, p.x);
-            ymx = max(ymx, p.y);
+#pragma unroll
+        for (int k = 0; k < kPtsPerThread; ++k) {
+            if (tid + k * kThreads >= n) break;
+            xmn = min(xmn, pt[k].x);
+            ymn = min(ymn, pt[k].y);
+            xmx = max(xmx, pt[k].x);
+            ymx = max(ymx, pt[k].y);
         }
         xmn = wave_min(xmn);
         ymn = wave_min(ymn);
@@ -351,40 +505,19 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         g.dxmax = s_dxmax;
     }
 
-    // 3. counting sort by cell
+    // 3. counting sort by cell (wave 0 also builds the stencil tables)
     for (int32_t c = tid; c <= g.ncell; c += kThreads) cell[c] = 0;
-    if (tid == 0) {
-        for (int dy = 0; dy <= g.reach; ++dy) {
-            const int64_t gy = cell_gap(dy, g.side);
-            int dx = g.reach;
-            while (dx > 0) {
-                const int64_t gx = cell_gap(dx, g.side);
-                if (gx * gx + gy * gy <= (int64_t)r.e2) break;
-                --dx;
-            }
-            s_dxmax[dy] = dx;
-        }
-        // forward half of the neighbour-cell stencil (cells after this one in
-        // row-major order): adjacent cells in table 0, the rest in table 1
-        int k[2] = {0, 0};
-        for (int dy = 0; dy <= g.reach; ++dy)
-            for (int dx = (dy == 0 ? 1 : -s_dxmax[dy]); dx <= s_dxmax[dy]; ++dx) {
-                const int t = (dx >= -1 && dx <= 1 && dy <= 1) ? 0 : 1;
-                if (k[t] < kMaxOffsets) {
-                    s_odx[t][k[t]] = dx;
-                    s_ody[t][k[t]] = dy;
-                    ++k[t];
-                }
-            }
-        s_noff[0] = k[0];
-        s_noff[1] = k[1];
-    }
+    if (tid < 64)
+        build_stencil(g.reach, g.side, r, lane, s_dxmax, s_sdx, s_sdy, &s_nsten, s_odx, s_ody, s_noff);
     __syncthreads();
-    for (int32_t i = tid; i < n; i += kThreads) {
-        const int2 p = P[i];
-        const uint32_t v = (uint32_t)(p.x - x0) | ((uint32_t)(p.y - y0) << 16);
+    uint32_t pv[kPtsPerThread];
+    uint16_t prank[kPtsPerThread];
+#pragma unroll
+    for (int k = 0; k < kPtsPerThread; ++k) {
+        if (tid + k * kThreads >= n) break;
+        pv[k] = (uint32_t)(pt[k].x - x0) | ((uint32_t)(pt[k].y - y0) << 16);
         int32_t cx, cy;
-        list[i] = (uint16_t)atomicAdd(&cell[cell_id(v, g, &cx, &cy)], 1u);  // rank in cell
+        prank[k] = (uint16_t)atomicAdd(&cell[cell_id(pv[k], g, &cx, &cy)], 1u);  // rank in cell
     }
     __syncthreads();
     {
@@ -402,12 +535,13 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         if (tid == kThreads - 1) cell[g.ncell] = (uint32_t)run | 0xffff0000u;
     }
     __syncthreads();
-    for (int32_t i = tid; i < n; i += kThreads) {
-        const int2 p = P[i];
-        const uint32_t v = (uint32_t)(p.x - x0) | ((uint32_t)(p.y - y0) << 16);
+#pragma unroll
+    for (int k = 0; k < kPtsPerThread; ++k) {
+        const int32_t i = tid + k * kThreads;
+        if (i >= n) break;
         int32_t cx, cy;
-        const int32_t pos = cstart(cell_id(v, g, &cx, &cy)) + list[i];
-        pxy[pos] = v;
+        const int32_t pos = cstart(cell_id(pv[k], g, &cx, &cy)) + prank[k];
+        pxy[pos] = pv[k];
         sid[pos] = (uint16_t)i;
     }
     __syncthreads();
@@ -476,43 +610,13 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         // across the cells is within eps.  Adjacent cells go first; by the
         // second pass most farther pairs are already in one tree.
         const int32_t ncl = s_ncells;
-        for (int pass = 0; pass < 2; ++pass) {
-            const int noff = s_noff[pass];
-            for (int32_t item = tid; item < ncl * noff; item += kThreads) {
-                const int32_t j = item / noff;
-                const int o = item - j * noff;
-                const int32_t ca = clist[j];
-                const int32_t ay = ca / g.ncx, ax = ca - ay * g.ncx;
-                const int32_t bx = ax + s_odx[pass][o], by = ay + s_ody[pass][o];
-                if (bx < 0 || bx >= g.ncx || by >= g.ncy) continue;
-                const int32_t cb = by * g.ncx + bx;
-                const uint32_t nb = cnode(cb);
-                if (nb == kNone) continue;
-                const uint32_t na = cnode(ca);
-                if (uf_find<kGroup>(parent, (int32_t)na) == uf_find<kGroup>(parent, (int32_t)nb)) continue;
-                // B's rectangle, to skip points of A that cannot reach it
-                const int32_t bx0 = bx * g.side, bx1 = bx0 + g.side - 1;
-                const int32_t by0 = by * g.side, by1 = by0 + g.side - 1;
-                const int32_t a0 = cstart(ca), a1 = cstart(ca + 1);
-                const int32_t b0 = cstart(cb), b1 = cstart(cb + 1);
-                bool hit = false;
-                for (int32_t qa = a0; qa < a1 && !hit; ++qa) {
-                    if (!score[qa]) continue;
-                    const uint32_t va = pxy[qa];
-                    const int32_t ddx = min(max(max(bx0 - pk_x(va), pk_x(va) - bx1), 0), r.e1);
-                    const int32_t ddy = min(max(max(by0 - pk_y(va), pk_y(va) - by1), 0), r.e1);
-                    if (__mul24(ddx, ddx) + __mul24(ddy, ddy) > r.e2) continue;
-                    for (int32_t qb = b0; qb < b1; ++qb) {
-                        if (score[qb] && sq_dist_pk(va, pxy[qb], r.e1) <= r.e2) {
-                            hit = true;
-                            break;
-                        }
-                    }
-                }
-                if (hit) uf_unite<kGroup>(parent, (int32_t)na, (int32_t)nb);
-            }
-            __syncthreads();
-        }
+        const float inv_ncx = 1.0f / (float)g.ncx;
+        for (int32_t j = tid; j < ncl; j += kThreads)
+            union_cell<4>(j, clist, cell, parent, pxy, score, g, r, s_odx[0], s_ody[0], s_noff[0], inv_ncx);
+        __syncthreads();
+        for (int32_t j = tid; j < ncl; j += kThreads)
+            union_cell<kMaxFar>(j, clist, cell, parent, pxy, score, g, r, s_odx[1], s_ody[1], s_noff[1], inv_ncx);
+        __syncthreads();
     } else {
         // coarsened grid: point-level unions (each pair once: the later point
         // of a cell, or the point in the earlier cell, does the work)
@@ -563,48 +667,57 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     }
     __syncthreads();
     {
+        // kBorderLanes consecutive lanes share a point: lane g scans stencil
+        // cells g, g + kBorderLanes, ...; the group keeps the smallest key
+        // d^2 << 32 | packed (y, x), then the smallest sorted index among
+        // equal keys (coincident cores, one cluster).
         const int32_t nl = s_nlist;
-        for (int32_t j = tid; j < nl; j += kThreads) {
+        const int ns = s_nsten;
+        const int gl = lane & (kBorderLanes - 1);
+        for (int32_t j = tid / kBorderLanes; j < nl; j += kThreads / kBorderLanes) {
             const int32_t p = list[j];
             const uint32_t v = pxy[p];
             const int32_t vx = pk_x(v), vy = pk_y(v);
             int32_t cx, cy;
             cell_id(v, g, &cx, &cy);
-            int32_t best = -1, best_d2 = INT32_MAX;
-            uint32_t bestv = 0;
-            for (int dy = -g.reach; dy <= g.reach; ++dy) {
-                const int32_t ry = cy + dy;
-                if (ry < 0 || ry >= g.ncy) continue;
-                const int32_t y0c = ry * g.side;
+            uint64_t bestk = ~0ull;
+            int32_t best = -1;
+            for (int s = gl; s < ns; s += kBorderLanes) {
+                const int32_t rx = cx + s_sdx[s], ry = cy + s_sdy[s];
+                if (rx < 0 || rx >= g.ncx || ry < 0 || ry >= g.ncy) continue;
+                const int32_t c = ry * g.ncx + rx;
+                const uint32_t cw = cell[c];
+                if ((cw >> 16) == kNone) continue;  // no core in this cell
+                const int32_t x0c = rx * g.side, y0c = ry * g.side;
+                const int32_t ddx = min(max(max(x0c - vx, vx - (x0c + g.side - 1)), 0), r.e1);
                 const int32_t ddy = min(max(max(y0c - vy, vy - (y0c + g.side - 1)), 0), r.e1);
-                const int dxm = g.dxmax[dy < 0 ? -dy : dy];
-                const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
-                for (int32_t rx = rx0; rx <= rx1; ++rx) {
-                    const int32_t c = ry * g.ncx + rx;
-                    if (cnode(c) == kNone) continue;  // no core in this cell
-                    const int32_t x0c = rx * g.side;
-                    const int32_t ddx = min(max(max(x0c - vx, vx - (x0c + g.side - 1)), 0), r.e1);
-                    if (__mul24(ddx, ddx) + __mul24(ddy, ddy) > r.e2) continue;  // cell out of reach
-                    const int32_t q1 = cstart(c + 1);
-                    for (int32_t q = cstart(c); q < q1; ++q) {
-                        if (!score[q]) continue;
-                        const uint32_t w = pxy[q];
-                        const int32_t d2 = sq_dist_pk(v, w, r.e1);
-                        if (d2 > r.e2) continue;
-                        // packed y<<16|x orders as (y, x)
-                        const bool take = (d2 < best_d2) | ((d2 == best_d2) & (w < bestv));
-                        best = take ? q : best;
-                        best_d2 = take ? d2 : best_d2;
-                        bestv = take ? w : bestv;
-                    }
+                if (__mul24(ddx, ddx) + __mul24(ddy, ddy) > r.e2) continue;  // cell out of reach
+                const int32_t q1 = cstart(c + 1);
+                for (int32_t q = (int32_t)(cw & 0xffffu); q < q1; ++q) {
+                    const uint32_t w = pxy[q];
+                    const int32_t d2 = sq_dist_pk(v, w, r.e1);
+                    const uint64_t key = ((uint64_t)(uint32_t)d2 << 32) | w;
+                    const bool take = (d2 <= r.e2) & (score[q] != 0) & (key < bestk);
+                    best = take ? q : best;
+                    bestk = take ? key : bestk;
                 }
             }
-            const int32_t o = sid[p];
-            if (best >= 0) {
-                parent[o] = parent[sid[best]];
-                kindo[o] = 1;
-            } else {
-                parent[o] = -1;
+#pragma unroll
+            for (int o = 1; o < kBorderLanes; o <<= 1) {
+                const uint64_t ok = __shfl_xor(bestk, o, 64);
+                const int32_t ob = __shfl_xor(best, o, 64);
+                const bool take = (ok < bestk) | ((ok == bestk) & (ob < best));
+                best = take ? ob : best;
+                bestk = take ? ok : bestk;
+            }
+            if (gl == 0) {
+                const int32_t o = sid[p];
+                if (best >= 0) {
+                    parent[o] = parent[sid[best]];
+                    kindo[o] = 1;
+                } else {
+                    parent[o] = -1;
+                }
             }
         }
     }
@@ -636,7 +749,7 @@ int32_t cluster_max_cap_points(size_t lds_limit) {
     const size_t reserve = 1024 + 4096 * 6 + 4;
     if (lds_limit <= reserve) return 0;
     size_t cap = (lds_limit - reserve) / 14;
-    if (cap > 65535) cap = 65535;  // original indices are kept as uint16
+    if (cap > (size_t)kThreads * kPtsPerThread) cap = (size_t)kThreads * kPtsPerThread;  // register sort
     return (int32_t)cap;
 }
 

@@ -6,50 +6,62 @@
 //     c = 1 / (2 pi s^2),
 // separates into per-axis factors Fy[gy][i] = exp(-(cy - y_i)^2 / (2 s^2)) and
 // Fx[gx][i] = exp(-(cx - x_i)^2 / (2 s^2)), so D = c * Fy . Fx^T: a dense
-// contraction over the birds of the frame.
+// contraction over the birds of the frame, run on v_mfma_f32_32x32x16_f16
+// with fp16 factors and fp32 accumulation.
 //
-// Each workgroup (4 waves) owns one frame and one output region of
-// (32 RM) gy rows x (32 RN) gx columns.  Birds stream through in chunks of
-// kChunk: the chunk's factors for the region's rows and columns are written
-// to LDS as fp16, then each wave runs v_mfma_f32_32x32x16_f16 over its quarter
-// of the chunk for every tile of the region, accumulating in fp32.  At the
-// end the four waves' partial sums are added in a fixed order through LDS, so
-// the result is deterministic.
+// A factor below 2^-25 rounds to +0 in fp16, and exp(-t^2/2) < 2^-25 for
+// |t| > 5.9, so a bird has nonzero factors only in the rows within 6 s of it
+// (its window); every other factor is +0 in either evaluation, and the
+// contraction stays dense over all (row, column, bird) triples.
 //
-// Factor generation is windowed: a factor below 2^-25 rounds to +0 in fp16,
-// and exp(-t^2/2) < 2^-25 for |t| > 5.9, so each bird only evaluates the rows
-// within 6 s of it; the rest of the LDS tile is cleared to zero.  The fp16
-// operands are those of the dense evaluation (up to fp32 rounding before the
-// conversion), and the contraction itself stays dense over all (row, column,
-// bird) triples.
+// Two ways to make the factor tiles:
 //
-// Along a window the factor follows a two-multiply recurrence on the row
-// spacing h: with d the offset of a row centre from the bird,
+// Table path (the cell size c = 16 W / G is a whole number of 1/16-px quanta
+// on both axes).  A bird at y = G c + r (0 <= r < c, in quanta) sits at the
+// same offset r - c/2 - j c from the centre of row G + j for every G, so its
+// window is one row of an exact table T[r][j], built once per workgroup.
+// Producer waves copy table rows into the factor tiles of the next chunk of
+// birds while consumer waves run the matrix-core contraction on the current
+// chunk (two LDS buffers, one barrier per chunk).  The tiles carry a halo of
+// window height above and below the output rows, so every window lands in
+// the tile without clipping, and each producer thread clears exactly the
+// window it wrote into the same buffer two chunks earlier.  Workgroups of few-
+// frame batches each take a slice of a frame's birds; a second kernel adds
+// the slices' partial grids in slice order.
+//
+// Recurrence path (any other grid).  Each workgroup generates its factors
+// with a two-multiply recurrence along the window,
 //     F(d + h) = F(d) * R(d),   R(d + h) = R(d) * Q,
 //     R(d) = exp(-(2 d h + h^2) / (2 s^2)),  Q = exp(-h^2 / s^2),
-// started from exact exponentials at the two ends of the window's halves
-// (two independent chains per thread) and restarted every kRestart rows,
-// which bounds the accumulated fp32 error far below the fp16 rounding.  When
-// h > 2 s (windows of a few rows) every factor is an exact exponential.
+// started from exact exponentials at both ends of the window (two chains per
+// thread) and restarted every kRestart rows; when h > 2 s every factor is an
+// exact exponential.
 //
-// Accuracy: each fp16 factor carries a relative rounding error <= 2^-11, so
-// each term of the sum is within about 2^-10 of exact; all terms are positive,
-// so the same relative bound holds for every output, which is <= the frame's
-// maximum.
+// Accuracy: each fp16 factor carries a relative rounding error <= 2^-11 (plus
+// at most a few fp32 ulps before the conversion), so each term of the sum is
+// within about 2^-10 of exact; all terms are positive, so the same relative
+// bound holds for every output, which is <= the frame's maximum.  Every sum
+// is taken in a fixed order, so results are deterministic.
 
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
+#include <algorithm>
 
 #include "internal.h"
 
 namespace flock {
 namespace {
 
-constexpr int kThreads = 256;       // 4 waves
-constexpr int kChunk = 128;         // birds per LDS chunk: one (bird, axis) window per thread
-constexpr int kPitch = kChunk + 8;  // halves per LDS row (16-byte skew between rows)
-constexpr int kRestart = 16;        // rows between exact restarts of the recurrence
+// ---------------------------------------------------------------------------
+// Recurrence path
+// ---------------------------------------------------------------------------
+
+constexpr int kRThreads = 256;       // 4 waves
+constexpr int kRChunk = 128;         // birds per LDS chunk: one (bird, axis) window per thread
+constexpr int kRPitch = kRChunk + 8; // halves per LDS row (16-byte skew between rows)
+constexpr int kRestart = 16;         // rows between exact restarts of the recurrence
 constexpr float kCutSigmas = 6.0f;
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
@@ -65,16 +77,16 @@ struct Geometry {
 };
 
 template <int RM, int RN>
-struct Layout {
+struct RecurLayout {
     static constexpr int kRowsY = 32 * RM;
     static constexpr int kRowsX = 32 * RN;
-    static constexpr int kFactorBytes = (kRowsY + kRowsX) * kPitch * 2;
+    static constexpr int kFactorBytes = (kRowsY + kRowsX) * kRPitch * 2;
     static constexpr int kRedBytes = 4 * 32 * 33 * 4;  // one tile from each wave, padded rows
     static constexpr int kBytes = kFactorBytes > kRedBytes ? kFactorBytes : kRedBytes;
 };
 
 // Write one bird's factors for rows [row0, row0 + nrows) of one axis into a
-// column of buf (row-major, kPitch halves per row); rows outside the window
+// column of buf (row-major, kRPitch halves per row); rows outside the window
 // are left as they are (cleared).  A row just outside the computed window has
 // a factor below 2^-25 (its fp16 value is +0), so float rounding of the
 // bounds cannot change the tile.
@@ -85,7 +97,7 @@ __device__ __forceinline__ void fill_window(_Float16 *col, float pos, float h, f
     if (!recur) {
         for (int row = lo; row <= hi; ++row) {
             const float d = ((float)row + 0.5f) * h - pos;
-            col[(row - row0) * kPitch] = (_Float16)__builtin_amdgcn_exp2f(d * d * neg_k);
+            col[(row - row0) * kRPitch] = (_Float16)__builtin_amdgcn_exp2f(d * d * neg_k);
         }
         return;
     }
@@ -101,8 +113,8 @@ __device__ __forceinline__ void fill_window(_Float16 *col, float pos, float h, f
         float rb = __builtin_amdgcn_exp2f((h - 2.0f * db) * h * neg_k);  // ratio going down
         const int steps = min(kRestart, mid - base + 1);
         for (int i = 0; i < steps; ++i) {
-            col[(base + i - row0) * kPitch] = (_Float16)fa;
-            if (top - i > mid) col[(top - i - row0) * kPitch] = (_Float16)fb;
+            col[(base + i - row0) * kRPitch] = (_Float16)fa;
+            if (top - i > mid) col[(top - i - row0) * kRPitch] = (_Float16)fb;
             fa *= ra;
             ra *= q;
             fb *= rb;
@@ -112,12 +124,12 @@ __device__ __forceinline__ void fill_window(_Float16 *col, float pos, float h, f
 }
 
 template <int RM, int RN>
-__global__ __launch_bounds__(kThreads) void density_kernel(DensityArgs a, Geometry g, int regions_y,
+__global__ __launch_bounds__(kRThreads) void density_recur_kernel(DensityArgs a, Geometry g, int regions_y,
                                                            int regions_x) {
-    using L = Layout<RM, RN>;
+    using L = RecurLayout<RM, RN>;
     __shared__ __align__(16) unsigned char lds[L::kBytes];
     _Float16 *fy = reinterpret_cast<_Float16 *>(lds);
-    _Float16 *fx = fy + L::kRowsY * kPitch;
+    _Float16 *fx = fy + L::kRowsY * kRPitch;
 
     const int regions = regions_y * regions_x;
     const int f = blockIdx.x / regions;
@@ -145,21 +157,21 @@ __global__ __launch_bounds__(kThreads) void density_kernel(DensityArgs a, Geomet
     const int r32 = lane & 31;
     const int kq = (lane >> 5) * 8;
     // thread -> (bird k of the chunk, axis); the bird is fetched one chunk ahead
-    const int k = tid & (kChunk - 1);
-    const bool yaxis = tid < kChunk;
+    const int k = tid & (kRChunk - 1);
+    const bool yaxis = tid < kRChunk;
     int2 p = make_int2(0, 0);
     if (k < n) p = P[k];
-    for (int32_t k0 = 0; k0 < n; k0 += kChunk) {
+    for (int32_t k0 = 0; k0 < n; k0 += kRChunk) {
         // clear both factor tiles (16-byte stores)
         {
             uint4 *z = reinterpret_cast<uint4 *>(lds);
             constexpr int nz = L::kFactorBytes / 16;
             const uint4 zero = make_uint4(0, 0, 0, 0);
 #pragma unroll 4
-            for (int i = tid; i < nz; i += kThreads) z[i] = zero;
+            for (int i = tid; i < nz; i += kRThreads) z[i] = zero;
         }
         const int2 pc = p;
-        if (k0 + kChunk + k < n) p = P[k0 + kChunk + k];
+        if (k0 + kRChunk + k < n) p = P[k0 + kRChunk + k];
         __syncthreads();
         if (k0 + k < n) {
             if (yaxis)
@@ -177,10 +189,10 @@ __global__ __launch_bounds__(kThreads) void density_kernel(DensityArgs a, Geomet
             half8 bx[RN];
 #pragma unroll
             for (int t = 0; t < RN; ++t)
-                bx[t] = *reinterpret_cast<const half8 *>(fx + (t * 32 + r32) * kPitch + kk);
+                bx[t] = *reinterpret_cast<const half8 *>(fx + (t * 32 + r32) * kRPitch + kk);
 #pragma unroll
             for (int m = 0; m < RM; ++m) {
-                const half8 ay = *reinterpret_cast<const half8 *>(fy + (m * 32 + r32) * kPitch + kk);
+                const half8 ay = *reinterpret_cast<const half8 *>(fy + (m * 32 + r32) * kRPitch + kk);
 #pragma unroll
                 for (int t = 0; t < RN; ++t)
                     acc[m][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ay, bx[t], acc[m][t], 0, 0, 0);
@@ -205,7 +217,7 @@ __global__ __launch_bounds__(kThreads) void density_kernel(DensityArgs a, Geomet
             __syncthreads();
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int el = tid + i * kThreads;  // 0..1023 over the 32x32 tile
+                const int el = tid + i * kRThreads;  // 0..1023 over the 32x32 tile
                 const int row = el >> 5, colx = el & 31;
                 const float s = ((red[row * 33 + colx] + red[(32 + row) * 33 + colx]) +
                                  red[(64 + row) * 33 + colx]) + red[(96 + row) * 33 + colx];
@@ -218,11 +230,272 @@ __global__ __launch_bounds__(kThreads) void density_kernel(DensityArgs a, Geomet
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Table path
+// ---------------------------------------------------------------------------
+
+constexpr int kTCons = 4;                        // consumer waves: matrix-core contraction
+constexpr int kTProd = 2;                        // producer waves: one per axis
+constexpr int kTThreads = 64 * (kTCons + kTProd);
+constexpr int kTChunk = 64;                      // birds per chunk: one (bird, axis) window per producer
+constexpr int kTPitch = kTChunk + 8;             // halves per tile row (16-byte skew between rows)
+constexpr int kMaxWin = 48;                      // window rows per axis (table row width)
+constexpr int kSplitTarget = 256;                // workgroups a split launch aims for
+constexpr int kMinSliceBirds = 256;              // birds per slice, at least
+constexpr int kRedTiles = 6;                     // output tiles per round of the final cross-wave sum
+
+// Per-axis table geometry (quanta per cell c, window half-width j, window rows
+// w = 2 j + 1, table row width tw = w rounded up to a multiple of 8 = halo
+// rows per side of a tile).
+struct TableAxis {
+    int c, j, w, tw;
+};
+struct TableGeom {
+    TableAxis ay, ax;
+    int rows_y, rows_x;   // tile rows incl. halos: 32 RM + 2 tw_y, 32 RN + 2 tw_x
+    int buf;              // halves per buffer (Fy tile then Fx tile)
+    int tab_y, tab_x;     // half offsets of the two tables (tab_x == tab_y when they coincide)
+    float neg_k;          // -log2(e) / (2 s^2), in px^-2
+    float scale;          // 1 / (2 pi s^2)
+    int lds_bytes;
+};
+
+__device__ __forceinline__ int32_t floor_div(int32_t v, int32_t c) {
+    const int32_t q = v / c;
+    return (v % c != 0 && v < 0) ? q - 1 : q;
+}
+
+// Producer: copy the window of one bird on one axis into column k of a tile
+// (rows of pitch kTPitch), after clearing the window this thread wrote into
+// the same buffer two chunks earlier (*prev, -1 if none).  Windows are moved
+// as tw rows in groups of eight (the table row is zero past w), and the
+// tile's halos are tw rows high, so every write stays inside the tile.
+__device__ __forceinline__ void put_window(_Float16 *tile, const _Float16 *table, int32_t pos_q,
+                                           const TableAxis &t, int row0, int nrows, int k, bool have,
+                                           int *prev) {
+    const int groups = t.tw >> 3;
+    if (*prev >= 0) {
+        _Float16 *old = tile + *prev;
+        for (int q = 0; q < groups; ++q, old += 8 * kTPitch)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) old[e * kTPitch] = (_Float16)0.0f;
+    }
+    if (!have) {
+        *prev = -1;
+        return;
+    }
+    const int32_t g = floor_div(pos_q, t.c);
+    const int32_t r = pos_q - g * t.c;
+    // first window row relative to the output rows, kept inside the halos
+    const int32_t lo = min(max(g - t.j - row0, -t.tw), nrows);
+    const int off = (lo + t.tw) * kTPitch + k;
+    _Float16 *dst = tile + off;
+    const half8 *src = reinterpret_cast<const half8 *>(table + r * t.tw);
+    for (int q = 0; q < groups; ++q, dst += 8 * kTPitch) {
+        const half8 v = src[q];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dst[e * kTPitch] = v[e];
+    }
+    *prev = off;
+}
+
 template <int RM, int RN>
-hipError_t launch_rm_rn(const DensityArgs &a, const Geometry &g, const DensityPlan &p, hipStream_t stream) {
+__global__ __launch_bounds__(kTThreads) void density_table_kernel(DensityArgs a, TableGeom tg, int regions_y,
+                                                                  int regions_x, int split, float *partial) {
+    constexpr int kRowsY = 32 * RM, kRowsX = 32 * RN;
+    extern __shared__ __align__(16) unsigned char lds[];
+    _Float16 *const sh = reinterpret_cast<_Float16 *>(lds);
+
+    const int per_frame = regions_y * regions_x * split;
+    const int f = blockIdx.x / per_frame;
+    const int rem = blockIdx.x - f * per_frame;
+    const int reg = rem / split;
+    const int sl = rem - reg * split;
+    const int gy0 = (reg / regions_x) * kRowsY;
+    const int gx0 = (reg % regions_x) * kRowsX;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+
+    const int32_t b = a.offsets[f];
+    const int32_t e = a.offsets[f + 1];
+    const bool ok = !(b < 0 || e < b || e > a.total);
+    const int32_t n = ok ? e - b : 0;
+    // this workgroup's slice of the frame's birds
+    const int32_t k0 = (int32_t)((int64_t)n * sl / split);
+    const int32_t k1 = (int32_t)((int64_t)n * (sl + 1) / split);
+    const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
+
+    // the output rows of both buffers start at zero (halo rows are never
+    // read); the tables hold the exact windows
+    {
+        const uint4 zero = make_uint4(0, 0, 0, 0);
+        constexpr int kRowVecs = kTPitch / 8;  // uint4 per tile row
+        for (int i = tid; i < 2 * (kRowsY + kRowsX) * kRowVecs; i += kTThreads) {
+            const int bsel = i / ((kRowsY + kRowsX) * kRowVecs);
+            const int rr = i - bsel * (kRowsY + kRowsX) * kRowVecs;
+            const int row = rr / kRowVecs, v = rr - row * kRowVecs;
+            const int trow = row < kRowsY ? tg.ay.tw + row : tg.rows_y + tg.ax.tw + (row - kRowsY);
+            *reinterpret_cast<uint4 *>(sh + bsel * tg.buf + trow * kTPitch + v * 8) = zero;
+        }
+        auto build = [&](const TableAxis &t, _Float16 *tab) {
+            for (int r = tid; r < t.c; r += kTThreads) {
+                const float base = ((float)r - 0.5f * (float)t.c + (float)(t.j * t.c)) * 0.0625f;
+                const float step = (float)t.c * 0.0625f;
+                for (int jj = 0; jj < t.tw; ++jj) {
+                    const float d = base - (float)jj * step;  // exact: multiples of 1/32 px
+                    tab[r * t.tw + jj] =
+                        jj < t.w ? (_Float16)__builtin_amdgcn_exp2f(d * d * tg.neg_k) : (_Float16)0.0f;
+                }
+            }
+        };
+        build(tg.ay, sh + tg.tab_y);
+        if (tg.tab_x != tg.tab_y) build(tg.ax, sh + tg.tab_x);
+    }
+
+    float16v acc[RM][RN];
+#pragma unroll
+    for (int m = 0; m < RM; ++m)
+#pragma unroll
+        for (int t = 0; t < RN; ++t)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) acc[m][t][j] = 0.0f;
+
+    // producers: wave kTCons makes Fy, wave kTCons + 1 makes Fx; lane = bird of the chunk
+    const bool producer = wave >= kTCons;
+    const bool yaxis = wave == kTCons;
+    const TableAxis ta = yaxis ? tg.ay : tg.ax;
+    const int tile_off = yaxis ? 0 : tg.rows_y * kTPitch;
+    const _Float16 *table = sh + (yaxis ? tg.tab_y : tg.tab_x);
+    const int row0 = yaxis ? gy0 : gx0;
+    const int nrows = yaxis ? kRowsY : kRowsX;
+    int prev[2] = {-1, -1};
+    auto produce = [&](int c, int32_t pos) {
+        const bool have = k0 + c * kTChunk + lane < k1;
+        put_window(sh + (c & 1) * tg.buf + tile_off, table, pos, ta, row0, nrows, lane, have, &prev[c & 1]);
+    };
+    // Producer lanes fetch their axis coordinate kGroup chunks ahead: the
+    // coordinates of group g + 1 are loaded while group g is processed.
+    constexpr int kGroup = 8;
+    int32_t pn[kGroup];
+    auto load_group = [&](int grp) {
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) {
+            const int32_t kb = k0 + (grp * kGroup + i) * kTChunk + lane;
+            pn[i] = 0;
+            if (kb < k1) pn[i] = yaxis ? P[kb].y : P[kb].x;
+        }
+    };
+    if (producer) load_group(0);
+    __syncthreads();  // buffers cleared, tables written
+
+    const int nchunks = (k1 - k0 + kTChunk - 1) / kTChunk;
+    const int r32 = lane & 31;
+    const int kq = (lane >> 5) * 8;
+    for (int grp = 0; grp * kGroup < nchunks; ++grp) {
+        int32_t pc[kGroup];
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) pc[i] = pn[i];
+        if (producer) load_group(grp + 1);
+        if (grp == 0) {
+            if (producer) produce(0, pc[0]);
+            __syncthreads();
+        }
+#pragma unroll
+        for (int i = 0; i < kGroup; ++i) {
+            const int c = grp * kGroup + i;
+            if (c >= nchunks) break;
+            if (producer) {
+                if (c + 1 < nchunks) produce(c + 1, i + 1 < kGroup ? pc[(i + 1) % kGroup] : pn[0]);
+            } else {
+                // this wave's 16 birds of the chunk: one k-step
+                const _Float16 *fy = sh + (c & 1) * tg.buf + tg.ay.tw * kTPitch;
+                const _Float16 *fx = sh + (c & 1) * tg.buf + (tg.rows_y + tg.ax.tw) * kTPitch;
+                const int kk = wave * 16 + kq;
+                half8 bx[RN];
+#pragma unroll
+                for (int t = 0; t < RN; ++t)
+                    bx[t] = *reinterpret_cast<const half8 *>(fx + (t * 32 + r32) * kTPitch + kk);
+#pragma unroll
+                for (int m = 0; m < RM; ++m) {
+                    const half8 ay = *reinterpret_cast<const half8 *>(fy + (m * 32 + r32) * kTPitch + kk);
+#pragma unroll
+                    for (int t = 0; t < RN; ++t)
+                        acc[m][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ay, bx[t], acc[m][t], 0, 0, 0);
+                }
+            }
+            __syncthreads();
+        }
+    }
+
+    // Sum the consumer waves' tiles in a fixed order and store.  Lane l of a
+    // wave holds column (l & 31) and rows 8*(j/4) + 4*(l/32) + (j%4), j = 0..15.
+    float *red = reinterpret_cast<float *>(lds);
+    const size_t cells = (size_t)a.grid_h * a.grid_w;
+    float *out = split > 1 ? partial + ((size_t)f * split + sl) * cells : a.density + (size_t)f * cells;
+    const float scale = split > 1 ? 1.0f : tg.scale;
+    constexpr int kTiles = RM * RN;
+    constexpr int kPerRound = kTiles < kRedTiles ? kTiles : kRedTiles;
+    constexpr int kTile = kTCons * 32 * 33;  // floats per tile: every consumer's partial, padded rows
+#pragma unroll
+    for (int t0 = 0; t0 < kTiles; t0 += kPerRound) {
+        if (!producer) {
+#pragma unroll
+            for (int q = 0; q < kPerRound; ++q) {
+                if (t0 + q >= kTiles) break;
+                const int m = (t0 + q) / RN, t = (t0 + q) % RN;
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int row = 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
+                    red[q * kTile + (wave * 32 + row) * 33 + r32] = acc[m][t][j];
+                }
+            }
+        }
+        __syncthreads();
+        const int ntiles = min(kPerRound, kTiles - t0);
+        for (int el = tid; el < ntiles * 1024; el += kTThreads) {
+            const int q = el >> 10, row = (el >> 5) & 31, colx = el & 31;
+            const float *rq = red + q * kTile;
+            const float v = ((rq[row * 33 + colx] + rq[(32 + row) * 33 + colx]) + rq[(64 + row) * 33 + colx]) +
+                            rq[(96 + row) * 33 + colx];
+            const int m = (t0 + q) / RN, t = (t0 + q) % RN;
+            const int gy = gy0 + m * 32 + row;
+            const int gx = gx0 + t * 32 + colx;
+            if ((ok || split > 1) && gy < a.grid_h && gx < a.grid_w) out[(size_t)gy * a.grid_w + gx] = v * scale;
+        }
+        __syncthreads();
+    }
+}
+
+// density[f][cell] = scale * sum over slices s = 0, 1, ... of partial[f][s][cell].
+__global__ __launch_bounds__(256) void density_reduce_kernel(float *density, const float *partial,
+                                                             int64_t cells, int64_t total, int split,
+                                                             float scale) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+        const int64_t f = i / cells, c = i - f * cells;
+        const float *src = partial + f * split * cells + c;
+        float s = 0.0f;
+        for (int k = 0; k < split; ++k) s += src[k * cells];
+        density[i] = s * scale;
+    }
+}
+
+template <int RM, int RN>
+hipError_t launch_recur(const DensityArgs &a, const Geometry &g, const DensityPlan &p, hipStream_t stream) {
     const long long blocks = (long long)a.n_frames * p.regions_y * p.regions_x;
-    hipLaunchKernelGGL((density_kernel<RM, RN>), dim3((unsigned)blocks), dim3(kThreads), 0, stream, a, g,
+    hipLaunchKernelGGL((density_recur_kernel<RM, RN>), dim3((unsigned)blocks), dim3(kRThreads), 0, stream, a, g,
                        p.regions_y, p.regions_x);
+    return hipGetLastError();
+}
+
+template <int RM, int RN>
+hipError_t launch_table(const DensityArgs &a, const TableGeom &tg, const DensityPlan &p, float *partial,
+                        hipStream_t stream) {
+    const long long blocks = (long long)a.n_frames * p.regions_y * p.regions_x * p.split;
+    const size_t lds = (size_t)tg.lds_bytes;
+    hipLaunchKernelGGL((density_table_kernel<RM, RN>), dim3((unsigned)blocks), dim3(kTThreads), lds, stream, a,
+                       tg, p.regions_y, p.regions_x, p.split, partial);
     return hipGetLastError();
 }
 
@@ -249,30 +522,141 @@ Geometry make_geometry(const DensityArgs &a) {
     return g;
 }
 
+
+// Table geometry for a region shape; false when the table path does not apply
+// (a cell is not a whole number of quanta, a window is wider than kMaxWin rows,
+// or the tiles and tables exceed the LDS budget).
+bool make_table_geom(const DensityArgs &a, int rm, int rn, size_t lds_limit, TableGeom *tg) {
+    if ((16LL * a.height_px) % a.grid_h != 0 || (16LL * a.width_px) % a.grid_w != 0) return false;
+    const double cut_q = 16.0 * kCutSigmas * (double)a.sigma_px;  // window half-width, quanta
+    auto axis = [&](int64_t c, TableAxis *t) {
+        if (c < 1 || c > (1 << 20)) return false;
+        // rows G + j with |j| <= j cover every row centre within cut_q of the bird
+        const double jd = std::ceil(cut_q / (double)c) + 1.0;
+        if (jd > (kMaxWin - 1) / 2) return false;
+        t->c = (int)c;
+        t->j = (int)jd;
+        t->w = 2 * t->j + 1;
+        t->tw = (t->w + 7) / 8 * 8;
+        return true;
+    };
+    if (!axis(16LL * a.height_px / a.grid_h, &tg->ay) || !axis(16LL * a.width_px / a.grid_w, &tg->ax))
+        return false;
+    tg->rows_y = 32 * rm + 2 * tg->ay.tw;
+    tg->rows_x = 32 * rn + 2 * tg->ax.tw;
+    tg->buf = (tg->rows_y + tg->rows_x) * kTPitch;
+    tg->tab_y = 2 * tg->buf;
+    const bool shared = tg->ay.c == tg->ax.c && tg->ay.j == tg->ax.j;
+    tg->tab_x = shared ? tg->tab_y : tg->tab_y + tg->ay.c * tg->ay.tw;
+    const int64_t halves = (int64_t)tg->tab_x + (shared ? (int64_t)tg->ay.c * tg->ay.tw
+                                                        : (int64_t)tg->ax.c * tg->ax.tw);
+    const int64_t red = (int64_t)std::min(rm * rn, kRedTiles) * kTCons * 32 * 33 * 4;
+    const int64_t bytes = std::max<int64_t>(2 * halves, red);
+    if (bytes > (int64_t)lds_limit) return false;
+    tg->lds_bytes = (int)bytes;
+    const double s = (double)a.sigma_px;
+    tg->neg_k = (float)(-1.4426950408889634 / (2.0 * s * s));
+    tg->scale = (float)(1.0 / (2.0 * 3.14159265358979323846 * s * s));
+    return true;
+}
+
+long long shape_regions(const Shape &sh, int grid_w, int grid_h) {
+    return ((grid_h + 32LL * sh.rm - 1) / (32LL * sh.rm)) * ((grid_w + 32LL * sh.rn - 1) / (32LL * sh.rn));
+}
+
+// Ordering of region shapes for the table path: least padded area, then
+// fewest regions.
+bool table_better(const Shape &x, const Shape &y, int grid_w, int grid_h) {
+    const long long rx = shape_regions(x, grid_w, grid_h), ry = shape_regions(y, grid_w, grid_h);
+    const long long ax = rx * x.rm * x.rn, ay = ry * y.rm * y.rn;
+    return ax < ay || (ax == ay && rx < ry);
+}
+
+Shape table_shape(int grid_w, int grid_h) {
+    Shape best = kShapes[0];
+    for (const Shape &sh : kShapes)
+        if (table_better(sh, best, grid_w, grid_h)) best = sh;
+    return best;
+}
+
+// Bird slices per (frame, region): enough workgroups to fill the chip, at
+// least kMinSliceBirds birds per slice on average.
+int table_split(int32_t n_frames, int32_t total, long long regions) {
+    const long long wgs = (long long)n_frames * regions;
+    if (n_frames <= 0 || wgs >= kSplitTarget) return 1;
+    const long long want = (kSplitTarget + wgs - 1) / wgs;
+    const long long cap = std::max<long long>(1, (long long)total / n_frames / kMinSliceBirds);
+    return (int)std::max<long long>(1, std::min<long long>(std::min(want, cap), 64));
+}
+
 }  // namespace
 
-// Choose the output region per workgroup with a small cost model: per bird a
-// region costs its matrix-core time (RM*RN/2 cycles), the factor rows its
-// windows cover and its tile clearing; workgroups spread over the compute
-// units, and a launch never finishes before one workgroup does.
-// FLOCK_DENSITY_SHAPE="rm,rn" forces a region shape (for tuning).
-DensityPlan plan_density(const DensityArgs &a, int n_cus) {
+size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h) {
+    if (n_frames <= 0 || grid_w < 1 || grid_h < 1) return 0;
+    const Shape sh = table_shape(grid_w, grid_h);
+    const int split = table_split(n_frames, total, shape_regions(sh, grid_w, grid_h));
+    if (split <= 1) return 0;
+    return (size_t)n_frames * split * (size_t)grid_w * grid_h * sizeof(float);
+}
+
+// Recurrence path: choose the output region per workgroup with a small cost
+// model: per bird a region costs its matrix-core time (RM*RN/2 cycles), the
+// factor rows its windows cover and its tile clearing; workgroups spread over
+// the compute units, and a launch never finishes before one workgroup does.
+// Table path: the least padded region shape whose tiles fit in LDS, and bird
+// slices when the batch has few (frame, region) pairs.
+// FLOCK_DENSITY_SHAPE="rm,rn" forces a region shape and FLOCK_DENSITY_PATH=
+// "recur" or "table" a path where it applies (for tuning).
+DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit) {
     const int tiles_y = (a.grid_h + 31) / 32;
     const int tiles_x = (a.grid_w + 31) / 32;
     const char *force = std::getenv("FLOCK_DENSITY_SHAPE");
-    if (force) {
-        int rm = 0, rn = 0;
-        if (std::sscanf(force, "%d,%d", &rm, &rn) == 2)
-            for (const Shape &sh : kShapes)
-                if (sh.rm == rm && sh.rn == rn)
-                    return DensityPlan{rm, rn, (tiles_y + rm - 1) / rm, (tiles_x + rn - 1) / rn};
+    const char *path = std::getenv("FLOCK_DENSITY_PATH");
+    const bool force_recur = path && std::strcmp(path, "recur") == 0;
+    const bool force_table = path && std::strcmp(path, "table") == 0;
+    int frm = 0, frn = 0;
+    if (force && std::sscanf(force, "%d,%d", &frm, &frn) == 2) {
+        bool known = false;
+        for (const Shape &sh : kShapes) known |= sh.rm == frm && sh.rn == frn;
+        if (!known) frm = frn = 0;
     }
+    // The table path's single-column LDS writes conflict across banks, so on
+    // batches that already fill the chip the recurrence path is faster; the
+    // table path serves batches with fewer (frame, region) pairs than
+    // workgroups wanted, which it splits by birds.
+    const Shape pref = table_shape(a.grid_w, a.grid_h);
+    const bool few = (long long)a.n_frames * shape_regions(pref, a.grid_w, a.grid_h) < kSplitTarget;
+    if (!force_recur && (few || force_table)) {
+        // table path: the forced shape, else the best shape whose tiles fit
+        const int split_cap = table_split(a.n_frames, a.total, shape_regions(pref, a.grid_w, a.grid_h));
+        TableGeom tg;
+        bool found = false;
+        Shape best = kShapes[0];
+        if (frm) {
+            best = Shape{frm, frn};
+            found = make_table_geom(a, frm, frn, lds_limit, &tg);
+        } else {
+            for (const Shape &sh : kShapes)
+                if ((!found || table_better(sh, best, a.grid_w, a.grid_h)) &&
+                    make_table_geom(a, sh.rm, sh.rn, lds_limit, &tg)) {
+                    best = sh;
+                    found = true;
+                }
+        }
+        if (found) {
+            const long long regions = shape_regions(best, a.grid_w, a.grid_h);
+            const int split = std::min(split_cap, table_split(a.n_frames, a.total, regions));
+            return DensityPlan{1, best.rm, best.rn, (int)((a.grid_h + 32LL * best.rm - 1) / (32LL * best.rm)),
+                               (int)((a.grid_w + 32LL * best.rn - 1) / (32LL * best.rn)), split};
+        }
+    }
+    if (frm) return DensityPlan{0, frm, frn, (tiles_y + frm - 1) / frm, (tiles_x + frn - 1) / frn, 1};
     const double s = (double)a.sigma_px;
     const double hx = (double)a.width_px / a.grid_w, hy = (double)a.height_px / a.grid_h;
     const double lx = std::min(2.0 * kCutSigmas * s / hx + 1.0, (double)a.grid_w);
     const double ly = std::min(2.0 * kCutSigmas * s / hy + 1.0, (double)a.grid_h);
     const double birds = a.n_frames > 0 ? (double)a.total / a.n_frames : 0.0;
-    DensityPlan best{1, 1, tiles_y, tiles_x};
+    DensityPlan best{0, 1, 1, tiles_y, tiles_x, 1};
     double best_t = 1e300;
     for (const Shape &sh : kShapes) {
         if (sh.rm > tiles_y && sh.rm > 1) continue;
@@ -286,23 +670,41 @@ DensityPlan plan_density(const DensityArgs &a, int n_cus) {
         const double t = std::max(blocks * per_block / n_cus, per_block);
         if (t < best_t * 0.999) {
             best_t = t;
-            best = DensityPlan{sh.rm, sh.rn, ry, rx};
+            best = DensityPlan{0, sh.rm, sh.rn, ry, rx, 1};
         }
     }
     return best;
 }
 
-hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, size_t lds_limit,
+hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, size_t lds_limit, float *partial,
                           hipStream_t stream) {
-    (void)lds_limit;
+    hipError_t err = hipErrorInvalidValue;
+    if (p.table) {
+        TableGeom tg;
+        if (!make_table_geom(a, p.rm, p.rn, lds_limit, &tg)) return hipErrorInvalidValue;
+        if (p.split > 1 && !partial) return hipErrorInvalidValue;
+#define FLOCK_SHAPE(RM, RN) \
+    if (p.rm == RM && p.rn == RN) err = launch_table<RM, RN>(a, tg, p, partial, stream);
+        FLOCK_SHAPE(1, 1) FLOCK_SHAPE(1, 2) FLOCK_SHAPE(2, 1) FLOCK_SHAPE(2, 2) FLOCK_SHAPE(1, 4)
+        FLOCK_SHAPE(3, 2) FLOCK_SHAPE(2, 4) FLOCK_SHAPE(3, 4) FLOCK_SHAPE(4, 2) FLOCK_SHAPE(5, 2)
+        FLOCK_SHAPE(4, 1) FLOCK_SHAPE(5, 1)
+#undef FLOCK_SHAPE
+        if (err != hipSuccess || p.split <= 1) return err;
+        const int64_t cells = (int64_t)a.grid_h * a.grid_w;
+        const int64_t total = cells * a.n_frames;
+        const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 4096);
+        hipLaunchKernelGGL(density_reduce_kernel, dim3(blocks), dim3(256), 0, stream, a.density, partial, cells,
+                           total, p.split, tg.scale);
+        return hipGetLastError();
+    }
     const Geometry g = make_geometry(a);
 #define FLOCK_SHAPE(RM, RN) \
-    if (p.rm == RM && p.rn == RN) return launch_rm_rn<RM, RN>(a, g, p, stream);
+    if (p.rm == RM && p.rn == RN) return launch_recur<RM, RN>(a, g, p, stream);
     FLOCK_SHAPE(1, 1) FLOCK_SHAPE(1, 2) FLOCK_SHAPE(2, 1) FLOCK_SHAPE(2, 2) FLOCK_SHAPE(1, 4)
     FLOCK_SHAPE(3, 2) FLOCK_SHAPE(2, 4) FLOCK_SHAPE(3, 4) FLOCK_SHAPE(4, 2) FLOCK_SHAPE(5, 2)
     FLOCK_SHAPE(4, 1) FLOCK_SHAPE(5, 1)
 #undef FLOCK_SHAPE
-    return hipErrorInvalidValue;
+    return err;
 }
 
 }  // namespace flock

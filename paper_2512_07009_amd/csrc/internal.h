@@ -57,13 +57,18 @@ struct DensityArgs {
 };
 
 struct DensityPlan {
+    int table;                // 1: exact factor tables; 0: recurrence
     int rm;                   // 32-row gy tiles per workgroup region
     int rn;                   // 32-column gx tiles per workgroup region
     int regions_y, regions_x; // regions per frame
+    int split;                // bird slices per (frame, region); > 1 adds partial grids afterwards
 };
 
-DensityPlan plan_density(const DensityArgs &a, int n_cus);
-hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, size_t lds_limit,
+DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit);
+// Workspace for the partial grids of a split launch (0 if none); depends on the
+// batch shape and grid only, and bounds every plan for that shape.
+size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h);
+hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, size_t lds_limit, float *partial,
                           hipStream_t stream);
 
 }  // namespace flock

@@ -264,6 +264,56 @@ def test_density_input_order_path_gpu(max_fp):
     assert_density_close(got, ref, np.diff(off), 30.0, tag=f"max_fp {max_fp}")
 
 
+@pytest.mark.parametrize("path", ["table", "recur"])
+@pytest.mark.parametrize("w,h,gx,gy,sigma,frames", [
+    (1920, 1080, 128, 72, 30.0, 20), (3840, 2160, 512, 288, 20.0, 3), (3840, 2160, 256, 144, 45.0, 6),
+])
+def test_density_paths_gpu(path, w, h, gx, gy, sigma, frames, monkeypatch):
+    """Both ways of making the factor tiles (exact tables / recurrence) agree with the oracle."""
+    monkeypatch.setenv("FLOCK_DENSITY_PATH", path)
+    xy, off = wl.random_batch(gx + frames, frames, 1500, width_px=w, height_px=h)
+    got = run_density(xy, off, w, h, gx, gy, sigma)
+    ref = oracle.density_frames(xy, off, w, h, gx, gy, sigma)
+    worst = assert_density_close(got, ref, np.diff(off), sigma, tag=f"{path} {gx}x{gy}")
+    print(f"density {path} {gx}x{gy}: worst rel err {worst:.2e}")
+
+
+def test_density_bird_slices_gpu():
+    """Few frames split into bird slices whose partial grids are added afterwards,
+    including frames with fewer birds than slices and an empty frame."""
+    rng = np.random.default_rng(77)
+    frames = [np.stack([rng.integers(0, 16 * 1920, n), rng.integers(0, 16 * 1080, n)], 1).astype(np.int32)
+              for n in (6000, 3, 0, 700)]
+    xy, off = wl.pack(frames)
+    assert flock.lib().density_frames_workspace(len(frames), xy.shape[0], 128, 72) > 0
+    got = run_density(xy, off, 1920, 1080, 128, 72, 30.0)
+    ref = oracle.density_frames(xy, off, 1920, 1080, 128, 72, 30.0)
+    assert_density_close(got, ref, np.diff(off), 30.0, tag="slices")
+    assert not got[2].any()
+
+
+def test_density_workspace_gpu():
+    import ctypes
+    rng = np.random.default_rng(5)
+    xy, off = wl.pack([np.stack([rng.integers(0, 16 * 1920, 4000), rng.integers(0, 16 * 1080, 4000)],
+                                1).astype(np.int32)])
+    dxy, doff = dev_batch(xy, off)
+    lib = flock.lib()
+    need = lib.density_frames_workspace(1, xy.shape[0], 128, 72)
+    assert need > 0
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    out = torch.empty((1, 72, 128), dtype=torch.float32, device="cuda")
+    args = (ctypes.c_void_p(dxy.data_ptr()), ctypes.c_void_p(doff.data_ptr()), 1, xy.shape[0], 0, 1920, 1080,
+            128, 72, ctypes.c_float(30.0), ctypes.c_void_p(out.data_ptr()))
+    assert lib.density_frames(*args, ctypes.c_void_p(ws.data_ptr()), need - 1, None) == flock.binding.FLOCK_ENOMEM
+    ref = oracle.density_frames(xy, off, 1920, 1080, 128, 72, 30.0)
+    for w, nbytes in ((ctypes.c_void_p(ws.data_ptr()), need), (None, 0)):  # caller's, then the library's
+        out.fill_(-1.0)
+        assert lib.density_frames(*args, w, nbytes, None) == 0
+        torch.cuda.synchronize()
+        assert_density_close(out.cpu().numpy(), ref, np.diff(off), 30.0, tag="workspace")
+
+
 def test_density_single_bird_peak_gpu():
     sigma = 30.0
     # bird exactly at the centre of cell (40, 30) of a 128 x 72 grid on 1920 x 1080
