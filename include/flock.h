@@ -124,15 +124,20 @@ size_t cluster_frames_workspace(int32_t n_frames, int32_t total, int32_t max_fra
  *   sigma_px              bandwidth, finite, > 0.
  *   density               device out, float[n_frames][grid_h][grid_w].
  *   workspace             as for cluster_frames, sized by
- *                         density_frames_workspace(...).
- * The result is deterministic (fixed summation order).
+ *                         density_frames_workspace(...).  Batches with few
+ *                         frames are split into bird slices whose partial
+ *                         grids are kept there and added in slice order.
+ * The result is deterministic (fixed summation order).  Frames whose offsets
+ * are invalid (checked only with FLOCK_VALIDATE) leave their grid unspecified.
  */
 flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
                             int32_t total, int32_t max_frame_points, int32_t width_px,
                             int32_t height_px, int32_t grid_w, int32_t grid_h, float sigma_px,
                             float *density, void *workspace, size_t workspace_bytes, void *stream);
 
-/* Bytes of workspace density_frames needs for this batch shape (may be 0). */
+/* Bytes of workspace density_frames needs for this batch shape and grid
+ * (0 when no split is needed); the same value bounds every call with these
+ * four arguments, whatever the frame extent and sigma. */
 size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h);
 
 /* Text of the last error on this thread ("" if none); valid until the next
