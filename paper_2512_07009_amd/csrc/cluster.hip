@@ -173,7 +173,6 @@ constexpr int kMaxOffsets = 16;
 // reach = 1 + (E - 1) / side with side >= max(1, floor(E / sqrt 2)) > (E - 1) / 2.
 // So the full stencil has at most 5 x 5 cells.
 constexpr int kMaxStencil = 25;
-constexpr int kMaxFar = 8;  // forward stencil cells beyond the adjacent four (reach <= 2)
 constexpr int kBorderLanes = 8;  // lanes that share one border candidate
 // Points per thread held in registers during the sort: the planner keeps a
 // resident frame at <= kThreads * kPtsPerThread points.
@@ -184,10 +183,17 @@ constexpr int kPtsPerThread = 10;
 __device__ __forceinline__ int32_t pk_x(uint32_t v) { return (int32_t)(v & 0xffffu); }
 __device__ __forceinline__ int32_t pk_y(uint32_t v) { return (int32_t)(v >> 16); }
 
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// Squared distance of two packed points, per axis clamped to E + 1, on both
+// 16-bit halves at once: |a - b| = max - min, then dx^2 + dy^2 by one 16-bit
+// dot product (<= 2 (E + 1)^2 < 2^31 for E <= 32766).
 __device__ __forceinline__ int32_t sq_dist_pk(uint32_t a, uint32_t b, int32_t e1) {
-    const int32_t dx = clamp_abs(pk_x(a) - pk_x(b), e1);
-    const int32_t dy = clamp_abs(pk_y(a) - pk_y(b), e1);
-    return __mul24(dx, dx) + __mul24(dy, dy);
+    const u16x2 ua = __builtin_bit_cast(u16x2, a), ub = __builtin_bit_cast(u16x2, b);
+    const u16x2 lim = {(unsigned short)e1, (unsigned short)e1};
+    const u16x2 d = __builtin_elementwise_min(__builtin_elementwise_max(ua, ub) - __builtin_elementwise_min(ua, ub),
+                                              lim);
+    return (int32_t)__builtin_amdgcn_udot2(d, d, 0u, false);
 }
 
 // Cell geometry of one frame (relative coordinates).
@@ -301,13 +307,50 @@ __device__ void build_stencil(int32_t reach, int32_t side, const Radius &r, int 
     }
 }
 
-// Join core cell clist[j] with its forward neighbours (odx/ody, noff <= K
+// True if some core of sorted points [a0, a1) lies within eps of some core of
+// [b0, b1), whose cell rectangle starts at (bx0, by0).  Points go four at a
+// time from each side, so each step keeps eight LDS reads in flight; cores of
+// A beyond eps of B's rectangle are skipped.
+__device__ __forceinline__ bool cells_touch(const uint32_t *pxy, const uint8_t *score, int32_t a0, int32_t a1,
+                                            int32_t b0, int32_t b1, int32_t bx0, int32_t by0, int32_t side,
+                                            const Radius &r) {
+    for (int32_t qa = a0; qa < a1; qa += 4) {
+        uint32_t va[4];
+        bool ok[4];
+        bool any = false;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int32_t q = min(qa + i, a1 - 1);
+            va[i] = pxy[q];
+            ok[i] = (qa + i < a1) & (score[q] != 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            ok[i] = ok[i] && rect_near2(pk_x(va[i]), pk_y(va[i]), bx0, by0, side, r.e1) <= r.e2;
+            any |= ok[i];
+        }
+        if (!any) continue;
+        for (int32_t qb = b0; qb < b1; qb += 4) {
+            bool hit = false;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int32_t q = min(qb + j, b1 - 1);
+                const uint32_t vb = pxy[q];
+                const bool cb = (qb + j < b1) & (score[q] != 0);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) hit |= ok[i] & cb & (sq_dist_pk(va[i], vb, r.e1) <= r.e2);
+            }
+            if (hit) return true;
+        }
+    }
+    return false;
+}
+
+// Join core cell clist[j] with its forward neighbours (offsets odx/ody, noff
 // of them): a neighbour holding a core is joined when some core pair across
 // the two cells is within eps.  All cores of a cell form one node (its
-// smallest core index), since any two points of a cell are neighbours.
-// The neighbour cell words and the first step of each neighbour's find are
-// loaded together, so one thread keeps several LDS reads in flight.
-template <int K>
+// smallest core index), since any two points of a cell are neighbours.  The
+// loop is kept rolled: one copy of the pair test keeps the kernel's code small.
 __device__ __forceinline__ void union_cell(int32_t j, const uint16_t *clist, const uint32_t *cell,
                                            int32_t *parent, const uint32_t *pxy, const uint8_t *score,
                                            const Grid &g, const Radius &r, const int *odx, const int *ody,
@@ -316,51 +359,21 @@ __device__ __forceinline__ void union_cell(int32_t j, const uint16_t *clist, con
     const int32_t ay = div_small(ca, g.ncx, inv_ncx), ax = ca - ay * g.ncx;
     const uint32_t wa = cell[ca];
     const int32_t a0 = (int32_t)(wa & 0xffffu), a1 = (int32_t)(cell[ca + 1] & 0xffffu);
-    int32_t cb[K], bxs[K], bys[K];
-    uint32_t wb[K], wb1[K];
-#pragma unroll
-    for (int o = 0; o < K; ++o) {
-        const int32_t bx = ax + odx[o < noff ? o : 0], by = ay + ody[o < noff ? o : 0];
-        const bool ok = o < noff && bx >= 0 && bx < g.ncx && by < g.ncy;
-        bxs[o] = bx;
-        bys[o] = by;
-        cb[o] = ok ? by * g.ncx + bx : -1;
-        const int32_t c = ok ? cb[o] : ca;
-        wb[o] = cell[c];
-        wb1[o] = cell[c + 1];
-    }
-    int32_t pb[K];
-#pragma unroll
-    for (int o = 0; o < K; ++o) {
-        const int32_t nb = (int32_t)(wb[o] >> 16);
-        const bool has = cb[o] >= 0 && nb != (int32_t)kNone;
-        cb[o] = has ? cb[o] : -1;
-        pb[o] = has ? ld_rlx<kGroup>(parent + nb) : 0;
-    }
-    int32_t ra = uf_find<kGroup>(parent, (int32_t)(wa >> 16));
-#pragma unroll
-    for (int o = 0; o < K; ++o) {
-        if (cb[o] < 0) continue;
-        // pb is an ancestor of the neighbour's node: its root is the node's root
-        const int32_t rb = uf_find<kGroup>(parent, pb[o]);
-        ra = uf_find<kGroup>(parent, ra);
+    const int32_t na = (int32_t)(wa >> 16);
+#pragma unroll 1
+    for (int o = 0; o < noff; ++o) {
+        const int32_t bx = ax + odx[o], by = ay + ody[o];
+        if (bx < 0 || bx >= g.ncx || by >= g.ncy) continue;
+        const int32_t cb = by * g.ncx + bx;
+        const uint32_t wb = cell[cb];
+        const int32_t nb = (int32_t)(wb >> 16);
+        if (nb == (int32_t)kNone) continue;
+        const int32_t ra = uf_find<kGroup>(parent, na);
+        const int32_t rb = uf_find<kGroup>(parent, nb);
         if (ra == rb) continue;  // already one tree
-        // B's rectangle, to skip cores of A that cannot reach it
-        const int32_t bx0 = bxs[o] * g.side, by0 = bys[o] * g.side;
-        const int32_t b0 = (int32_t)(wb[o] & 0xffffu), b1 = (int32_t)(wb1[o] & 0xffffu);
-        bool hit = false;
-        for (int32_t qa = a0; qa < a1 && !hit; ++qa) {
-            if (!score[qa]) continue;
-            const uint32_t va = pxy[qa];
-            if (rect_near2(pk_x(va), pk_y(va), bx0, by0, g.side, r.e1) > r.e2) continue;
-            for (int32_t qb = b0; qb < b1; ++qb) {
-                if (score[qb] && sq_dist_pk(va, pxy[qb], r.e1) <= r.e2) {
-                    hit = true;
-                    break;
-                }
-            }
-        }
-        if (hit) uf_unite<kGroup>(parent, ra, rb);
+        const int32_t b0 = (int32_t)(wb & 0xffffu), b1 = (int32_t)(cell[cb + 1] & 0xffffu);
+        if (cells_touch(pxy, score, a0, a1, b0, b1, bx * g.side, by * g.side, g.side, r))
+            uf_unite<kGroup>(parent, ra, rb);
     }
 }
 
@@ -414,25 +427,21 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         s_nlist = 0;
         s_ncells = 0;
     }
-    if (n > a.cap_points) {
-        if (a.big_path) return;  // the multi-workgroup path owns this frame
-        __syncthreads();
-        cluster_frame_inplace(a, f, b, n, smem, &s_red);
-        return;
-    }
+    if (n > a.cap_points && a.big_path) return;  // the multi-workgroup path owns this frame
 
     const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
     const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
 
     // 1. bounding box; each thread keeps its points (i = tid + k * kThreads)
     //    in registers for the sort
+    const bool fits = n <= a.cap_points;
     int2 pt[kPtsPerThread];
 #pragma unroll
     for (int k = 0; k < kPtsPerThread; ++k) {
         const int32_t i = tid + k * kThreads;
-        pt[k] = i < n ? P[i] : make_int2(0, 0);
+        pt[k] = fits && i < n ? P[i] : make_int2(0, 0);
     }
-    {
+    if (fits) {
         int xmn = INT_MAX, ymn = INT_MAX, xmx = INT_MIN, ymx = INT_MIN;
 #pragma unroll
         for (int k = 0; k < kPtsPerThread; ++k) {
@@ -457,7 +466,10 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     }
     const int32_t x0 = s_bbox[0], y0 = s_bbox[1];
     const uint32_t wx = (uint32_t)(s_bbox[2] - x0), wy = (uint32_t)(s_bbox[3] - y0);
-    if (wx > 0xffffu || wy > 0xffffu) {  // extent beyond 16 bits: keep the data off chip
+    // frames above the LDS capacity, or whose extent needs more than 16 bits,
+    // keep their data off chip
+    if (!fits || wx > 0xffffu || wy > 0xffffu) {
+        __syncthreads();
         cluster_frame_inplace(a, f, b, n, smem, &s_red);
         return;
     }
@@ -611,12 +623,14 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         // second pass most farther pairs are already in one tree.
         const int32_t ncl = s_ncells;
         const float inv_ncx = 1.0f / (float)g.ncx;
-        for (int32_t j = tid; j < ncl; j += kThreads)
-            union_cell<4>(j, clist, cell, parent, pxy, score, g, r, s_odx[0], s_ody[0], s_noff[0], inv_ncx);
-        __syncthreads();
-        for (int32_t j = tid; j < ncl; j += kThreads)
-            union_cell<kMaxFar>(j, clist, cell, parent, pxy, score, g, r, s_odx[1], s_ody[1], s_noff[1], inv_ncx);
-        __syncthreads();
+        // adjacent cells first; by the second pass most farther pairs are
+        // already in one tree
+        for (int pass = 0; pass < 2; ++pass) {
+            for (int32_t j = tid; j < ncl; j += kThreads)
+                union_cell(j, clist, cell, parent, pxy, score, g, r, s_odx[pass], s_ody[pass], s_noff[pass],
+                           inv_ncx);
+            __syncthreads();
+        }
     } else {
         // coarsened grid: point-level unions (each pair once: the later point
         // of a cell, or the point in the earlier cell, does the work)
