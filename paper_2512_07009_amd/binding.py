@@ -76,6 +76,18 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _workspace(nbytes: int, dev, stream):
+    """Scratch for one call.  torch's caching allocator ties a block to the
+    stream it was allocated on, so the block is also recorded on the stream
+    the kernels run on: it is not handed out again before they finish."""
+    if not nbytes:
+        return None
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    if stream is not None:
+        ws.record_stream(stream)
+    return ws
+
+
 def _batch(xy: torch.Tensor, offsets: torch.Tensor):
     if not (xy.is_cuda and offsets.is_cuda):
         raise ValueError("xy and offsets must be device tensors")
@@ -112,7 +124,7 @@ def cluster_frames(xy: torch.Tensor, offsets: torch.Tensor, eps_px: float, min_p
     else:
         labels, kind, ncl = out
     ws_bytes = lib().cluster_frames_workspace(F, T, int(max_frame_points))
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
+    ws = _workspace(ws_bytes, dev, stream)
     with torch.cuda.device(dev):
         st = lib().cluster_frames(_ptr(xy), _ptr(offsets), F, T, int(max_frame_points),
                                   eps_to_quanta(eps_px), int(min_pts), _ptr(labels), _ptr(kind),
@@ -133,7 +145,7 @@ def density_frames(xy: torch.Tensor, offsets: torch.Tensor, width_px: int, heigh
     dens = out if out is not None else torch.empty((max(F, 0), grid_h, grid_w), dtype=torch.float32,
                                                   device=dev)
     ws_bytes = lib().density_frames_workspace(F, T, int(grid_w), int(grid_h))
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev) if ws_bytes else None
+    ws = _workspace(ws_bytes, dev, stream)
     with torch.cuda.device(dev):
         st = lib().density_frames(_ptr(xy), _ptr(offsets), F, T, int(max_frame_points),
                                   int(width_px), int(height_px),
