@@ -326,7 +326,7 @@ __device__ __forceinline__ bool cells_touch(const uint32_t *pxy, const uint8_t *
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            ok[i] = ok[i] && rect_near2(pk_x(va[i]), pk_y(va[i]), bx0, by0, side, r.e1) <= r.e2;
+            ok[i] = ok[i] & (rect_near2(pk_x(va[i]), pk_y(va[i]), bx0, by0, side, r.e1) <= r.e2);
             any |= ok[i];
         }
         if (!any) continue;
@@ -363,7 +363,7 @@ __device__ __forceinline__ void union_cell(int32_t j, const uint16_t *clist, con
 #pragma unroll 1
     for (int o = 0; o < noff; ++o) {
         const int32_t bx = ax + odx[o], by = ay + ody[o];
-        if (bx < 0 || bx >= g.ncx || by >= g.ncy) continue;
+        if ((bx < 0) | (bx >= g.ncx) | (by >= g.ncy)) continue;
         const int32_t cb = by * g.ncx + bx;
         const uint32_t wb = cell[cb];
         const int32_t nb = (int32_t)(wb >> 16);
@@ -698,7 +698,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
             int32_t best = -1;
             for (int s = gl; s < ns; s += kBorderLanes) {
                 const int32_t rx = cx + s_sdx[s], ry = cy + s_sdy[s];
-                if (rx < 0 || rx >= g.ncx || ry < 0 || ry >= g.ncy) continue;
+                if ((rx < 0) | (rx >= g.ncx) | (ry < 0) | (ry >= g.ncy)) continue;
                 const int32_t c = ry * g.ncx + rx;
                 const uint32_t cw = cell[c];
                 if ((cw >> 16) == kNone) continue;  // no core in this cell
