@@ -117,7 +117,11 @@ struct ClusterPlan {
 
 ClusterPlan plan_cluster(int32_t max_frame_points, size_t lds_limit) {
     ClusterPlan p;
-    const int32_t limit = flock::cluster_max_cap_points(lds_limit);
+    int32_t limit = flock::cluster_max_cap_points(lds_limit);
+    // FLOCK_CLUSTER_CAP lowers the on-chip capacity (for tuning the split
+    // between the on-chip and the multi-workgroup paths)
+    const char *cap = std::getenv("FLOCK_CLUSTER_CAP");
+    if (cap && std::atoi(cap) > 0) limit = std::min(limit, std::atoi(cap));
     p.cap_points = (max_frame_points > 0 && max_frame_points < limit) ? max_frame_points : limit;
     const size_t reserve = 1024;  // static shared variables
     const int64_t avail = (int64_t)lds_limit - (int64_t)reserve - 14 * (int64_t)p.cap_points - 4;

@@ -20,14 +20,13 @@
 // on both axes).  A bird at y = G c + r (0 <= r < c, in quanta) sits at the
 // same offset r - c/2 - j c from the centre of row G + j for every G, so its
 // window is one row of an exact table T[r][j], built once per workgroup.
-// Producer waves copy table rows into the factor tiles of the next chunk of
-// birds while consumer waves run the matrix-core contraction on the current
-// chunk (two LDS buffers, one barrier per chunk).  The tiles carry a halo of
-// window height above and below the output rows, so every window lands in
-// the tile without clipping, and each producer thread clears exactly the
-// window it wrote into the same buffer two chunks earlier.  Workgroups of few-
-// frame batches each take a slice of a frame's birds; a second kernel adds
-// the slices' partial grids in slice order.
+// Each of the eight waves of a workgroup works on its own: it copies the
+// windows of 16 birds from the table into private factor tiles (a halo of
+// one window height above and below the output rows takes the windows of
+// birds near or past the region's edge without clipping), then runs one MFMA
+// k-step over them; the copy of the next 16 birds overlaps that contraction.
+// Workgroups of few-frame batches each take a slice of a frame's birds; a
+// second kernel adds the slices' partial grids in slice order.
 //
 // Recurrence path (any other grid).  Each workgroup generates its factors
 // with a two-multiply recurrence along the window,
@@ -235,73 +234,72 @@ __global__ __launch_bounds__(kRThreads) void density_recur_kernel(DensityArgs a,
 // Table path
 // ---------------------------------------------------------------------------
 
-constexpr int kTCons = 4;                        // consumer waves: matrix-core contraction
-constexpr int kTProd = 2;                        // producer waves: one per axis
-constexpr int kTThreads = 64 * (kTCons + kTProd);
-constexpr int kTChunk = 64;                      // birds per chunk: one (bird, axis) window per producer
-constexpr int kTPitch = kTChunk + 8;             // halves per tile row (16-byte skew between rows)
+constexpr int kWWaves = 8;                       // waves per workgroup, each one self-sufficient
+constexpr int kWThreads = 64 * kWWaves;
+constexpr int kWBirds = 16;                      // birds per wave step: one MFMA k-step
+constexpr int kWPitch = kWBirds + 8;             // halves per private tile row (48 B: reads hit 8 bank groups)
 constexpr int kMaxWin = 48;                      // window rows per axis (table row width)
 constexpr int kSplitTarget = 256;                // workgroups a split launch aims for
 constexpr int kMinSliceBirds = 256;              // birds per slice, at least
-constexpr int kRedTiles = 6;                     // output tiles per round of the final cross-wave sum
+constexpr int kRedTiles = 3;                     // output tiles per round of the final cross-wave sum
 
 // Per-axis table geometry (quanta per cell c, window half-width j, window rows
 // w = 2 j + 1, table row width tw = w rounded up to a multiple of 8 = halo
 // rows per side of a tile).
 struct TableAxis {
-    int c, j, w, tw;
+    int32_t c, j, w, tw;
 };
 struct TableGeom {
     TableAxis ay, ax;
     int rows_y, rows_x;   // tile rows incl. halos: 32 RM + 2 tw_y, 32 RN + 2 tw_x
-    int buf;              // halves per buffer (Fy tile then Fx tile)
+    int wave_tile;        // halves of one wave's private tiles (Fy then Fx)
     int tab_y, tab_x;     // half offsets of the two tables (tab_x == tab_y when they coincide)
     float neg_k;          // -log2(e) / (2 s^2), in px^-2
     float scale;          // 1 / (2 pi s^2)
     int lds_bytes;
 };
 
-__device__ __forceinline__ int32_t floor_div(int32_t v, int32_t c) {
-    const int32_t q = v / c;
-    return (v % c != 0 && v < 0) ? q - 1 : q;
+// floor(v / c) for |v| < 2^24, 1 <= c < 2^20: a float reciprocal, then one
+// correction step either way.
+__device__ __forceinline__ int32_t floor_div(int32_t v, int32_t c, float inv_c) {
+    int32_t q = (int32_t)floorf((float)v * inv_c);
+    if (q * c > v) --q;
+    else if ((q + 1) * c <= v) ++q;
+    return q;
 }
 
-// Producer: copy the window of one bird on one axis into column k of a tile
-// (rows of pitch kTPitch), after clearing the window this thread wrote into
-// the same buffer two chunks earlier (*prev, -1 if none).  Windows are moved
-// as tw rows in groups of eight (the table row is zero past w), and the
-// tile's halos are tw rows high, so every write stays inside the tile.
-__device__ __forceinline__ void put_window(_Float16 *tile, const _Float16 *table, int32_t pos_q,
-                                           const TableAxis &t, int row0, int nrows, int k, bool have,
-                                           int *prev) {
-    const int groups = t.tw >> 3;
-    if (*prev >= 0) {
-        _Float16 *old = tile + *prev;
-        for (int q = 0; q < groups; ++q, old += 8 * kTPitch)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) old[e * kTPitch] = (_Float16)0.0f;
-    }
-    if (!have) {
-        *prev = -1;
-        return;
-    }
-    const int32_t g = floor_div(pos_q, t.c);
-    const int32_t r = pos_q - g * t.c;
+// One lane's half of a bird's window on one axis: table groups [q0, q1) of
+// eight rows go to column k of the wave's tile (rows of pitch kWPitch).  The
+// table row is zero past w, and the tile's halos are tw rows high, so every
+// write stays inside the tile.
+__device__ __forceinline__ void put_half_window(_Float16 *tile, const _Float16 *table, int32_t pos_q,
+                                                const TableAxis &t, float inv_c, int row0, int nrows, int k,
+                                                int q0, int q1, bool have) {
+    if (!have) return;
+    const int32_t g = floor_div(pos_q, t.c, inv_c);
+    // exact for |pos_q| < 2^24; beyond that the bird is far outside any grid
+    // this path takes and only the table index needs keeping in range
+    const int32_t r = min(max(pos_q - g * t.c, 0), t.c - 1);
     // first window row relative to the output rows, kept inside the halos
     const int32_t lo = min(max(g - t.j - row0, -t.tw), nrows);
-    const int off = (lo + t.tw) * kTPitch + k;
+    const int off = (lo + t.tw + 8 * q0) * kWPitch + k;
     _Float16 *dst = tile + off;
     const half8 *src = reinterpret_cast<const half8 *>(table + r * t.tw);
-    for (int q = 0; q < groups; ++q, dst += 8 * kTPitch) {
+    for (int q = q0; q < q1; ++q, dst += 8 * kWPitch) {
         const half8 v = src[q];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dst[e * kTPitch] = v[e];
+        for (int e = 0; e < 8; ++e) dst[e * kWPitch] = v[e];
     }
-    *prev = off;
 }
 
+// Eight waves, each with private factor tiles for kWBirds birds: a wave takes
+// every eighth block of kWBirds birds of its slice, copies their windows from
+// the tables into its tiles (lane = bird, axis and half of the window), and
+// runs one MFMA k-step over them for every tile of the region.  No barrier is
+// needed between waves until the final sum; the next block's copy overlaps
+// the current block's matrix-core work.
 template <int RM, int RN>
-__global__ __launch_bounds__(kTThreads) void density_table_kernel(DensityArgs a, TableGeom tg, int regions_y,
+__global__ __launch_bounds__(kWThreads) void density_table_kernel(DensityArgs a, TableGeom tg, int regions_y,
                                                                   int regions_x, int split, float *partial) {
     constexpr int kRowsY = 32 * RM, kRowsX = 32 * RN;
     extern __shared__ __align__(16) unsigned char lds[];
@@ -327,20 +325,15 @@ __global__ __launch_bounds__(kTThreads) void density_table_kernel(DensityArgs a,
     const int32_t k1 = (int32_t)((int64_t)n * (sl + 1) / split);
     const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
 
-    // the output rows of both buffers start at zero (halo rows are never
-    // read); the tables hold the exact windows
+    _Float16 *const tile = sh + wave * tg.wave_tile;
     {
+        // this wave's tiles start at zero (halo rows too: never read, but cheap)
+        uint4 *z = reinterpret_cast<uint4 *>(tile);
         const uint4 zero = make_uint4(0, 0, 0, 0);
-        constexpr int kRowVecs = kTPitch / 8;  // uint4 per tile row
-        for (int i = tid; i < 2 * (kRowsY + kRowsX) * kRowVecs; i += kTThreads) {
-            const int bsel = i / ((kRowsY + kRowsX) * kRowVecs);
-            const int rr = i - bsel * (kRowsY + kRowsX) * kRowVecs;
-            const int row = rr / kRowVecs, v = rr - row * kRowVecs;
-            const int trow = row < kRowsY ? tg.ay.tw + row : tg.rows_y + tg.ax.tw + (row - kRowsY);
-            *reinterpret_cast<uint4 *>(sh + bsel * tg.buf + trow * kTPitch + v * 8) = zero;
-        }
+        for (int i = lane; i < tg.wave_tile / 8; i += 64) z[i] = zero;
+        // the tables hold the exact windows
         auto build = [&](const TableAxis &t, _Float16 *tab) {
-            for (int r = tid; r < t.c; r += kTThreads) {
+            for (int r = tid; r < t.c; r += kWThreads) {
                 const float base = ((float)r - 0.5f * (float)t.c + (float)(t.j * t.c)) * 0.0625f;
                 const float step = (float)t.c * 0.0625f;
                 for (int jj = 0; jj < t.tw; ++jj) {
@@ -362,103 +355,104 @@ __global__ __launch_bounds__(kTThreads) void density_table_kernel(DensityArgs a,
 #pragma unroll
             for (int j = 0; j < 16; ++j) acc[m][t][j] = 0.0f;
 
-    // producers: wave kTCons makes Fy, wave kTCons + 1 makes Fx; lane = bird of the chunk
-    const bool producer = wave >= kTCons;
-    const bool yaxis = wave == kTCons;
+    // copy roles: lane -> (bird bk of the block, axis, half of the window)
+    const int bk = lane & (kWBirds - 1);
+    const bool yaxis = (lane & 16) == 0;
+    const int half = lane >> 5;
     const TableAxis ta = yaxis ? tg.ay : tg.ax;
-    const int tile_off = yaxis ? 0 : tg.rows_y * kTPitch;
-    const _Float16 *table = sh + (yaxis ? tg.tab_y : tg.tab_x);
+    const int groups = ta.tw >> 3;
+    const int q0 = half ? (groups + 1) >> 1 : 0;
+    const int q1 = half ? groups : (groups + 1) >> 1;
+    _Float16 *const atile = tile + (yaxis ? 0 : tg.rows_y * kWPitch);
+    const _Float16 *const table = sh + (yaxis ? tg.tab_y : tg.tab_x);
     const int row0 = yaxis ? gy0 : gx0;
     const int nrows = yaxis ? kRowsY : kRowsX;
-    int prev[2] = {-1, -1};
-    auto produce = [&](int c, int32_t pos) {
-        const bool have = k0 + c * kTChunk + lane < k1;
-        put_window(sh + (c & 1) * tg.buf + tile_off, table, pos, ta, row0, nrows, lane, have, &prev[c & 1]);
-    };
-    // Producer lanes fetch their axis coordinate kGroup chunks ahead: the
-    // coordinates of group g + 1 are loaded while group g is processed.
-    constexpr int kGroup = 8;
-    int32_t pn[kGroup];
-    auto load_group = [&](int grp) {
-#pragma unroll
-        for (int i = 0; i < kGroup; ++i) {
-            const int32_t kb = k0 + (grp * kGroup + i) * kTChunk + lane;
-            pn[i] = 0;
-            if (kb < k1) pn[i] = yaxis ? P[kb].y : P[kb].x;
-        }
-    };
-    if (producer) load_group(0);
-    __syncthreads();  // buffers cleared, tables written
-
-    const int nchunks = (k1 - k0 + kTChunk - 1) / kTChunk;
+    // MFMA roles: lane -> (tile row, eight birds)
     const int r32 = lane & 31;
     const int kq = (lane >> 5) * 8;
-    for (int grp = 0; grp * kGroup < nchunks; ++grp) {
-        int32_t pc[kGroup];
+    const _Float16 *const fy = tile + tg.ay.tw * kWPitch;
+    const _Float16 *const fx = tile + (tg.rows_y + tg.ax.tw) * kWPitch;
+
+    const float inv_c = 1.0f / (float)ta.c;
+    const int32_t nblk = (k1 - k0 + kWBirds - 1) / kWBirds;
+    // each lane's coordinate for this wave's next kAhead blocks (register ring)
+    constexpr int kAhead = 4;
+    auto coord = [&](int32_t blk) -> int32_t {
+        const int32_t kb = k0 + blk * kWBirds + bk;
+        return kb < k1 ? (yaxis ? P[kb].y : P[kb].x) : 0;
+    };
+    int32_t pos[kAhead];
 #pragma unroll
-        for (int i = 0; i < kGroup; ++i) pc[i] = pn[i];
-        if (producer) load_group(grp + 1);
-        if (grp == 0) {
-            if (producer) produce(0, pc[0]);
-            __syncthreads();
-        }
+    for (int j = 0; j < kAhead; ++j) pos[j] = coord(wave + j * kWWaves);
+    __syncthreads();  // tables written
+
+    for (int32_t i = 0; wave + i * kWWaves < nblk; i += kAhead) {
 #pragma unroll
-        for (int i = 0; i < kGroup; ++i) {
-            const int c = grp * kGroup + i;
-            if (c >= nchunks) break;
-            if (producer) {
-                if (c + 1 < nchunks) produce(c + 1, i + 1 < kGroup ? pc[(i + 1) % kGroup] : pn[0]);
-            } else {
-                // this wave's 16 birds of the chunk: one k-step
-                const _Float16 *fy = sh + (c & 1) * tg.buf + tg.ay.tw * kTPitch;
-                const _Float16 *fx = sh + (c & 1) * tg.buf + (tg.rows_y + tg.ax.tw) * kTPitch;
-                const int kk = wave * 16 + kq;
-                half8 bx[RN];
+        for (int j = 0; j < kAhead; ++j) {
+            const int32_t blk = wave + (i + j) * kWWaves;
+            if (blk >= nblk) break;
+            const int32_t kb = k0 + blk * kWBirds + bk;
+            put_half_window(atile, table, pos[j], ta, inv_c, row0, nrows, bk, q0, q1, kb < k1);
+            pos[j] = coord(blk + kAhead * kWWaves);  // fetched kAhead blocks ahead
+            // this wave's own writes are read back below; LDS keeps one wave's
+            // accesses in order, and the fence keeps the compiler from moving them
+            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            half8 bx[RN];
+#pragma unroll
+            for (int t = 0; t < RN; ++t)
+                bx[t] = *reinterpret_cast<const half8 *>(fx + (t * 32 + r32) * kWPitch + kq);
+#pragma unroll
+            for (int m = 0; m < RM; ++m) {
+                const half8 ay = *reinterpret_cast<const half8 *>(fy + (m * 32 + r32) * kWPitch + kq);
 #pragma unroll
                 for (int t = 0; t < RN; ++t)
-                    bx[t] = *reinterpret_cast<const half8 *>(fx + (t * 32 + r32) * kTPitch + kk);
-#pragma unroll
-                for (int m = 0; m < RM; ++m) {
-                    const half8 ay = *reinterpret_cast<const half8 *>(fy + (m * 32 + r32) * kTPitch + kk);
-#pragma unroll
-                    for (int t = 0; t < RN; ++t)
-                        acc[m][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ay, bx[t], acc[m][t], 0, 0, 0);
-                }
+                    acc[m][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ay, bx[t], acc[m][t], 0, 0, 0);
             }
-            __syncthreads();
+            // clear the output rows for the next block (16-byte stores of whole
+            // rows, after this wave's operand reads, which LDS keeps in order);
+            // halo rows are never read and keep whatever the windows left there
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int i = lane; i < 2 * (kRowsY + kRowsX); i += 64) {
+                const int row = i >> 1;
+                const int trow = row < kRowsY ? tg.ay.tw + row : tg.rows_y + tg.ax.tw + (row - kRowsY);
+                *reinterpret_cast<half8 *>(tile + trow * kWPitch + (i & 1) * 8) = half8{};
+            }
+            __builtin_amdgcn_wave_barrier();
         }
     }
+    __syncthreads();  // every wave is done with its tiles: the space holds the final sum
 
-    // Sum the consumer waves' tiles in a fixed order and store.  Lane l of a
-    // wave holds column (l & 31) and rows 8*(j/4) + 4*(l/32) + (j%4), j = 0..15.
+    // Sum the waves' tiles in a fixed order and store.  Lane l of a wave holds
+    // column (l & 31) and rows 8*(j/4) + 4*(l/32) + (j%4), j = 0..15.
     float *red = reinterpret_cast<float *>(lds);
     const size_t cells = (size_t)a.grid_h * a.grid_w;
     float *out = split > 1 ? partial + ((size_t)f * split + sl) * cells : a.density + (size_t)f * cells;
     const float scale = split > 1 ? 1.0f : tg.scale;
     constexpr int kTiles = RM * RN;
     constexpr int kPerRound = kTiles < kRedTiles ? kTiles : kRedTiles;
-    constexpr int kTile = kTCons * 32 * 33;  // floats per tile: every consumer's partial, padded rows
+    constexpr int kTile = kWWaves * 32 * 33;  // floats per tile: every wave's partial, padded rows
 #pragma unroll
     for (int t0 = 0; t0 < kTiles; t0 += kPerRound) {
-        if (!producer) {
 #pragma unroll
-            for (int q = 0; q < kPerRound; ++q) {
-                if (t0 + q >= kTiles) break;
-                const int m = (t0 + q) / RN, t = (t0 + q) % RN;
+        for (int q = 0; q < kPerRound; ++q) {
+            if (t0 + q >= kTiles) break;
+            const int m = (t0 + q) / RN, t = (t0 + q) % RN;
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const int row = 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
-                    red[q * kTile + (wave * 32 + row) * 33 + r32] = acc[m][t][j];
-                }
+            for (int j = 0; j < 16; ++j) {
+                const int row = 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
+                red[q * kTile + (wave * 32 + row) * 33 + r32] = acc[m][t][j];
             }
         }
         __syncthreads();
         const int ntiles = min(kPerRound, kTiles - t0);
-        for (int el = tid; el < ntiles * 1024; el += kTThreads) {
+        for (int el = tid; el < ntiles * 1024; el += kWThreads) {
             const int q = el >> 10, row = (el >> 5) & 31, colx = el & 31;
-            const float *rq = red + q * kTile;
-            const float v = ((rq[row * 33 + colx] + rq[(32 + row) * 33 + colx]) + rq[(64 + row) * 33 + colx]) +
-                            rq[(96 + row) * 33 + colx];
+            const float *rq = red + q * kTile + row * 33 + colx;
+            float v = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kWWaves; ++w) v += rq[w * 32 * 33];
             const int m = (t0 + q) / RN, t = (t0 + q) % RN;
             const int gy = gy0 + m * 32 + row;
             const int gx = gx0 + t * 32 + colx;
@@ -494,7 +488,7 @@ hipError_t launch_table(const DensityArgs &a, const TableGeom &tg, const Density
                         hipStream_t stream) {
     const long long blocks = (long long)a.n_frames * p.regions_y * p.regions_x * p.split;
     const size_t lds = (size_t)tg.lds_bytes;
-    hipLaunchKernelGGL((density_table_kernel<RM, RN>), dim3((unsigned)blocks), dim3(kTThreads), lds, stream, a,
+    hipLaunchKernelGGL((density_table_kernel<RM, RN>), dim3((unsigned)blocks), dim3(kWThreads), lds, stream, a,
                        tg, p.regions_y, p.regions_x, p.split, partial);
     return hipGetLastError();
 }
@@ -544,13 +538,13 @@ bool make_table_geom(const DensityArgs &a, int rm, int rn, size_t lds_limit, Tab
         return false;
     tg->rows_y = 32 * rm + 2 * tg->ay.tw;
     tg->rows_x = 32 * rn + 2 * tg->ax.tw;
-    tg->buf = (tg->rows_y + tg->rows_x) * kTPitch;
-    tg->tab_y = 2 * tg->buf;
+    tg->wave_tile = (tg->rows_y + tg->rows_x) * kWPitch;
+    tg->tab_y = kWWaves * tg->wave_tile;
     const bool shared = tg->ay.c == tg->ax.c && tg->ay.j == tg->ax.j;
     tg->tab_x = shared ? tg->tab_y : tg->tab_y + tg->ay.c * tg->ay.tw;
     const int64_t halves = (int64_t)tg->tab_x + (shared ? (int64_t)tg->ay.c * tg->ay.tw
                                                         : (int64_t)tg->ax.c * tg->ax.tw);
-    const int64_t red = (int64_t)std::min(rm * rn, kRedTiles) * kTCons * 32 * 33 * 4;
+    const int64_t red = (int64_t)std::min(rm * rn, kRedTiles) * kWWaves * 32 * 33 * 4;
     const int64_t bytes = std::max<int64_t>(2 * halves, red);
     if (bytes > (int64_t)lds_limit) return false;
     tg->lds_bytes = (int)bytes;
