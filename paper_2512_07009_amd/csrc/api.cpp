@@ -152,7 +152,11 @@ size_t cluster_frames_workspace(int32_t n_frames, int32_t total, int32_t max_fra
 }
 
 size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h) {
-    return flock::density_workspace_bytes(n_frames, total, grid_w, grid_h);
+    const DeviceInfo *dev = nullptr;
+    int n_cus = 256;
+    if (device_info(&dev) == FLOCK_OK) n_cus = dev->n_cus;
+    g_error.clear();
+    return flock::density_workspace_bytes(n_frames, total, grid_w, grid_h, n_cus);
 }
 
 flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
@@ -266,10 +270,9 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     a.sigma_px = sigma_px;
     a.density = density;
     const flock::DensityPlan plan = flock::plan_density(a, dev->n_cus, dev->lds_per_block);
-    const long long blocks = (long long)n_frames * plan.regions_y * plan.regions_x * plan.split;
-    if (blocks > 0x7fffffffLL) return fail(FLOCK_EUNSUPPORTED, "batch too large for one launch");
+    if (plan.blocks > 0x7fffffffLL) return fail(FLOCK_EUNSUPPORTED, "batch too large for one launch");
     // a split launch keeps partial grids in the workspace
-    const size_t need = plan.split > 1 ? flock::density_workspace_bytes(n_frames, total, grid_w, grid_h) : 0;
+    const size_t need = plan.split > 1 ? (size_t)n_frames * plan.split * (size_t)grid_w * grid_h * sizeof(float) : 0;
     if (workspace && workspace_bytes < need)
         return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
     if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
@@ -279,7 +282,7 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
         err = hipMallocAsync(&ws, need, s);
         if (err != hipSuccess) return hip_fail(err, "workspace allocation");
     }
-    err = flock::launch_density(a, plan, dev->lds_per_block, static_cast<float *>(ws), s);
+    err = flock::launch_density(a, plan, static_cast<float *>(ws), s);
     if (need > 0 && !workspace) {
         const hipError_t ferr = hipFreeAsync(ws, s);
         if (err == hipSuccess) err = ferr;

@@ -6,27 +6,27 @@
 //     c = 1 / (2 pi s^2),
 // separates into per-axis factors Fy[gy][i] = exp(-(cy - y_i)^2 / (2 s^2)) and
 // Fx[gx][i] = exp(-(cx - x_i)^2 / (2 s^2)), so D = c * Fy . Fx^T: a dense
-// contraction over the birds of the frame, run on v_mfma_f32_32x32x16_f16
-// with fp16 factors and fp32 accumulation.
+// contraction over the birds of the frame, run on the matrix cores with fp16
+// factors and fp32 accumulation.
 //
 // A factor below 2^-25 rounds to +0 in fp16, and exp(-t^2/2) < 2^-25 for
 // |t| > 5.9, so a bird has nonzero factors only in the rows within 6 s of it
 // (its window); every other factor is +0 in either evaluation, and the
 // contraction stays dense over all (row, column, bird) triples.
 //
-// Two ways to make the factor tiles:
+// Two ways to make the operands:
 //
-// Table path (the cell size c = 16 W / G is a whole number of 1/16-px quanta
+// Gather path (the cell size c = 16 W / G is a whole number of 1/16-px quanta
 // on both axes).  A bird at y = G c + r (0 <= r < c, in quanta) sits at the
-// same offset r - c/2 - j c from the centre of row G + j for every G, so its
-// window is one row of an exact table T[r][j], built once per workgroup.
-// Each of the eight waves of a workgroup works on its own: it copies the
-// windows of 16 birds from the table into private factor tiles (a halo of
-// one window height above and below the output rows takes the windows of
-// birds near or past the region's edge without clipping), then runs one MFMA
-// k-step over them; the copy of the next 16 birds overlaps that contraction.
-// Workgroups of few-frame batches each take a slice of a frame's birds; a
-// second kernel adds the slices' partial grids in slice order.
+// same offset (n + 1/2) c - r from the centre of row G + n for every G, so its
+// factors are one row of an exact table indexed by r, built in LDS once per
+// workgroup.  Each lane of a wave builds its own v_mfma_f32_16x16x32_f16
+// operands from that table (one clamped index, one 32-bit read giving the
+// factors of two 16-row tiles), with no tile writes and no barriers; the
+// next k-step's operands are gathered while the current one's MFMAs run.
+// Waves sharing a frame region add their tiles in a fixed order at the end;
+// batches with few (frame, region) pairs also split frames into bird slices
+// whose partial grids a second kernel adds in slice order.
 //
 // Recurrence path (any other grid).  Each workgroup generates its factors
 // with a two-multiply recurrence along the window,
@@ -42,6 +42,7 @@
 // bound holds for every output, which is <= the frame's maximum.  Every sum
 // is taken in a fixed order, so results are deterministic.
 
+#include <climits>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -231,32 +232,43 @@ __global__ __launch_bounds__(kRThreads) void density_recur_kernel(DensityArgs a,
 
 
 // ---------------------------------------------------------------------------
-// Table path
+// Gather path
 // ---------------------------------------------------------------------------
 
-constexpr int kWWaves = 8;                       // waves per workgroup, each one self-sufficient
-constexpr int kWThreads = 64 * kWWaves;
-constexpr int kWBirds = 16;                      // birds per wave step: one MFMA k-step
-constexpr int kWPitch = kWBirds + 8;             // halves per private tile row (48 B: reads hit 8 bank groups)
-constexpr int kMaxWin = 48;                      // window rows per axis (table row width)
-constexpr int kSplitTarget = 256;                // workgroups a split launch aims for
-constexpr int kMinSliceBirds = 256;              // birds per slice, at least
-constexpr int kRedTiles = 3;                     // output tiles per round of the final cross-wave sum
+constexpr int kGWaves = 4;                 // waves per workgroup
+constexpr int kGThreads = 64 * kGWaves;
+constexpr int kGStep = 32;                 // birds per MFMA k-step (16 x 16 x 32)
+constexpr int kGRedTiles = 8;              // 16 x 16 tiles per round of the cross-wave sum
+constexpr int kGMaxTableBytes = 96 * 1024; // both factor tables
+constexpr int kGMinWaveBirds = 192;        // birds per wave, at least, when a launch splits frames
+constexpr int32_t kGFar = 1 << 28;         // bird term that clamps every row to a zero entry
 
-// Per-axis table geometry (quanta per cell c, window half-width j, window rows
-// w = 2 j + 1, table row width tw = w rounded up to a multiple of 8 = halo
-// rows per side of a tile).
-struct TableAxis {
-    int32_t c, j, w, tw;
+typedef float float4v __attribute__((ext_vector_type(4)));
+
+// Factor table of one axis.  Row r (the bird's offset within its cell, in
+// quanta, 0 <= r < c) holds the factors of cells G + n, n = -j .. j, as
+// T(i) = f((i - 1 - j + 1/2) c - r) for i = 1 .. 2 j + 1 and T(i) = 0
+// elsewhere; its entry i (i = -16 .. PW - 1) is the pair (T(i), T(i + 16)), so
+// one 32-bit read gives a bird's factors for two 16-row tiles.
+struct GatherAxis {
+    int32_t c;      // quanta per cell
+    int32_t j;      // window half-width, cells (2 j + 3 <= PW)
+    int32_t tab;    // byte offset of the table in LDS
 };
-struct TableGeom {
-    TableAxis ay, ax;
-    int rows_y, rows_x;   // tile rows incl. halos: 32 RM + 2 tw_y, 32 RN + 2 tw_x
-    int wave_tile;        // halves of one wave's private tiles (Fy then Fx)
-    int tab_y, tab_x;     // half offsets of the two tables (tab_x == tab_y when they coincide)
-    float neg_k;          // -log2(e) / (2 s^2), in px^-2
-    float scale;          // 1 / (2 pi s^2)
+
+struct GatherGeom {
+    GatherAxis ay, ax;
+    int pw;           // 32 or 64
+    float neg_k;      // -log2(e) / (2 s^2), px^-2
+    float scale;      // 1 / (2 pi s^2)
+    int table_bytes;  // the tables (one when both axes agree), 16-byte aligned
     int lds_bytes;
+};
+
+// One bird as a lane reads it: per axis the byte offset of its table row and
+// 4 (j + 17 - G), G its cell.
+struct GBird {
+    int32_t rb_y, g_y, rb_x, g_x;
 };
 
 // floor(v / c) for |v| < 2^24, 1 <= c < 2^20: a float reciprocal, then one
@@ -268,195 +280,250 @@ __device__ __forceinline__ int32_t floor_div(int32_t v, int32_t c, float inv_c) 
     return q;
 }
 
-// One lane's half of a bird's window on one axis: table groups [q0, q1) of
-// eight rows go to column k of the wave's tile (rows of pitch kWPitch).  The
-// table row is zero past w, and the tile's halos are tw rows high, so every
-// write stays inside the tile.
-__device__ __forceinline__ void put_half_window(_Float16 *tile, const _Float16 *table, int32_t pos_q,
-                                                const TableAxis &t, float inv_c, int row0, int nrows, int k,
-                                                int q0, int q1, bool have) {
-    if (!have) return;
-    const int32_t g = floor_div(pos_q, t.c, inv_c);
-    // exact for |pos_q| < 2^24; beyond that the bird is far outside any grid
-    // this path takes and only the table index needs keeping in range
-    const int32_t r = min(max(pos_q - g * t.c, 0), t.c - 1);
-    // first window row relative to the output rows, kept inside the halos
-    const int32_t lo = min(max(g - t.j - row0, -t.tw), nrows);
-    const int off = (lo + t.tw + 8 * q0) * kWPitch + k;
-    _Float16 *dst = tile + off;
-    const half8 *src = reinterpret_cast<const half8 *>(table + r * t.tw);
-    for (int q = q0; q < q1; ++q, dst += 8 * kWPitch) {
-        const half8 v = src[q];
+template <int PW>
+__device__ __forceinline__ void stage_axis(int32_t q, const GatherAxis &t, float inv_c, int32_t *rb, int32_t *g) {
+    // exact for |q| < 2^24; beyond that the bird is far outside any grid and
+    // only the table row needs keeping in range
+    const int32_t G = floor_div(q, t.c, inv_c);
+    const int32_t r = min(max(q - G * t.c, 0), t.c - 1);
+    *rb = t.tab + 4 * (PW + 16) * r;
+    *g = 4 * (t.j + 17 - G);
+}
+
+// A bird's factor pair for tiles M and M + 1 (M even) of a lane: with
+// v = 4 (R0 + (lane & 15)) + 4 (j + 17 - G), the entry's byte offset in the
+// bird's row is clamp(v + 64 M, 0, 4 (PW + 15)) (16 rows of 4 bytes per
+// tile).  An index clamped from below or above holds two zeros, as do the
+// true factors there, so the clamp is exact.  Constant bounds make it one
+// v_med3, and the 64 M goes into the read's offset field.
+template <int M, int PW>
+__device__ __forceinline__ uint32_t factor_pair(const unsigned char *lds, int32_t rb, int32_t v) {
+    const int32_t o = min(max(v, -64 * M), 4 * (PW + 15) - 64 * M);
+    return *reinterpret_cast<const uint32_t *>(lds + rb + o + 64 * M);
+}
+
+// Operands of tiles M and M + 1 from the pairs of eight birds.
+template <int M, int PW>
+__device__ __forceinline__ void operands(half8 &lo, half8 &hi, const int32_t (&rb)[8], const int32_t (&v)[8],
+                                         const unsigned char *lds) {
+    uint32_t w[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) dst[e * kWPitch] = v[e];
+    for (int e = 0; e < 8; ++e) w[e] = factor_pair<M, PW>(lds, rb[e], v[e]);
+    uint32_t l4[4], h4[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        l4[e] = __builtin_amdgcn_perm(w[2 * e + 1], w[2 * e], 0x05040100u);  // low halves: tile M
+        h4[e] = __builtin_amdgcn_perm(w[2 * e + 1], w[2 * e], 0x07060302u);  // high halves: tile M + 1
+    }
+    lo = __builtin_bit_cast(half8, l4);
+    hi = __builtin_bit_cast(half8, h4);
+}
+
+template <int TN, int PW, int N = 0>
+__device__ __forceinline__ void operands_x(half8 (&bx)[TN], const int32_t (&rb)[8], const int32_t (&v)[8],
+                                           const unsigned char *lds) {
+    if constexpr (N < TN) {
+        half8 hi;
+        operands<N, PW>(bx[N], hi, rb, v, lds);
+        if constexpr (N + 1 < TN) bx[N + 1] = hi;
+        operands_x<TN, PW, N + 2>(bx, rb, v, lds);
     }
 }
 
-// Eight waves, each with private factor tiles for kWBirds birds: a wave takes
-// every eighth block of kWBirds birds of its slice, copies their windows from
-// the tables into its tiles (lane = bird, axis and half of the window), and
-// runs one MFMA k-step over them for every tile of the region.  No barrier is
-// needed between waves until the final sum; the next block's copy overlaps
-// the current block's matrix-core work.
-template <int RM, int RN>
-__global__ __launch_bounds__(kWThreads) void density_table_kernel(DensityArgs a, TableGeom tg, int regions_y,
-                                                                  int regions_x, int split, float *partial) {
-    constexpr int kRowsY = 32 * RM, kRowsX = 32 * RN;
-    extern __shared__ __align__(16) unsigned char lds[];
-    _Float16 *const sh = reinterpret_cast<_Float16 *>(lds);
+template <int TM, int TN, int PW, int M = 0>
+__device__ __forceinline__ void contract_y(float4v (&acc)[TM][TN], const half8 (&bx)[TN], const int32_t (&rb)[8],
+                                           const int32_t (&v)[8], const unsigned char *lds) {
+    if constexpr (M < TM) {
+        half8 a0, a1;
+        operands<M, PW>(a0, a1, rb, v, lds);
+#pragma unroll
+        for (int n = 0; n < TN; ++n) acc[M][n] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a0, bx[n], acc[M][n], 0, 0, 0);
+        if constexpr (M + 1 < TM) {
+#pragma unroll
+            for (int n = 0; n < TN; ++n)
+                acc[M + 1][n] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a1, bx[n], acc[M + 1][n], 0, 0, 0);
+        }
+        contract_y<TM, TN, PW, M + 2>(acc, bx, rb, v, lds);
+    }
+}
 
-    const int per_frame = regions_y * regions_x * split;
-    const int f = blockIdx.x / per_frame;
-    const int rem = blockIdx.x - f * per_frame;
-    const int reg = rem / split;
-    const int sl = rem - reg * split;
-    const int gy0 = (reg / regions_x) * kRowsY;
-    const int gx0 = (reg % regions_x) * kRowsX;
+// One workgroup of four waves.  A work item is (frame, output region of
+// 16 TM rows x 16 TN columns, slice of the frame's birds); `waves` waves share
+// an item, each taking a contiguous part of the slice, and their tiles are
+// added in a fixed order at the end (deterministic).  Every wave stages its
+// own birds (lane = bird) and needs no barrier until that final sum.  With
+// split > 1 the slices' grids go to `partial` for a second kernel to add.
+template <int TM, int TN, int PW>
+__global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) void density_gather_kernel(DensityArgs a, GatherGeom gg, int regions_y,
+                                                                   int regions_x, int split, int waves,
+                                                                   long long items, float *partial) {
+    extern __shared__ __align__(16) unsigned char lds[];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
 
-    const int32_t b = a.offsets[f];
-    const int32_t e = a.offsets[f + 1];
-    const bool ok = !(b < 0 || e < b || e > a.total);
-    const int32_t n = ok ? e - b : 0;
-    // this workgroup's slice of the frame's birds
-    const int32_t k0 = (int32_t)((int64_t)n * sl / split);
-    const int32_t k1 = (int32_t)((int64_t)n * (sl + 1) / split);
+    // the factor tables (exact: every distance is a multiple of 1/32 px)
+    auto build = [&](const GatherAxis &t) {
+        auto T = [&](int r, int i) -> _Float16 {
+            if (i < 1 || i > 2 * t.j + 1) return (_Float16)0.0f;
+            const float d = (((float)(i - 1 - t.j) + 0.5f) * (float)t.c - (float)r) * 0.0625f;
+            return (_Float16)__builtin_amdgcn_exp2f(d * d * gg.neg_k);
+        };
+        uint32_t *tab = reinterpret_cast<uint32_t *>(lds + t.tab);
+        const int nent = t.c * (PW + 16);
+        for (int e = tid; e < nent; e += kGThreads) {
+            const int r = e / (PW + 16), i = e % (PW + 16) - 16;
+            const _Float16 lo = T(r, i), hi = T(r, i + 16);
+            tab[e] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+        }
+    };
+    build(gg.ay);
+    if (gg.ax.tab != gg.ay.tab) build(gg.ax);
+
+    // this wave's item and its part of the item's birds
+    const int per_wg = kGWaves / waves;
+    const long long item = (long long)blockIdx.x * per_wg + wave / waves;
+    const int part = wave % waves;
+    const bool active = item < items;
+    const int regions = regions_y * regions_x;
+    int f = 0, reg = 0, sl = 0;
+    if (active) {
+        sl = (int)(item % split);
+        const long long fr = item / split;
+        reg = (int)(fr % regions);
+        f = (int)(fr / regions);
+    }
+    const int row0 = (reg / regions_x) * 16 * TM;
+    const int col0 = (reg % regions_x) * 16 * TN;
+    int32_t b = 0, n = 0;
+    if (active) {
+        b = a.offsets[f];
+        const int32_t e = a.offsets[f + 1];
+        n = (b < 0 || e < b || e > a.total) ? 0 : e - b;
+    }
+    const int32_t k0 = (int32_t)((int64_t)n * sl / split), k1 = (int32_t)((int64_t)n * (sl + 1) / split);
+    const int32_t p0 = k0 + (int32_t)((int64_t)(k1 - k0) * part / waves);
+    const int32_t p1 = k0 + (int32_t)((int64_t)(k1 - k0) * (part + 1) / waves);
     const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
 
-    _Float16 *const tile = sh + wave * tg.wave_tile;
-    {
-        // this wave's tiles start at zero (halo rows too: never read, but cheap)
-        uint4 *z = reinterpret_cast<uint4 *>(tile);
-        const uint4 zero = make_uint4(0, 0, 0, 0);
-        for (int i = lane; i < tg.wave_tile / 8; i += 64) z[i] = zero;
-        // the tables hold the exact windows
-        auto build = [&](const TableAxis &t, _Float16 *tab) {
-            for (int r = tid; r < t.c; r += kWThreads) {
-                const float base = ((float)r - 0.5f * (float)t.c + (float)(t.j * t.c)) * 0.0625f;
-                const float step = (float)t.c * 0.0625f;
-                for (int jj = 0; jj < t.tw; ++jj) {
-                    const float d = base - (float)jj * step;  // exact: multiples of 1/32 px
-                    tab[r * t.tw + jj] =
-                        jj < t.w ? (_Float16)__builtin_amdgcn_exp2f(d * d * tg.neg_k) : (_Float16)0.0f;
-                }
-            }
-        };
-        build(tg.ay, sh + tg.tab_y);
-        if (tg.tab_x != tg.tab_y) build(tg.ax, sh + tg.tab_x);
-    }
+    GBird *stage = reinterpret_cast<GBird *>(lds + gg.table_bytes) + wave * 2 * kGStep;
+    const float inv_cy = 1.0f / (float)gg.ay.c, inv_cx = 1.0f / (float)gg.ax.c;
+    const int r16 = lane & 15, grp = lane >> 4;
+    const int32_t yoff = 4 * (row0 + r16), xoff = 4 * (col0 + r16);
 
-    float16v acc[RM][RN];
+    float4v acc[TM][TN];
 #pragma unroll
-    for (int m = 0; m < RM; ++m)
+    for (int m = 0; m < TM; ++m)
 #pragma unroll
-        for (int t = 0; t < RN; ++t)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) acc[m][t][j] = 0.0f;
+        for (int t = 0; t < TN; ++t) acc[m][t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
 
-    // copy roles: lane -> (bird bk of the block, axis, half of the window)
-    const int bk = lane & (kWBirds - 1);
-    const bool yaxis = (lane & 16) == 0;
-    const int half = lane >> 5;
-    const TableAxis ta = yaxis ? tg.ay : tg.ax;
-    const int groups = ta.tw >> 3;
-    const int q0 = half ? (groups + 1) >> 1 : 0;
-    const int q1 = half ? groups : (groups + 1) >> 1;
-    _Float16 *const atile = tile + (yaxis ? 0 : tg.rows_y * kWPitch);
-    const _Float16 *const table = sh + (yaxis ? tg.tab_y : tg.tab_x);
-    const int row0 = yaxis ? gy0 : gx0;
-    const int nrows = yaxis ? kRowsY : kRowsX;
-    // MFMA roles: lane -> (tile row, eight birds)
-    const int r32 = lane & 31;
-    const int kq = (lane >> 5) * 8;
-    const _Float16 *const fy = tile + tg.ay.tw * kWPitch;
-    const _Float16 *const fx = tile + (tg.rows_y + tg.ax.tw) * kWPitch;
-
-    const float inv_c = 1.0f / (float)ta.c;
-    const int32_t nblk = (k1 - k0 + kWBirds - 1) / kWBirds;
-    // each lane's coordinate for this wave's next kAhead blocks (register ring)
-    constexpr int kAhead = 4;
-    auto coord = [&](int32_t blk) -> int32_t {
-        const int32_t kb = k0 + blk * kWBirds + bk;
-        return kb < k1 ? (yaxis ? P[kb].y : P[kb].x) : 0;
+    // Software pipeline over k-steps of 32 birds: while the matrix cores run
+    // step s, the wave stages the birds of step s + 1 (lane = bird and axis,
+    // coordinates fetched two steps ahead) and gathers that step's x
+    // operands, so both kinds of work are in flight in one instruction stream.
+    const int32_t nsteps = (p1 - p0 + kGStep - 1) / kGStep;
+    const int sbird = lane & (kGStep - 1);
+    const bool sx = lane >= kGStep;  // lanes 0-31 stage the y axis, 32-63 the x axis
+    const GatherAxis &sax = sx ? gg.ax : gg.ay;
+    const float sinv = sx ? inv_cx : inv_cy;
+    auto coord = [&](int32_t t) -> int32_t {
+        const int32_t k = p0 + t * kGStep + sbird;
+        return k < p1 ? (sx ? P[k].x : P[k].y) : INT_MIN;
     };
-    int32_t pos[kAhead];
+    auto put = [&](int32_t t, int32_t q) {
+        int32_t rb = sax.tab, g = kGFar;  // beyond the slice: factors 0
+        if (q != INT_MIN) stage_axis<PW>(q, sax, sinv, &rb, &g);
+        reinterpret_cast<int2 *>(stage + (t & 1) * kGStep + sbird)[sx] = make_int2(rb, g);
+        // a wave's LDS accesses stay in program order; the fences keep the
+        // compiler from moving them
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+    auto x_operands = [&](int32_t t, half8 (&bx)[TN]) {
+        const GBird *sb = stage + (t & 1) * kGStep + 8 * grp;  // this lane's eight birds of step t
+        int32_t rbx[8], vx[8];
 #pragma unroll
-    for (int j = 0; j < kAhead; ++j) pos[j] = coord(wave + j * kWWaves);
-    __syncthreads();  // tables written
-
-    for (int32_t i = 0; wave + i * kWWaves < nblk; i += kAhead) {
-#pragma unroll
-        for (int j = 0; j < kAhead; ++j) {
-            const int32_t blk = wave + (i + j) * kWWaves;
-            if (blk >= nblk) break;
-            const int32_t kb = k0 + blk * kWBirds + bk;
-            put_half_window(atile, table, pos[j], ta, inv_c, row0, nrows, bk, q0, q1, kb < k1);
-            pos[j] = coord(blk + kAhead * kWWaves);  // fetched kAhead blocks ahead
-            // this wave's own writes are read back below; LDS keeps one wave's
-            // accesses in order, and the fence keeps the compiler from moving them
-            __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            half8 bx[RN];
-#pragma unroll
-            for (int t = 0; t < RN; ++t)
-                bx[t] = *reinterpret_cast<const half8 *>(fx + (t * 32 + r32) * kWPitch + kq);
-#pragma unroll
-            for (int m = 0; m < RM; ++m) {
-                const half8 ay = *reinterpret_cast<const half8 *>(fy + (m * 32 + r32) * kWPitch + kq);
-#pragma unroll
-                for (int t = 0; t < RN; ++t)
-                    acc[m][t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ay, bx[t], acc[m][t], 0, 0, 0);
-            }
-            // clear the output rows for the next block (16-byte stores of whole
-            // rows, after this wave's operand reads, which LDS keeps in order);
-            // halo rows are never read and keep whatever the windows left there
-            __builtin_amdgcn_wave_barrier();
-#pragma unroll
-            for (int i = lane; i < 2 * (kRowsY + kRowsX); i += 64) {
-                const int row = i >> 1;
-                const int trow = row < kRowsY ? tg.ay.tw + row : tg.rows_y + tg.ax.tw + (row - kRowsY);
-                *reinterpret_cast<half8 *>(tile + trow * kWPitch + (i & 1) * 8) = half8{};
-            }
-            __builtin_amdgcn_wave_barrier();
+        for (int e = 0; e < 8; ++e) {
+            const int2 q = reinterpret_cast<const int2 *>(sb + e)[1];
+            rbx[e] = q.x;
+            vx[e] = q.y + xoff;
         }
-    }
-    __syncthreads();  // every wave is done with its tiles: the space holds the final sum
+        operands_x<TN, PW>(bx, rbx, vx, lds);
+    };
 
-    // Sum the waves' tiles in a fixed order and store.  Lane l of a wave holds
-    // column (l & 31) and rows 8*(j/4) + 4*(l/32) + (j%4), j = 0..15.
-    float *red = reinterpret_cast<float *>(lds);
+    int32_t qa = 0, qb = 0;
+    if (nsteps > 0) {
+        const int32_t q0 = coord(0);
+        qa = coord(1);
+        qb = coord(2);
+        __syncthreads();  // tables written
+        put(0, q0);
+    } else {
+        __syncthreads();
+    }
+    half8 bx[TN];
+    if (nsteps > 0) x_operands(0, bx);
+    for (int32_t st = 0; st < nsteps; ++st) {
+        put(st + 1, qa);  // harmless past the last step: every factor 0
+        qa = qb;
+        qb = coord(st + 3);
+        half8 bxn[TN];
+        x_operands(st + 1, bxn);
+        const GBird *sb = stage + (st & 1) * kGStep + 8 * grp;
+        int32_t rby[8], vy[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int2 q = reinterpret_cast<const int2 *>(sb + e)[0];
+            rby[e] = q.x;
+            vy[e] = q.y + yoff;
+        }
+        contract_y<TM, TN, PW>(acc, bx, rby, vy, lds);
+#pragma unroll
+        for (int n = 0; n < TN; ++n) bx[n] = bxn[n];
+    }
+
     const size_t cells = (size_t)a.grid_h * a.grid_w;
     float *out = split > 1 ? partial + ((size_t)f * split + sl) * cells : a.density + (size_t)f * cells;
-    const float scale = split > 1 ? 1.0f : tg.scale;
-    constexpr int kTiles = RM * RN;
-    constexpr int kPerRound = kTiles < kRedTiles ? kTiles : kRedTiles;
-    constexpr int kTile = kWWaves * 32 * 33;  // floats per tile: every wave's partial, padded rows
+    const float scale = split > 1 ? 1.0f : gg.scale;
+    if (waves == 1) {
+        // lane l holds rows 4 (l / 16) + i, column l % 16 of every tile
+        if (!active) return;
 #pragma unroll
-    for (int t0 = 0; t0 < kTiles; t0 += kPerRound) {
+        for (int m = 0; m < TM; ++m)
 #pragma unroll
-        for (int q = 0; q < kPerRound; ++q) {
-            if (t0 + q >= kTiles) break;
-            const int m = (t0 + q) / RN, t = (t0 + q) % RN;
+            for (int t = 0; t < TN; ++t)
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const int row = 8 * (j >> 2) + 4 * (lane >> 5) + (j & 3);
-                red[q * kTile + (wave * 32 + row) * 33 + r32] = acc[m][t][j];
-            }
+                for (int i = 0; i < 4; ++i) {
+                    const int gy = row0 + 16 * m + 4 * grp + i, gx = col0 + 16 * t + r16;
+                    if (gy < a.grid_h && gx < a.grid_w) out[(size_t)gy * a.grid_w + gx] = acc[m][t][i] * scale;
+                }
+        return;
+    }
+
+    // the waves of an item add their tiles in wave order, kGRedTiles at a time
+    __syncthreads();  // tables and staging are done with: the space holds the tiles
+    float *red = reinterpret_cast<float *>(lds);
+    const int w0 = (wave / waves) * waves;
+    const int gt = part * 64 + lane;
+#pragma unroll
+    for (int t0 = 0; t0 < TM * TN; t0 += kGRedTiles) {
+#pragma unroll
+        for (int q = 0; q < kGRedTiles; ++q) {
+            const int t = t0 + q;
+            if (t >= TM * TN) break;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) red[(wave * kGRedTiles + q) * 256 + (4 * grp + i) * 16 + r16] = acc[t / TN][t % TN][i];
         }
         __syncthreads();
-        const int ntiles = min(kPerRound, kTiles - t0);
-        for (int el = tid; el < ntiles * 1024; el += kWThreads) {
-            const int q = el >> 10, row = (el >> 5) & 31, colx = el & 31;
-            const float *rq = red + q * kTile + row * 33 + colx;
+        const int nt = min(kGRedTiles, TM * TN - t0);
+        for (int el = gt; el < nt * 256; el += 64 * waves) {
+            const int q = el >> 8, within = el & 255;
             float v = 0.0f;
-#pragma unroll
-            for (int w = 0; w < kWWaves; ++w) v += rq[w * 32 * 33];
-            const int m = (t0 + q) / RN, t = (t0 + q) % RN;
-            const int gy = gy0 + m * 32 + row;
-            const int gx = gx0 + t * 32 + colx;
-            if ((ok || split > 1) && gy < a.grid_h && gx < a.grid_w) out[(size_t)gy * a.grid_w + gx] = v * scale;
+            for (int w = 0; w < waves; ++w) v += red[((w0 + w) * kGRedTiles + q) * 256 + within];
+            const int t = t0 + q;
+            const int gy = row0 + 16 * (t / TN) + (within >> 4), gx = col0 + 16 * (t % TN) + (within & 15);
+            if (active && gy < a.grid_h && gx < a.grid_w) out[(size_t)gy * a.grid_w + gx] = v * scale;
         }
         __syncthreads();
     }
@@ -483,22 +550,17 @@ hipError_t launch_recur(const DensityArgs &a, const Geometry &g, const DensityPl
     return hipGetLastError();
 }
 
-template <int RM, int RN>
-hipError_t launch_table(const DensityArgs &a, const TableGeom &tg, const DensityPlan &p, float *partial,
-                        hipStream_t stream) {
-    const long long blocks = (long long)a.n_frames * p.regions_y * p.regions_x * p.split;
-    const size_t lds = (size_t)tg.lds_bytes;
-    hipLaunchKernelGGL((density_table_kernel<RM, RN>), dim3((unsigned)blocks), dim3(kWThreads), lds, stream, a,
-                       tg, p.regions_y, p.regions_x, p.split, partial);
-    return hipGetLastError();
-}
-
 struct Shape {
     int rm, rn;
 };
-// instantiated region shapes (tiles of 32 x 32; at most 12 tiles per region)
+// instantiated region shapes of the recurrence path (tiles of 32 x 32; at
+// most 12 tiles per region)
 constexpr Shape kShapes[] = {{1, 1}, {1, 2}, {2, 1}, {2, 2}, {1, 4}, {3, 2},
                              {2, 4}, {3, 4}, {4, 2}, {5, 2}, {4, 1}, {5, 1}};
+// instantiated region shapes of the gather path (tiles of 16 x 16; at most 40
+// tiles per region)
+constexpr Shape kGShapes[] = {{1, 1}, {2, 2}, {1, 4}, {4, 1}, {2, 4}, {4, 2}, {3, 4},
+                              {4, 4}, {5, 4}, {5, 8}, {9, 2}, {9, 4}, {3, 8}, {4, 8}};
 
 Geometry make_geometry(const DensityArgs &a) {
     Geometry g;
@@ -516,141 +578,149 @@ Geometry make_geometry(const DensityArgs &a) {
     return g;
 }
 
-
-// Table geometry for a region shape; false when the table path does not apply
-// (a cell is not a whole number of quanta, a window is wider than kMaxWin rows,
-// or the tiles and tables exceed the LDS budget).
-bool make_table_geom(const DensityArgs &a, int rm, int rn, size_t lds_limit, TableGeom *tg) {
+// Factor-table geometry of the gather path; false when it does not apply (a
+// cell is not a whole number of quanta, or the tables exceed their budget).
+bool make_gather_geom(const DensityArgs &a, GatherGeom *gg) {
     if ((16LL * a.height_px) % a.grid_h != 0 || (16LL * a.width_px) % a.grid_w != 0) return false;
     const double cut_q = 16.0 * kCutSigmas * (double)a.sigma_px;  // window half-width, quanta
-    auto axis = [&](int64_t c, TableAxis *t) {
+    auto axis = [&](int64_t c, GatherAxis *t) {
         if (c < 1 || c > (1 << 20)) return false;
-        // rows G + j with |j| <= j cover every row centre within cut_q of the bird
+        // cells G + n with |n| <= j cover every cell centre within cut_q of the bird
         const double jd = std::ceil(cut_q / (double)c) + 1.0;
-        if (jd > (kMaxWin - 1) / 2) return false;
-        t->c = (int)c;
-        t->j = (int)jd;
-        t->w = 2 * t->j + 1;
-        t->tw = (t->w + 7) / 8 * 8;
+        if (jd > 64.0) return false;
+        t->c = (int32_t)c;
+        t->j = (int32_t)jd;
         return true;
     };
-    if (!axis(16LL * a.height_px / a.grid_h, &tg->ay) || !axis(16LL * a.width_px / a.grid_w, &tg->ax))
-        return false;
-    tg->rows_y = 32 * rm + 2 * tg->ay.tw;
-    tg->rows_x = 32 * rn + 2 * tg->ax.tw;
-    tg->wave_tile = (tg->rows_y + tg->rows_x) * kWPitch;
-    tg->tab_y = kWWaves * tg->wave_tile;
-    const bool shared = tg->ay.c == tg->ax.c && tg->ay.j == tg->ax.j;
-    tg->tab_x = shared ? tg->tab_y : tg->tab_y + tg->ay.c * tg->ay.tw;
-    const int64_t halves = (int64_t)tg->tab_x + (shared ? (int64_t)tg->ay.c * tg->ay.tw
-                                                        : (int64_t)tg->ax.c * tg->ax.tw);
-    const int64_t red = (int64_t)std::min(rm * rn, kRedTiles) * kWWaves * 32 * 33 * 4;
-    const int64_t bytes = std::max<int64_t>(2 * halves, red);
-    if (bytes > (int64_t)lds_limit) return false;
-    tg->lds_bytes = (int)bytes;
+    if (!axis(16LL * a.height_px / a.grid_h, &gg->ay) || !axis(16LL * a.width_px / a.grid_w, &gg->ax)) return false;
+    const int jmax = std::max(gg->ay.j, gg->ax.j);
+    if (2 * jmax + 3 <= 32) gg->pw = 32;
+    else if (2 * jmax + 3 <= 64) gg->pw = 64;
+    else return false;
+    auto bytes16 = [](int64_t pairs) { return (pairs * 4 + 15) / 16 * 16; };
+    const int64_t ty = bytes16((int64_t)gg->ay.c * (gg->pw + 16));
+    const bool shared = gg->ay.c == gg->ax.c && gg->ay.j == gg->ax.j;
+    const int64_t tx = shared ? 0 : bytes16((int64_t)gg->ax.c * (gg->pw + 16));
+    if (ty + tx > kGMaxTableBytes) return false;
+    gg->ay.tab = 0;
+    gg->ax.tab = shared ? 0 : (int32_t)ty;
+    gg->table_bytes = (int)(ty + tx);
+    const int stage = kGWaves * 2 * kGStep * (int)sizeof(GBird);
+    gg->lds_bytes = std::max(gg->table_bytes + stage, kGWaves * kGRedTiles * 256 * 4);
     const double s = (double)a.sigma_px;
-    tg->neg_k = (float)(-1.4426950408889634 / (2.0 * s * s));
-    tg->scale = (float)(1.0 / (2.0 * 3.14159265358979323846 * s * s));
+    gg->neg_k = (float)(-1.4426950408889634 / (2.0 * s * s));
+    gg->scale = (float)(1.0 / (2.0 * 3.14159265358979323846 * s * s));
     return true;
 }
 
-long long shape_regions(const Shape &sh, int grid_w, int grid_h) {
-    return ((grid_h + 32LL * sh.rm - 1) / (32LL * sh.rm)) * ((grid_w + 32LL * sh.rn - 1) / (32LL * sh.rn));
+long long shape_regions(const Shape &sh, int tile, int grid_w, int grid_h) {
+    return ((grid_h + (long long)tile * sh.rm - 1) / ((long long)tile * sh.rm)) *
+           ((grid_w + (long long)tile * sh.rn - 1) / ((long long)tile * sh.rn));
 }
 
-// Ordering of region shapes for the table path: least padded area, then
-// fewest regions.
-bool table_better(const Shape &x, const Shape &y, int grid_w, int grid_h) {
-    const long long rx = shape_regions(x, grid_w, grid_h), ry = shape_regions(y, grid_w, grid_h);
-    const long long ax = rx * x.rm * x.rn, ay = ry * y.rm * y.rn;
-    return ax < ay || (ax == ay && rx < ry);
-}
-
-Shape table_shape(int grid_w, int grid_h) {
-    Shape best = kShapes[0];
-    for (const Shape &sh : kShapes)
-        if (table_better(sh, best, grid_w, grid_h)) best = sh;
+// Gather-path region shape: least padded area, then fewest regions.
+Shape gather_shape(int grid_w, int grid_h) {
+    Shape best = kGShapes[0];
+    long long best_area = -1, best_regions = 0;
+    for (const Shape &sh : kGShapes) {
+        const long long r = shape_regions(sh, 16, grid_w, grid_h);
+        const long long area = r * sh.rm * sh.rn;
+        if (best_area < 0 || area < best_area || (area == best_area && r < best_regions)) {
+            best = sh;
+            best_area = area;
+            best_regions = r;
+        }
+    }
     return best;
 }
 
-// Bird slices per (frame, region): enough workgroups to fill the chip, at
-// least kMinSliceBirds birds per slice on average.
-int table_split(int32_t n_frames, int32_t total, long long regions) {
-    const long long wgs = (long long)n_frames * regions;
-    if (n_frames <= 0 || wgs >= kSplitTarget) return 1;
-    const long long want = (kSplitTarget + wgs - 1) / wgs;
-    const long long cap = std::max<long long>(1, (long long)total / n_frames / kMinSliceBirds);
-    return (int)std::max<long long>(1, std::min<long long>(std::min(want, cap), 64));
+int env_int(const char *name) {
+    const char *v = std::getenv(name);
+    return v ? std::atoi(v) : 0;
+}
+
+// Waves per work item and slices per (frame, region) of a gather launch:
+// enough waves for two per SIMD, each with at least kGMinWaveBirds birds on
+// average.  FLOCK_DENSITY_WAVES / FLOCK_DENSITY_SPLIT override (for tuning).
+void gather_split(int32_t n_frames, int32_t total, long long regions, int n_cus, int *waves, int *split) {
+    const long long items = (long long)n_frames * regions;
+    const long long target = 8LL * std::max(n_cus, 1);
+    int w = items >= target ? 1 : (2 * items >= target ? 2 : 4);
+    const double birds = n_frames > 0 ? (double)total / n_frames : 0.0;
+    long long sp = 1;
+    if (items * w < target) {
+        sp = (target + items * w - 1) / (items * w);
+        sp = std::min<long long>(sp, std::max<long long>(1, (long long)(birds / (w * kGMinWaveBirds))));
+        sp = std::min<long long>(sp, 64);
+    }
+    const int fw = env_int("FLOCK_DENSITY_WAVES"), fs = env_int("FLOCK_DENSITY_SPLIT");
+    if (fw == 1 || fw == 2 || fw == 4) w = fw;
+    if (fs >= 1 && fs <= 64) sp = fs;
+    *waves = w;
+    *split = (int)sp;
 }
 
 }  // namespace
 
-size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h) {
+size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h, int n_cus) {
     if (n_frames <= 0 || grid_w < 1 || grid_h < 1) return 0;
-    const Shape sh = table_shape(grid_w, grid_h);
-    const int split = table_split(n_frames, total, shape_regions(sh, grid_w, grid_h));
+    const Shape sh = gather_shape(grid_w, grid_h);
+    int waves = 1, split = 1;
+    gather_split(n_frames, total, shape_regions(sh, 16, grid_w, grid_h), n_cus, &waves, &split);
     if (split <= 1) return 0;
     return (size_t)n_frames * split * (size_t)grid_w * grid_h * sizeof(float);
 }
 
-// Recurrence path: choose the output region per workgroup with a small cost
-// model: per bird a region costs its matrix-core time (RM*RN/2 cycles), the
-// factor rows its windows cover and its tile clearing; workgroups spread over
-// the compute units, and a launch never finishes before one workgroup does.
-// Table path: the least padded region shape whose tiles fit in LDS, and bird
-// slices when the batch has few (frame, region) pairs.
-// FLOCK_DENSITY_SHAPE="rm,rn" forces a region shape and FLOCK_DENSITY_PATH=
-// "recur" or "table" a path where it applies (for tuning).
+// Gather path whenever its tables apply; otherwise the recurrence path, whose
+// region per workgroup comes from a small cost model: per bird a region costs
+// its matrix-core time (RM*RN/2 cycles), the factor rows its windows cover and
+// its tile clearing; workgroups spread over the compute units, and a launch
+// never finishes before one workgroup does.
+// FLOCK_DENSITY_PATH="recur" forces the recurrence path and
+// FLOCK_DENSITY_SHAPE="rm,rn" its region shape (for tuning).
 DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit) {
     const int tiles_y = (a.grid_h + 31) / 32;
     const int tiles_x = (a.grid_w + 31) / 32;
     const char *force = std::getenv("FLOCK_DENSITY_SHAPE");
     const char *path = std::getenv("FLOCK_DENSITY_PATH");
     const bool force_recur = path && std::strcmp(path, "recur") == 0;
-    const bool force_table = path && std::strcmp(path, "table") == 0;
+    GatherGeom gg;
+    if (!force_recur && make_gather_geom(a, &gg) && (size_t)gg.lds_bytes <= lds_limit) {
+        const Shape sh = gather_shape(a.grid_w, a.grid_h);
+        DensityPlan p{};
+        p.gather = 1;
+        p.rm = sh.rm;
+        p.rn = sh.rn;
+        p.regions_y = (a.grid_h + 16 * sh.rm - 1) / (16 * sh.rm);
+        p.regions_x = (a.grid_w + 16 * sh.rn - 1) / (16 * sh.rn);
+        gather_split(a.n_frames, a.total, (long long)p.regions_y * p.regions_x, n_cus, &p.waves, &p.split);
+        const long long items = (long long)a.n_frames * p.regions_y * p.regions_x * p.split;
+        const int per_wg = kGWaves / p.waves;
+        p.blocks = (items + per_wg - 1) / per_wg;
+        return p;
+    }
     int frm = 0, frn = 0;
     if (force && std::sscanf(force, "%d,%d", &frm, &frn) == 2) {
         bool known = false;
         for (const Shape &sh : kShapes) known |= sh.rm == frm && sh.rn == frn;
         if (!known) frm = frn = 0;
     }
-    // The table path's single-column LDS writes conflict across banks, so on
-    // batches that already fill the chip the recurrence path is faster; the
-    // table path serves batches with fewer (frame, region) pairs than
-    // workgroups wanted, which it splits by birds.
-    const Shape pref = table_shape(a.grid_w, a.grid_h);
-    const bool few = (long long)a.n_frames * shape_regions(pref, a.grid_w, a.grid_h) < kSplitTarget;
-    if (!force_recur && (few || force_table)) {
-        // table path: the forced shape, else the best shape whose tiles fit
-        const int split_cap = table_split(a.n_frames, a.total, shape_regions(pref, a.grid_w, a.grid_h));
-        TableGeom tg;
-        bool found = false;
-        Shape best = kShapes[0];
-        if (frm) {
-            best = Shape{frm, frn};
-            found = make_table_geom(a, frm, frn, lds_limit, &tg);
-        } else {
-            for (const Shape &sh : kShapes)
-                if ((!found || table_better(sh, best, a.grid_w, a.grid_h)) &&
-                    make_table_geom(a, sh.rm, sh.rn, lds_limit, &tg)) {
-                    best = sh;
-                    found = true;
-                }
-        }
-        if (found) {
-            const long long regions = shape_regions(best, a.grid_w, a.grid_h);
-            const int split = std::min(split_cap, table_split(a.n_frames, a.total, regions));
-            return DensityPlan{1, best.rm, best.rn, (int)((a.grid_h + 32LL * best.rm - 1) / (32LL * best.rm)),
-                               (int)((a.grid_w + 32LL * best.rn - 1) / (32LL * best.rn)), split};
-        }
+    DensityPlan best{};
+    best.rm = best.rn = 1;
+    best.split = best.waves = 1;
+    if (frm) {
+        best.rm = frm;
+        best.rn = frn;
+        best.regions_y = (tiles_y + frm - 1) / frm;
+        best.regions_x = (tiles_x + frn - 1) / frn;
+        best.blocks = (long long)a.n_frames * best.regions_y * best.regions_x;
+        return best;
     }
-    if (frm) return DensityPlan{0, frm, frn, (tiles_y + frm - 1) / frm, (tiles_x + frn - 1) / frn, 1};
     const double s = (double)a.sigma_px;
     const double hx = (double)a.width_px / a.grid_w, hy = (double)a.height_px / a.grid_h;
     const double lx = std::min(2.0 * kCutSigmas * s / hx + 1.0, (double)a.grid_w);
     const double ly = std::min(2.0 * kCutSigmas * s / hy + 1.0, (double)a.grid_h);
     const double birds = a.n_frames > 0 ? (double)a.total / a.n_frames : 0.0;
-    DensityPlan best{0, 1, 1, tiles_y, tiles_x, 1};
     double best_t = 1e300;
     for (const Shape &sh : kShapes) {
         if (sh.rm > tiles_y && sh.rm > 1) continue;
@@ -664,31 +734,46 @@ DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit) {
         const double t = std::max(blocks * per_block / n_cus, per_block);
         if (t < best_t * 0.999) {
             best_t = t;
-            best = DensityPlan{0, sh.rm, sh.rn, ry, rx, 1};
+            best.rm = sh.rm;
+            best.rn = sh.rn;
+            best.regions_y = ry;
+            best.regions_x = rx;
         }
     }
+    if (best.regions_y == 0) {
+        best.regions_y = tiles_y;
+        best.regions_x = tiles_x;
+    }
+    best.blocks = (long long)a.n_frames * best.regions_y * best.regions_x;
     return best;
 }
 
-hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, size_t lds_limit, float *partial,
-                          hipStream_t stream) {
+hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, float *partial, hipStream_t stream) {
     hipError_t err = hipErrorInvalidValue;
-    if (p.table) {
-        TableGeom tg;
-        if (!make_table_geom(a, p.rm, p.rn, lds_limit, &tg)) return hipErrorInvalidValue;
+    if (p.gather) {
+        GatherGeom gg;
+        if (!make_gather_geom(a, &gg)) return hipErrorInvalidValue;
         if (p.split > 1 && !partial) return hipErrorInvalidValue;
-#define FLOCK_SHAPE(RM, RN) \
-    if (p.rm == RM && p.rn == RN) err = launch_table<RM, RN>(a, tg, p, partial, stream);
-        FLOCK_SHAPE(1, 1) FLOCK_SHAPE(1, 2) FLOCK_SHAPE(2, 1) FLOCK_SHAPE(2, 2) FLOCK_SHAPE(1, 4)
-        FLOCK_SHAPE(3, 2) FLOCK_SHAPE(2, 4) FLOCK_SHAPE(3, 4) FLOCK_SHAPE(4, 2) FLOCK_SHAPE(5, 2)
-        FLOCK_SHAPE(4, 1) FLOCK_SHAPE(5, 1)
-#undef FLOCK_SHAPE
+        const long long items = (long long)a.n_frames * p.regions_y * p.regions_x * p.split;
+#define FLOCK_GSHAPE_PW(TM, TN, PW)                                                                              \
+    if (p.rm == TM && p.rn == TN && gg.pw == PW) {                                                               \
+        hipLaunchKernelGGL((density_gather_kernel<TM, TN, PW>), dim3((unsigned)p.blocks), dim3(kGThreads),      \
+                           (size_t)gg.lds_bytes, stream, a, gg, p.regions_y, p.regions_x, p.split, p.waves, items, \
+                           partial);                                                                             \
+        err = hipGetLastError();                                                                                 \
+    }
+#define FLOCK_GSHAPE(TM, TN) FLOCK_GSHAPE_PW(TM, TN, 32) FLOCK_GSHAPE_PW(TM, TN, 64)
+        FLOCK_GSHAPE(1, 1) FLOCK_GSHAPE(2, 2) FLOCK_GSHAPE(1, 4) FLOCK_GSHAPE(4, 1) FLOCK_GSHAPE(2, 4)
+        FLOCK_GSHAPE(4, 2) FLOCK_GSHAPE(3, 4) FLOCK_GSHAPE(4, 4) FLOCK_GSHAPE(5, 4) FLOCK_GSHAPE(5, 8)
+        FLOCK_GSHAPE(9, 2) FLOCK_GSHAPE(9, 4) FLOCK_GSHAPE(3, 8) FLOCK_GSHAPE(4, 8)
+#undef FLOCK_GSHAPE
+#undef FLOCK_GSHAPE_PW
         if (err != hipSuccess || p.split <= 1) return err;
         const int64_t cells = (int64_t)a.grid_h * a.grid_w;
         const int64_t total = cells * a.n_frames;
         const unsigned blocks = (unsigned)std::min<int64_t>((total + 255) / 256, 4096);
         hipLaunchKernelGGL(density_reduce_kernel, dim3(blocks), dim3(256), 0, stream, a.density, partial, cells,
-                           total, p.split, tg.scale);
+                           total, p.split, gg.scale);
         return hipGetLastError();
     }
     const Geometry g = make_geometry(a);

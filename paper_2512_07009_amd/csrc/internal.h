@@ -57,18 +57,19 @@ struct DensityArgs {
 };
 
 struct DensityPlan {
-    int table;                // 1: exact factor tables; 0: recurrence
-    int rm;                   // 32-row gy tiles per workgroup region
-    int rn;                   // 32-column gx tiles per workgroup region
+    int gather;               // 1: factor tables gathered into registers; 0: recurrence
+    int rm;                   // region height in tiles (16 rows gather, 32 recurrence)
+    int rn;                   // region width in tiles
     int regions_y, regions_x; // regions per frame
     int split;                // bird slices per (frame, region); > 1 adds partial grids afterwards
+    int waves;                // gather: waves sharing one (frame, region, slice)
+    long long blocks;         // workgroups of the main kernel
 };
 
 DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit);
 // Workspace for the partial grids of a split launch (0 if none); depends on the
 // batch shape and grid only, and bounds every plan for that shape.
-size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h);
-hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, size_t lds_limit, float *partial,
-                          hipStream_t stream);
+size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h, int n_cus);
+hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, float *partial, hipStream_t stream);
 
 }  // namespace flock
