@@ -245,25 +245,15 @@ __device__ __forceinline__ int32_t div_small(int32_t x, int32_t d, float inv_d) 
     return q;
 }
 
-// Squared distance from v to the nearest point of the cell
-// rectangle [x0, x0 + side) x [y0, y0 + side), per axis clamped to E + 1.
-__device__ __forceinline__ int32_t rect_near2(int32_t vx, int32_t vy, int32_t x0, int32_t y0, int32_t side,
-                                              int32_t e1) {
-    const int32_t dx = min(max(max(x0 - vx, vx - (x0 + side - 1)), 0), e1);
-    const int32_t dy = min(max(max(y0 - vy, vy - (y0 + side - 1)), 0), e1);
-    return __mul24(dx, dx) + __mul24(dy, dy);
-}
-
 // Neighbour-cell tables of one frame, built by the 64 lanes of one wave.
 // Cell offset (dx, dy), |dx|, |dy| <= reach <= 2, can hold a neighbour iff the
 // gap between the two cells, gap(|dx|)^2 + gap(|dy|)^2, is <= E^2.
 //   sdx/sdy   the whole stencil, nearest cells first (ties in lane order)
-//   odx/ody   its forward half (cells later in row-major order): adjacent
-//             cells in table 0, the others in table 1
+//   fdx/fdy   its forward half (cells later in row-major order), the
+//             nadj adjacent cells first, nfwd in all (at most 4 + 8)
 //   dxmax[k]  the widest |dx| in row |dy| = k
 __device__ void build_stencil(int32_t reach, int32_t side, const Radius &r, int lane, int *dxmax, int *sdx,
-                              int *sdy, int *nsten, int (*odx)[kMaxOffsets], int (*ody)[kMaxOffsets],
-                              int *noff) {
+                              int *sdy, int *nsten, int *fdx, int *fdy, int *nadj, int *nfwd) {
     const int dx = lane % 5 - 2, dy = lane / 5 - 2;
     const int adx = dx < 0 ? -dx : dx, ady = dy < 0 ? -dy : dy;
     bool valid = false;
@@ -288,13 +278,10 @@ __device__ void build_stencil(int32_t reach, int32_t side, const Radius &r, int 
     const bool adj = adx <= 1 && ady <= 1;
     const uint64_t m0 = __ballot(fwd && adj), m1 = __ballot(fwd && !adj);
     const uint64_t below = (1ull << lane) - 1ull;
-    if (fwd && adj) {
-        odx[0][__popcll(m0 & below)] = dx;
-        ody[0][__popcll(m0 & below)] = dy;
-    }
-    if (fwd && !adj) {
-        odx[1][__popcll(m1 & below)] = dx;
-        ody[1][__popcll(m1 & below)] = dy;
+    if (fwd) {
+        const int at = adj ? __popcll(m0 & below) : __popcll(m0) + __popcll(m1 & below);
+        fdx[at] = dx;
+        fdy[at] = dy;
     }
     if (lane <= 2) {  // row dy = lane: valid cells are |dx| <= dxmax, a symmetric run
         const int cnt = __popcll((vm >> ((lane + 2) * 5)) & 31ull);
@@ -302,78 +289,122 @@ __device__ void build_stencil(int32_t reach, int32_t side, const Radius &r, int 
     }
     if (lane == 0) {
         *nsten = __popcll(vm);
-        noff[0] = __popcll(m0);
-        noff[1] = __popcll(m1);
+        *nadj = __popcll(m0);
+        *nfwd = __popcll(m0) + __popcll(m1);
     }
 }
 
+// The first two points of a cell (the first one twice in a one-point cell)
+// and their core flags.
+struct CellHead {
+    uint32_t p0, p1;
+    bool c0, c1;
+};
+
+__device__ __forceinline__ CellHead cell_head(const uint32_t *pxy, const uint8_t *score, int32_t q0, int32_t q1) {
+    const int32_t q = min(q0 + 1, q1 - 1);
+    return CellHead{pxy[q0], pxy[q], score[q0] != 0, score[q] != 0};
+}
+
+// Some core pair among the first two points of each cell within eps: in
+// clustered frames this settles about nine adjacent cell pairs in ten.
+__device__ __forceinline__ bool heads_touch(const CellHead &A, const CellHead &B, const Radius &r) {
+    return (A.c0 & B.c0 & (sq_dist_pk(A.p0, B.p0, r.e1) <= r.e2)) |
+           (A.c0 & B.c1 & (sq_dist_pk(A.p0, B.p1, r.e1) <= r.e2)) |
+           (A.c1 & B.c0 & (sq_dist_pk(A.p1, B.p0, r.e1) <= r.e2)) |
+           (A.c1 & B.c1 & (sq_dist_pk(A.p1, B.p1, r.e1) <= r.e2));
+}
+
 // True if some core of sorted points [a0, a1) lies within eps of some core of
-// [b0, b1), whose cell rectangle starts at (bx0, by0).  Points go four at a
-// time from each side, so each step keeps eight LDS reads in flight; cores of
-// A beyond eps of B's rectangle are skipped.
+// [b0, b1) (scalar loops with early exit).
 __device__ __forceinline__ bool cells_touch(const uint32_t *pxy, const uint8_t *score, int32_t a0, int32_t a1,
-                                            int32_t b0, int32_t b1, int32_t bx0, int32_t by0, int32_t side,
-                                            const Radius &r) {
-    for (int32_t qa = a0; qa < a1; qa += 4) {
-        uint32_t va[4];
-        bool ok[4];
-        bool any = false;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int32_t q = min(qa + i, a1 - 1);
-            va[i] = pxy[q];
-            ok[i] = (qa + i < a1) & (score[q] != 0);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            ok[i] = ok[i] & (rect_near2(pk_x(va[i]), pk_y(va[i]), bx0, by0, side, r.e1) <= r.e2);
-            any |= ok[i];
-        }
-        if (!any) continue;
-        for (int32_t qb = b0; qb < b1; qb += 4) {
-            bool hit = false;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int32_t q = min(qb + j, b1 - 1);
-                const uint32_t vb = pxy[q];
-                const bool cb = (qb + j < b1) & (score[q] != 0);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) hit |= ok[i] & cb & (sq_dist_pk(va[i], vb, r.e1) <= r.e2);
-            }
-            if (hit) return true;
-        }
+                                            int32_t b0, int32_t b1, const Radius &r) {
+    for (int32_t qa = a0; qa < a1; ++qa) {
+        if (!score[qa]) continue;
+        const uint32_t va = pxy[qa];
+        for (int32_t qb = b0; qb < b1; ++qb)
+            if ((score[qb] != 0) & (sq_dist_pk(va, pxy[qb], r.e1) <= r.e2)) return true;
     }
     return false;
 }
 
-// Join core cell clist[j] with its forward neighbours (offsets odx/ody, noff
-// of them): a neighbour holding a core is joined when some core pair across
-// the two cells is within eps.  All cores of a cell form one node (its
-// smallest core index), since any two points of a cell are neighbours.  The
-// loop is kept rolled: one copy of the pair test keeps the kernel's code small.
-__device__ __forceinline__ void union_cell(int32_t j, const uint16_t *clist, const uint32_t *cell,
-                                           int32_t *parent, const uint32_t *pxy, const uint8_t *score,
-                                           const Grid &g, const Radius &r, const int *odx, const int *ody,
-                                           int noff, float inv_ncx) {
-    const int32_t ca = clist[j];
-    const int32_t ay = div_small(ca, g.ncx, inv_ncx), ax = ca - ay * g.ncx;
-    const uint32_t wa = cell[ca];
-    const int32_t a0 = (int32_t)(wa & 0xffffu), a1 = (int32_t)(cell[ca + 1] & 0xffffu);
-    const int32_t na = (int32_t)(wa >> 16);
-#pragma unroll 1
-    for (int o = 0; o < noff; ++o) {
-        const int32_t bx = ax + odx[o], by = ay + ody[o];
-        if ((bx < 0) | (bx >= g.ncx) | (by >= g.ncy)) continue;
-        const int32_t cb = by * g.ncx + bx;
-        const uint32_t wb = cell[cb];
-        const int32_t nb = (int32_t)(wb >> 16);
-        if (nb == (int32_t)kNone) continue;
-        const int32_t ra = uf_find<kGroup>(parent, na);
-        const int32_t rb = uf_find<kGroup>(parent, nb);
-        if (ra == rb) continue;  // already one tree
-        const int32_t b0 = (int32_t)(wb & 0xffffu), b1 = (int32_t)(cell[cb + 1] & 0xffffu);
-        if (cells_touch(pxy, score, a0, a1, b0, b1, bx * g.side, by * g.side, g.side, r))
-            uf_unite<kGroup>(parent, ra, rb);
+// A core cell of the work list: its id, column and row, sorted range
+// [a0, a1), node (smallest core index) and first two points.
+struct CoreCell {
+    int32_t ca, ax, ay, a0, a1, node;
+    CellHead head;
+};
+
+// Append `flag` lanes' values to a queue of `cap` entries (wave-uniform call);
+// returns true for a flagged lane whose entry did not fit.
+__device__ __forceinline__ bool wave_enqueue(bool flag, uint32_t value, uint32_t *queue, int *counter, int cap) {
+    const uint64_t m = __ballot(flag);
+    if (m == 0) return false;
+    const int lane = threadIdx.x & 63;
+    int base = 0;
+    if (lane == 0) base = atomicAdd(counter, __popcll(m));
+    base = __shfl(base, 0, 64);
+    const int at = base + __popcll(m & ((1ull << lane) - 1ull));
+    if (flag && at < cap) queue[at] = value;
+    return flag && at >= cap;
+}
+
+// One pass of cell unions over this lane's core cell A (if `have`), forward
+// offsets fdx/fdy[o0, o1) with o1 - o0 <= NO (wave-uniform call).  A
+// neighbour holding a core is joined when a core pair across the two cells is
+// within eps; all cores of a cell form one node, since any two points of a
+// cell are neighbours.
+//   far = false: the adjacent cells;
+//   far = true:  the farther cells, after the adjacent unions and a flatten:
+//                a pair whose recorded roots agree is already joined (joins
+//                only merge trees) and is skipped.
+// The heads of both cells settle most pairs here.  The rest go to `queue` as
+// (cell A, cell B), to be tested after a barrier by one lane each, so that the
+// few long scans share a few waves instead of holding up every wave.
+template <int NO, bool far>
+__device__ __forceinline__ void union_heads(bool have, const CoreCell &A, const uint32_t *cell, int32_t *parent,
+                                            const uint32_t *pxy, const uint8_t *score, const Grid &g,
+                                            const Radius &r, const int *fdx, const int *fdy, int o0, int o1,
+                                            uint32_t *queue, int *nq, int qcap) {
+    const int32_t ra = far && have ? ld_rlx<kGroup>(parent + A.node) : 0;
+#pragma unroll
+    for (int k = 0; k < NO; ++k) {
+        const int o = o0 + k;
+        if (o >= o1) break;  // wave-uniform
+        bool open = false;
+        int32_t cb = 0, nb = 0;
+        if (have) {
+            const int32_t bx = A.ax + fdx[o], by = A.ay + fdy[o];
+            if (!((bx < 0) | (bx >= g.ncx) | (by >= g.ncy))) {
+                cb = by * g.ncx + bx;
+                const uint32_t wb = cell[cb];
+                nb = (int32_t)(wb >> 16);
+                if (nb != (int32_t)kNone && !(far && ld_rlx<kGroup>(parent + nb) == ra)) {
+                    const int32_t b0 = (int32_t)(wb & 0xffffu), b1 = (int32_t)(cell[cb + 1] & 0xffffu);
+                    const CellHead B = cell_head(pxy, score, b0, b1);
+                    if (heads_touch(A.head, B, r)) uf_unite<kGroup>(parent, A.node, nb);
+                    else open = (A.a1 - A.a0 > 2) | (b1 - b0 > 2);
+                }
+            }
+        }
+        if (wave_enqueue(open, (uint32_t)A.ca | ((uint32_t)cb << 16), queue, nq, qcap)) {
+            // queue full: test here
+            const int32_t b0 = (int32_t)(cell[cb] & 0xffffu), b1 = (int32_t)(cell[cb + 1] & 0xffffu);
+            if (cells_touch(pxy, score, A.a0, A.a1, b0, b1, r)) uf_unite<kGroup>(parent, A.node, nb);
+        }
+    }
+}
+
+// The queued cell pairs, one lane each.
+__device__ __forceinline__ void union_queue(const uint32_t *queue, int nq, const uint32_t *cell, int32_t *parent,
+                                            const uint32_t *pxy, const uint8_t *score, const Radius &r) {
+    for (int t = threadIdx.x; t < nq; t += kThreads) {
+        const uint32_t e = queue[t];
+        const int32_t ca = (int32_t)(e & 0xffffu), cb = (int32_t)(e >> 16);
+        const uint32_t wa = cell[ca], wb = cell[cb];
+        if (cells_touch(pxy, score, (int32_t)(wa & 0xffffu), (int32_t)(cell[ca + 1] & 0xffffu),
+                        (int32_t)(wb & 0xffffu), (int32_t)(cell[cb + 1] & 0xffffu), r))
+            uf_unite<kGroup>(parent, (int32_t)(wa >> 16), (int32_t)(wb >> 16));
     }
 }
 
@@ -396,9 +427,10 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     __shared__ int s_red;
     __shared__ int s_nlist;
     __shared__ int s_ncells;
-    __shared__ int s_noff[2];
-    __shared__ int s_odx[2][kMaxOffsets];
-    __shared__ int s_ody[2][kMaxOffsets];
+    __shared__ int s_nadj, s_nfwd;
+    __shared__ int s_nq;
+    __shared__ int s_fdx[kMaxOffsets];
+    __shared__ int s_fdy[kMaxOffsets];
     __shared__ int s_nsten;
     __shared__ int s_sdx[kMaxStencil];
     __shared__ int s_sdy[kMaxStencil];
@@ -520,7 +552,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     // 3. counting sort by cell (wave 0 also builds the stencil tables)
     for (int32_t c = tid; c <= g.ncell; c += kThreads) cell[c] = 0;
     if (tid < 64)
-        build_stencil(g.reach, g.side, r, lane, s_dxmax, s_sdx, s_sdy, &s_nsten, s_odx, s_ody, s_noff);
+        build_stencil(g.reach, g.side, r, lane, s_dxmax, s_sdx, s_sdy, &s_nsten, s_fdx, s_fdy, &s_nadj, &s_nfwd);
     __syncthreads();
     uint32_t pv[kPtsPerThread];
     uint16_t prank[kPtsPerThread];
@@ -618,19 +650,54 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     // 6. union-find over core points (the smaller index always becomes the root)
     if (g.dense_ok) {
         // All cores of a cell are neighbours, so a cell's cores form one node
-        // (its smallest core index).  Two nodes are joined when some core pair
-        // across the cells is within eps.  Adjacent cells go first; by the
-        // second pass most farther pairs are already in one tree.
+        // (its smallest core index).  Adjacent cells first, then a flatten,
+        // then the farther cells: in clustered frames nearly every farther
+        // pair is joined by then, which the recorded roots show at once.  A
+        // lane takes one core cell (wave-uniform loops).  The work list is
+        // free here and holds the queue of open cell pairs.
         const int32_t ncl = s_ncells;
         const float inv_ncx = 1.0f / (float)g.ncx;
-        // adjacent cells first; by the second pass most farther pairs are
-        // already in one tree
-        for (int pass = 0; pass < 2; ++pass) {
-            for (int32_t j = tid; j < ncl; j += kThreads)
-                union_cell(j, clist, cell, parent, pxy, score, g, r, s_odx[pass], s_ody[pass], s_noff[pass],
-                           inv_ncx);
-            __syncthreads();
+        uint32_t *queue = reinterpret_cast<uint32_t *>(list);
+        const int qcap = cap / 2;
+        auto core_cell = [&](int32_t j, bool have) {
+            CoreCell A{};
+            if (have) {
+                A.ca = clist[j];
+                A.ay = div_small(A.ca, g.ncx, inv_ncx);
+                A.ax = A.ca - A.ay * g.ncx;
+                const uint32_t wa = cell[A.ca];
+                A.a0 = (int32_t)(wa & 0xffffu);
+                A.a1 = (int32_t)(cell[A.ca + 1] & 0xffffu);
+                A.node = (int32_t)(wa >> 16);
+                A.head = cell_head(pxy, score, A.a0, A.a1);
+            }
+            return A;
+        };
+        const int nadj = s_nadj, nfwd = s_nfwd;
+        if (tid == 0) s_nq = 0;
+        __syncthreads();
+        for (int32_t j0 = tid - lane; j0 < ncl; j0 += kThreads) {
+            const bool have = j0 + lane < ncl;
+            union_heads<4, false>(have, core_cell(j0 + lane, have), cell, parent, pxy, score, g, r, s_fdx, s_fdy, 0,
+                                  nadj, queue, &s_nq, qcap);
         }
+        __syncthreads();
+        union_queue(queue, min(s_nq, qcap), cell, parent, pxy, score, r);
+        __syncthreads();
+        for (int32_t j = tid; j < ncl; j += kThreads) {
+            const int32_t node = (int32_t)cnode(clist[j]);
+            st_rlx<kGroup>(parent + node, uf_root<kGroup>(parent, node));
+        }
+        if (tid == 0) s_nq = 0;
+        __syncthreads();
+        for (int32_t j0 = tid - lane; j0 < ncl; j0 += kThreads) {
+            const bool have = j0 + lane < ncl;
+            union_heads<8, true>(have, core_cell(j0 + lane, have), cell, parent, pxy, score, g, r, s_fdx, s_fdy, nadj,
+                                 nfwd, queue, &s_nq, qcap);
+        }
+        __syncthreads();
+        union_queue(queue, min(s_nq, qcap), cell, parent, pxy, score, r);
+        __syncthreads();
     } else {
         // coarsened grid: point-level unions (each pair once: the later point
         // of a cell, or the point in the earlier cell, does the work)
