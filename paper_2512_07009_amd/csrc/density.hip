@@ -235,7 +235,7 @@ __global__ __launch_bounds__(kRThreads) void density_recur_kernel(DensityArgs a,
 // Gather path
 // ---------------------------------------------------------------------------
 
-constexpr int kGWaves = 4;                 // waves per workgroup
+constexpr int kGWaves = 8;                 // waves per workgroup (two per SIMD)
 constexpr int kGThreads = 64 * kGWaves;
 constexpr int kGStep = 32;                 // birds per MFMA k-step (16 x 16 x 32)
 constexpr int kGRedTiles = 8;              // 16 x 16 tiles per round of the cross-wave sum
@@ -362,23 +362,6 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
     const int lane = tid & 63;
     const int wave = tid >> 6;
 
-    // the factor tables (exact: every distance is a multiple of 1/32 px)
-    auto build = [&](const GatherAxis &t) {
-        auto T = [&](int r, int i) -> _Float16 {
-            if (i < 1 || i > 2 * t.j + 1) return (_Float16)0.0f;
-            const float d = (((float)(i - 1 - t.j) + 0.5f) * (float)t.c - (float)r) * 0.0625f;
-            return (_Float16)__builtin_amdgcn_exp2f(d * d * gg.neg_k);
-        };
-        uint32_t *tab = reinterpret_cast<uint32_t *>(lds + t.tab);
-        const int nent = t.c * (PW + 16);
-        for (int e = tid; e < nent; e += kGThreads) {
-            const int r = e / (PW + 16), i = e % (PW + 16) - 16;
-            const _Float16 lo = T(r, i), hi = T(r, i + 16);
-            tab[e] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
-        }
-    };
-    build(gg.ay);
-    if (gg.ax.tab != gg.ay.tab) build(gg.ax);
 
     // this wave's item and its part of the item's birds
     const int per_wg = kGWaves / waves;
@@ -452,16 +435,44 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
         operands_x<TN, PW>(bx, rbx, vx, lds);
     };
 
-    int32_t qa = 0, qb = 0;
+    // the first coordinates are in flight while the tables are built
+    int32_t q0 = 0, qa = 0, qb = 0;
     if (nsteps > 0) {
-        const int32_t q0 = coord(0);
+        q0 = coord(0);
         qa = coord(1);
         qb = coord(2);
-        __syncthreads();  // tables written
-        put(0, q0);
-    } else {
-        __syncthreads();
     }
+    // the factor tables (exact: every distance is a multiple of 1/32 px), one
+    // row per thread: its PW factors in registers, then its pairs
+    auto build = [&](const GatherAxis &t) {
+        for (int r = tid; r < t.c; r += kGThreads) {
+            uint32_t v[PW];
+#pragma unroll
+            for (int i = 0; i < PW; ++i) {
+                float f = 0.0f;
+                if (i >= 1 && i <= 2 * t.j + 1) {
+                    const float d = (((float)(i - 1 - t.j) + 0.5f) * (float)t.c - (float)r) * 0.0625f;
+                    f = __builtin_amdgcn_exp2f(d * d * gg.neg_k);
+                }
+                v[i] = __builtin_bit_cast(uint16_t, (_Float16)f);
+            }
+            uint4 *row = reinterpret_cast<uint4 *>(lds + t.tab + r * (PW + 16) * 4);
+#pragma unroll
+            for (int q = 0; q < (PW + 16) / 4; ++q) {
+                uint32_t w[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int i = 4 * q + u - 16;  // entry i = (T(i), T(i + 16)); T = 0 past PW - 2
+                    w[u] = (i >= 0 ? v[i] : 0u) | ((i + 16 < PW ? v[i + 16] : 0u) << 16);
+                }
+                row[q] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+        }
+    };
+    build(gg.ay);
+    if (gg.ax.tab != gg.ay.tab) build(gg.ax);
+    __syncthreads();  // tables written
+    if (nsteps > 0) put(0, q0);
     half8 bx[TN];
     if (nsteps > 0) x_operands(0, bx);
     for (int32_t st = 0; st < nsteps; ++st) {
@@ -639,22 +650,36 @@ int env_int(const char *name) {
     return v ? std::atoi(v) : 0;
 }
 
-// Waves per work item and slices per (frame, region) of a gather launch:
-// enough waves for two per SIMD, each with at least kGMinWaveBirds birds on
-// average.  FLOCK_DENSITY_WAVES / FLOCK_DENSITY_SPLIT override (for tuning).
+// Waves per work item and slices per (frame, region) of a gather launch.  A
+// compute unit holds kGWaves waves (two per SIMD); with w waves per item an
+// item takes about 1/w of one wave's time, and the launch runs in
+// ceil(items * w / resident) rounds, so w minimises rounds / w (ties to fewer
+// waves, which add fewer tiles at the end).  FLOCK_DENSITY_WAVES / FLOCK_DENSITY_SPLIT
+// override (for tuning and tests).
 void gather_split(int32_t n_frames, int32_t total, long long regions, int n_cus, int *waves, int *split) {
     const long long items = (long long)n_frames * regions;
-    const long long target = 8LL * std::max(n_cus, 1);
-    int w = items >= target ? 1 : (2 * items >= target ? 2 : 4);
+    const long long resident = (long long)kGWaves * std::max(n_cus, 1);
+    int w = 1;
+    double best = 1e300;
+    for (int c = 1; c <= kGWaves; c *= 2) {
+        const double cost = (double)((items * c + resident - 1) / resident) / c;
+        if (cost < best * 0.999) {
+            best = cost;
+            w = c;
+        }
+    }
+    // slices only while one launch would leave most of the chip idle (the
+    // partial grids cost traffic), up to one round of waves, with at least
+    // kGMinWaveBirds birds per wave
     const double birds = n_frames > 0 ? (double)total / n_frames : 0.0;
     long long sp = 1;
-    if (items * w < target) {
-        sp = (target + items * w - 1) / (items * w);
+    if (2 * items * w < resident) {
+        sp = resident / (items * w);
         sp = std::min<long long>(sp, std::max<long long>(1, (long long)(birds / (w * kGMinWaveBirds))));
         sp = std::min<long long>(sp, 64);
     }
     const int fw = env_int("FLOCK_DENSITY_WAVES"), fs = env_int("FLOCK_DENSITY_SPLIT");
-    if (fw == 1 || fw == 2 || fw == 4) w = fw;
+    if (fw == 1 || fw == 2 || fw == 4 || fw == 8) w = fw;
     if (fs >= 1 && fs <= 64) sp = fs;
     *waves = w;
     *split = (int)sp;

@@ -278,9 +278,11 @@ def test_density_paths_gpu(path, w, h, gx, gy, sigma, frames, monkeypatch):
     print(f"density {path} {gx}x{gy}: worst rel err {worst:.2e}")
 
 
-def test_density_bird_slices_gpu():
-    """Few frames split into bird slices whose partial grids are added afterwards,
+@pytest.mark.parametrize("split", ["3", "16"])
+def test_density_bird_slices_gpu(split, monkeypatch):
+    """Frames split into bird slices whose partial grids are added afterwards,
     including frames with fewer birds than slices and an empty frame."""
+    monkeypatch.setenv("FLOCK_DENSITY_SPLIT", split)
     rng = np.random.default_rng(77)
     frames = [np.stack([rng.integers(0, 16 * 1920, n), rng.integers(0, 16 * 1080, n)], 1).astype(np.int32)
               for n in (6000, 3, 0, 700)]
