@@ -4,12 +4,17 @@
 One step = cluster_frames + density_frames over one batch of synthetic frames
 (default: 64 frames x 2000 birds, 1920x1080 px, eps 40 px, minPts 4, density
 grid 128x72, sigma 30 px).  The two calls are independent analytics of the
-same batch, so a step issues them on two streams (default priority) and joins;
-the same steps issued back to back on one stream are reported as
-sequential_frames_per_s.  Inputs are resident in device memory before the
-timed region; W warm-up steps, then K timed steps bracketed by device
-synchronisation.  Per-kernel durations come from HIP events recorded on the
-stream each kernel runs on, inside the timed region.
+same batch, so a step issues them on two streams (default priority) and joins.
+Inputs are resident in device memory before any timed region.
+
+Timed regions (each bracketed by device synchronisation):
+  1. `value`: K steps replayed from HIP graphs captured from the two-stream
+     step (a graph of up to 10 steps, replayed; host launch cost out of the
+     loop).  One replay is checked against the eager outputs first.
+  2. per-kernel durations for the roofline: the same K steps issued eagerly,
+     with HIP events recorded on the stream each kernel runs on
+     (`eager_frames_per_s` is that region's rate).
+  3. `sequential_frames_per_s`: K steps with both calls on one stream.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -99,6 +104,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=2.0,
                     help="target wall seconds for the oracle sample (all host cores)")
+    ap.add_argument("--no-graph", action="store_true", help="time `value` from eager launches")
     ap.add_argument("--calibrate-copy-mb", type=float, default=0,
                     help="also run one plain device copy of this many MiB (counter scaling)")
     args = ap.parse_args()
@@ -125,14 +131,16 @@ def main():
     kind = torch.empty(T, dtype=torch.uint8, device=dev)
     ncl = torch.empty(F, dtype=torch.int32, device=dev)
     dens = torch.empty((F, w.grid_h, w.grid_w), dtype=torch.float32, device=dev)
-    stream = torch.cuda.current_stream(dev)
+    stream = main_stream = torch.cuda.current_stream(dev)
     log(f"workload {w.name}: {F} frames, {T} birds, max {max_fp}/frame; {flock.version()}")
 
     side = torch.cuda.Stream(dev)  # default priority
 
-    def run_pair(k, concurrent, evs=None):
-        """cluster_frames on `stream`, density_frames on `side` (or also on
-        `stream` when not concurrent), with the join back on `stream`."""
+    def run_pair(k, concurrent, evs=None, launch_stream=None):
+        """cluster_frames on `stream` (or `launch_stream`), density_frames on
+        `side` (or also on the first stream when not concurrent), with the join
+        back on the first stream."""
+        stream = launch_stream if launch_stream is not None else main_stream
         ds = side if concurrent else stream
         if concurrent:
             fork = torch.cuda.Event()
@@ -180,11 +188,54 @@ def main():
         run_pair(k, True)
         run_pair(k, False)
     torch.cuda.synchronize(dev)
-
     K = args.steps
+
+    # 1. graph replay of the two-stream step
+    ref = (labels.clone(), kind.clone(), ncl.clone(), dens.clone())
+    graph_note = None
+    wall = None
+    if not args.no_graph:
+        try:
+            cap = torch.cuda.Stream(dev)
+            cap.wait_stream(stream)
+            gsteps = min(K, 10)
+            graphs = []
+            for n_in in sorted({gsteps, K % gsteps} - {0}, reverse=True):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cap):
+                    for k in range(n_in):
+                        run_pair(k, True, launch_stream=cap)
+                graphs.append((n_in, g))
+            torch.cuda.synchronize(dev)
+            labels.fill_(-7)
+            dens.fill_(-1.0)
+            graphs[0][1].replay()
+            torch.cuda.synchronize(dev)
+            same = (torch.equal(labels, ref[0]) and torch.equal(kind, ref[1]) and torch.equal(ncl, ref[2])
+                    and torch.equal(dens, ref[3]))
+            if not same:
+                raise RuntimeError("graph replay differs from the eager outputs")
+            plan = [graphs[0][1]] * (K // gsteps) + ([graphs[-1][1]] if K % gsteps else [])
+            for g in plan[:3]:
+                g.replay()
+            torch.cuda.synchronize(dev)
+            t0 = time.perf_counter()
+            for g in plan:
+                g.replay()
+            torch.cuda.synchronize(dev)
+            wall = time.perf_counter() - t0
+        except RuntimeError as ex:
+            graph_note = f"graph replay unavailable ({ex}); value timed eagerly"
+            log(graph_note)
+            wall = None
+
+    # 2. eager steps with per-kernel events; 3. one stream
+    wall_eager, t_cluster, t_density = timed(True, K)
     wall_seq, _, _ = timed(False, K)
-    wall, t_cluster, t_density = timed(True, K)
-    ms_per_step = wall / K * 1e3
+    if wall is None:
+        wall = wall_eager
+    ms_per_step = wall / K
+    ms_per_step *= 1e3
     value = F / (wall / K)
 
     # algorithmic work per launch
@@ -219,7 +270,9 @@ def main():
                    "frame_px": [w.width_px, w.height_px], "eps_px": w.eps_px, "min_pts": w.min_pts,
                    "grid": [w.grid_w, w.grid_h], "sigma_px": w.sigma_px, "parallelism": "single-gpu"},
         "birds_per_s": T / (wall / K),
+        "eager_frames_per_s": F / (wall_eager / K),
         "sequential_frames_per_s": F / (wall_seq / K),
+        "timing": graph_note or "value: HIP graph replay of the two-stream step; kernels: eager events",
         "roofline": roof,
         "kernels": {"cluster_frames": cl, "density_frames": de},
     }
