@@ -8,13 +8,15 @@ same batch, so a step issues them on two streams (default priority) and joins.
 Inputs are resident in device memory before any timed region.
 
 Timed regions (each bracketed by device synchronisation):
-  1. `value`: K steps replayed from HIP graphs captured from the two-stream
-     step (a graph of up to 10 steps, replayed; host launch cost out of the
-     loop).  One replay is checked against the eager outputs first.
-  2. per-kernel durations for the roofline: the same K steps issued eagerly,
-     with HIP events recorded on the stream each kernel runs on
-     (`eager_frames_per_s` is that region's rate).
-  3. `sequential_frames_per_s`: K steps with both calls on one stream.
+  1. K steps replayed from HIP graphs captured from the step (graphs of up
+     to 10 steps; host launch cost out of the loop), once with the two calls
+     on two streams and once on one stream.  One replay of each is checked
+     against the eager outputs first.  `value` is the faster of the two
+     (`config.streams` says which): on large batches the two kernels compete
+     for compute units and one stream wins.
+  2. per-kernel durations for the roofline: the same K steps issued eagerly
+     in the same mode, with HIP events recorded on the stream each kernel
+     runs on.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -190,52 +192,56 @@ def main():
     torch.cuda.synchronize(dev)
     K = args.steps
 
-    # 1. graph replay of the two-stream step
+    # 1. graph replays: the two-stream step and the one-stream step
     ref = (labels.clone(), kind.clone(), ncl.clone(), dens.clone())
     graph_note = None
-    wall = None
+    walls = {}
     if not args.no_graph:
         try:
             cap = torch.cuda.Stream(dev)
             cap.wait_stream(stream)
             gsteps = min(K, 10)
-            graphs = []
-            for n_in in sorted({gsteps, K % gsteps} - {0}, reverse=True):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=cap):
-                    for k in range(n_in):
-                        run_pair(k, True, launch_stream=cap)
-                graphs.append((n_in, g))
-            torch.cuda.synchronize(dev)
-            labels.fill_(-7)
-            dens.fill_(-1.0)
-            graphs[0][1].replay()
-            torch.cuda.synchronize(dev)
-            same = (torch.equal(labels, ref[0]) and torch.equal(kind, ref[1]) and torch.equal(ncl, ref[2])
-                    and torch.equal(dens, ref[3]))
-            if not same:
-                raise RuntimeError("graph replay differs from the eager outputs")
-            plan = [graphs[0][1]] * (K // gsteps) + ([graphs[-1][1]] if K % gsteps else [])
-            for g in plan[:3]:
-                g.replay()
-            torch.cuda.synchronize(dev)
-            t0 = time.perf_counter()
-            for g in plan:
-                g.replay()
-            torch.cuda.synchronize(dev)
-            wall = time.perf_counter() - t0
+            for concurrent in (True, False):
+                graphs = []
+                for n_in in sorted({gsteps, K % gsteps} - {0}, reverse=True):
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=cap):
+                        for k in range(n_in):
+                            run_pair(k, concurrent, launch_stream=cap)
+                    graphs.append(g)
+                torch.cuda.synchronize(dev)
+                labels.fill_(-7)
+                dens.fill_(-1.0)
+                graphs[0].replay()
+                torch.cuda.synchronize(dev)
+                same = (torch.equal(labels, ref[0]) and torch.equal(kind, ref[1]) and torch.equal(ncl, ref[2])
+                        and torch.equal(dens, ref[3]))
+                if not same:
+                    raise RuntimeError("graph replay differs from the eager outputs")
+                plan = [graphs[0]] * (K // gsteps) + ([graphs[-1]] if K % gsteps else [])
+                for g in plan[:3]:
+                    g.replay()
+                torch.cuda.synchronize(dev)
+                t0 = time.perf_counter()
+                for g in plan:
+                    g.replay()
+                torch.cuda.synchronize(dev)
+                walls[concurrent] = time.perf_counter() - t0
         except RuntimeError as ex:
             graph_note = f"graph replay unavailable ({ex}); value timed eagerly"
             log(graph_note)
-            wall = None
+            walls = {}
 
-    # 2. eager steps with per-kernel events; 3. one stream
+    # 2. eager steps with per-kernel events, two streams and one stream
     wall_eager, t_cluster, t_density = timed(True, K)
-    wall_seq, _, _ = timed(False, K)
-    if wall is None:
-        wall = wall_eager
-    ms_per_step = wall / K
-    ms_per_step *= 1e3
+    wall_seq, t_cluster_seq, t_density_seq = timed(False, K)
+    if not walls:
+        walls = {True: wall_eager, False: wall_seq}
+    concurrent = walls[True] <= walls[False]
+    wall = walls[concurrent]
+    if not concurrent:
+        t_cluster, t_density = t_cluster_seq, t_density_seq
+    ms_per_step = wall / K * 1e3
     value = F / (wall / K)
 
     # algorithmic work per launch
@@ -268,11 +274,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "frames": F, "birds": T, "birds_per_frame_max": max_fp,
                    "frame_px": [w.width_px, w.height_px], "eps_px": w.eps_px, "min_pts": w.min_pts,
-                   "grid": [w.grid_w, w.grid_h], "sigma_px": w.sigma_px, "parallelism": "single-gpu"},
+                   "grid": [w.grid_w, w.grid_h], "sigma_px": w.sigma_px, "parallelism": "single-gpu",
+                   "streams": 2 if concurrent else 1},
         "birds_per_s": T / (wall / K),
-        "eager_frames_per_s": F / (wall_eager / K),
-        "sequential_frames_per_s": F / (wall_seq / K),
-        "timing": graph_note or "value: HIP graph replay of the two-stream step; kernels: eager events",
+        "two_stream_frames_per_s": F / (walls[True] / K),
+        "one_stream_frames_per_s": F / (walls[False] / K),
+        "eager_two_stream_frames_per_s": F / (wall_eager / K),
+        "eager_one_stream_frames_per_s": F / (wall_seq / K),
+        "timing": graph_note or ("value: HIP graph replay of the faster of the two-stream and one-stream steps; "
+                                 "kernel durations: HIP events in the eager run of the same mode"),
         "roofline": roof,
         "kernels": {"cluster_frames": cl, "density_frames": de},
     }
