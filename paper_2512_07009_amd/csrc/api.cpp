@@ -207,6 +207,12 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     a.kind = kind;
     a.n_clusters = n_clusters;
     a.big_path = big ? 1 : 0;
+    {
+        // FLOCK_CLUSTER_UNION=lds takes the general union stage for every
+        // frame (for tests of that path)
+        const char *u = std::getenv("FLOCK_CLUSTER_UNION");
+        a.union_regs = (u && std::strcmp(u, "lds") == 0) ? 0 : 1;
+    }
     hipError_t err = flock::launch_cluster_resident(a, plan.lds_bytes, s);
     if (err != hipSuccess) return hip_fail(err, "cluster kernel launch");
     if (big && total > 0) {

@@ -53,7 +53,7 @@ constexpr int kTile = 1024;  // points per LDS tile on the in-place path
 // In-place path for frames above the on-chip capacity
 // ---------------------------------------------------------------------------
 
-__device__ void cluster_frame_inplace(const ClusterArgs &a, int f, int32_t b, int32_t n,
+__device__ __forceinline__ void cluster_frame_inplace(const ClusterArgs &a, int f, int32_t b, int32_t n,
                                       unsigned char *smem, int *red) {
     const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
     int32_t *par = a.labels + b;
@@ -252,7 +252,7 @@ __device__ __forceinline__ int32_t div_small(int32_t x, int32_t d, float inv_d) 
 //   fdx/fdy   its forward half (cells later in row-major order), the
 //             nadj adjacent cells first, nfwd in all (at most 4 + 8)
 //   dxmax[k]  the widest |dx| in row |dy| = k
-__device__ void build_stencil(int32_t reach, int32_t side, const Radius &r, int lane, int *dxmax, int *sdx,
+__device__ __forceinline__ void build_stencil(int32_t reach, int32_t side, const Radius &r, int lane, int *dxmax, int *sdx,
                               int *sdy, int *nsten, int *fdx, int *fdy, int *nadj, int *nfwd) {
     const int dx = lane % 5 - 2, dy = lane / 5 - 2;
     const int adx = dx < 0 ? -dx : dx, ady = dy < 0 ? -dy : dy;
@@ -335,76 +335,427 @@ struct CoreCell {
     CellHead head;
 };
 
-// Append `flag` lanes' values to a queue of `cap` entries (wave-uniform call);
-// returns true for a flagged lane whose entry did not fit.
-__device__ __forceinline__ bool wave_enqueue(bool flag, uint32_t value, uint32_t *queue, int *counter, int cap) {
-    const uint64_t m = __ballot(flag);
-    if (m == 0) return false;
-    const int lane = threadIdx.x & 63;
-    int base = 0;
-    if (lane == 0) base = atomicAdd(counter, __popcll(m));
-    base = __shfl(base, 0, 64);
-    const int at = base + __popcll(m & ((1ull << lane) - 1ull));
-    if (flag && at < cap) queue[at] = value;
-    return flag && at >= cap;
+constexpr uint32_t kDeadPair = 0xffffffffu;
+
+// Exclusive prefix sum and total over the wave of per-lane counts below 16
+// (wave-uniform call): one ballot per bit of the count.
+__device__ __forceinline__ int wave_prefix16(int cnt, int *total) {
+    const uint64_t below = (1ull << (threadIdx.x & 63)) - 1ull;
+    int pre = 0, tot = 0;
+#pragma unroll
+    for (int bit = 0; bit < 4; ++bit) {
+        const uint64_t m = __ballot((cnt >> bit) & 1);
+        pre += __popcll(m & below) << bit;
+        tot += __popcll(m) << bit;
+    }
+    *total = tot;
+    return pre;
 }
 
-// One pass of cell unions over this lane's core cell A (if `have`), forward
-// offsets fdx/fdy[o0, o1) with o1 - o0 <= NO (wave-uniform call).  A
-// neighbour holding a core is joined when a core pair across the two cells is
-// within eps; all cores of a cell form one node, since any two points of a
-// cell are neighbours.
-//   far = false: the adjacent cells;
-//   far = true:  the farther cells, after the adjacent unions and a flatten:
-//                a pair whose recorded roots agree is already joined (joins
-//                only merge trees) and is skipped.
-// The heads of both cells settle most pairs here.  The rest go to `queue` as
-// (cell A, cell B), to be tested after a barrier by one lane each, so that the
-// few long scans share a few waves instead of holding up every wave.
+// Edges from core cell A (if `have`) to its neighbours at the forward offsets
+// fdx/fdy[o0 + k], k < NO, o0 + k < o1 (wave-uniform call): bit k of the
+// result is set when some core of A lies within eps of some core of the
+// neighbour.  All cores of a cell are neighbours, so a cell's cores form one
+// node of the graph (its smallest core index).
+//   far = false: every neighbour holding a core;
+//   far = true:  only neighbours whose root differs from A's (the forest is
+//                flat here, so equal roots mean already connected).
+// The first two points of both cells settle most pairs.  The pairs they leave
+// open go to `queue` as (cell A | cell B << 16), to be tested after a barrier
+// by one lane each, so that the few long scans share a few waves instead of
+// holding up every wave; pairs beyond its capacity are tested here.
 template <int NO, bool far>
-__device__ __forceinline__ void union_heads(bool have, const CoreCell &A, const uint32_t *cell, int32_t *parent,
-                                            const uint32_t *pxy, const uint8_t *score, const Grid &g,
-                                            const Radius &r, const int *fdx, const int *fdy, int o0, int o1,
-                                            uint32_t *queue, int *nq, int qcap) {
+__device__ __forceinline__ uint32_t cell_edges(bool have, const CoreCell &A, const uint32_t *cell,
+                                               const int32_t *parent, const uint32_t *pxy, const uint8_t *score,
+                                               const Grid &g, const Radius &r, const int *fdx, const int *fdy,
+                                               int o0, int o1, uint32_t *queue, int *nq, int qcap) {
     const int32_t ra = far && have ? ld_rlx<kGroup>(parent + A.node) : 0;
+    uint32_t touch = 0, open = 0;
+    int32_t cbs[NO];
 #pragma unroll
     for (int k = 0; k < NO; ++k) {
+        cbs[k] = 0;
         const int o = o0 + k;
-        if (o >= o1) break;  // wave-uniform
-        bool open = false;
-        int32_t cb = 0, nb = 0;
-        if (have) {
-            const int32_t bx = A.ax + fdx[o], by = A.ay + fdy[o];
-            if (!((bx < 0) | (bx >= g.ncx) | (by >= g.ncy))) {
-                cb = by * g.ncx + bx;
-                const uint32_t wb = cell[cb];
-                nb = (int32_t)(wb >> 16);
-                if (nb != (int32_t)kNone && !(far && ld_rlx<kGroup>(parent + nb) == ra)) {
-                    const int32_t b0 = (int32_t)(wb & 0xffffu), b1 = (int32_t)(cell[cb + 1] & 0xffffu);
-                    const CellHead B = cell_head(pxy, score, b0, b1);
-                    if (heads_touch(A.head, B, r)) uf_unite<kGroup>(parent, A.node, nb);
-                    else open = (A.a1 - A.a0 > 2) | (b1 - b0 > 2);
-                }
-            }
-        }
-        if (wave_enqueue(open, (uint32_t)A.ca | ((uint32_t)cb << 16), queue, nq, qcap)) {
-            // queue full: test here
-            const int32_t b0 = (int32_t)(cell[cb] & 0xffffu), b1 = (int32_t)(cell[cb + 1] & 0xffffu);
-            if (cells_touch(pxy, score, A.a0, A.a1, b0, b1, r)) uf_unite<kGroup>(parent, A.node, nb);
-        }
+        if (!have || o >= o1) continue;
+        const int32_t bx = A.ax + fdx[o], by = A.ay + fdy[o];
+        if ((bx < 0) | (bx >= g.ncx) | (by >= g.ncy)) continue;
+        const int32_t cb = by * g.ncx + bx;
+        cbs[k] = cb;
+        const uint32_t wb = cell[cb];
+        const int32_t nb = (int32_t)(wb >> 16);
+        if (nb == (int32_t)kNone) continue;
+        if (far && ld_rlx<kGroup>(parent + nb) == ra) continue;
+        const int32_t b0 = (int32_t)(wb & 0xffffu), b1 = (int32_t)(cell[cb + 1] & 0xffffu);
+        const CellHead B = cell_head(pxy, score, b0, b1);
+        if (heads_touch(A.head, B, r)) touch |= 1u << k;
+        else if ((A.a1 - A.a0 > 2) | (b1 - b0 > 2)) open |= 1u << k;
     }
+    int total;
+    const int pre = wave_prefix16(__popc(open), &total);
+    if (total == 0) return touch;  // wave-uniform
+    int base = 0;
+    if ((threadIdx.x & 63) == 0) base = atomicAdd(nq, total);
+    base = __shfl(base, 0, 64);
+    int at = base + pre;
+#pragma unroll
+    for (int k = 0; k < NO; ++k) {
+        if (!((open >> k) & 1u)) continue;
+        const int32_t cb = cbs[k];
+        if (at < qcap) {
+            queue[at] = (uint32_t)A.ca | ((uint32_t)cb << 16);
+        } else if (cells_touch(pxy, score, A.a0, A.a1, (int32_t)(cell[cb] & 0xffffu),
+                               (int32_t)(cell[cb + 1] & 0xffffu), r)) {
+            touch |= 1u << k;
+        }
+        ++at;
+    }
+    return touch;
 }
 
-// The queued cell pairs, one lane each.
-__device__ __forceinline__ void union_queue(const uint32_t *queue, int nq, const uint32_t *cell, int32_t *parent,
-                                            const uint32_t *pxy, const uint8_t *score, const Radius &r) {
+// Tests the queued cell pairs, one lane each; a pair with no core pair within
+// eps is marked dead.
+__device__ __forceinline__ void resolve_queue(uint32_t *queue, int nq, const uint32_t *cell, const uint32_t *pxy,
+                                              const uint8_t *score, const Radius &r) {
     for (int t = threadIdx.x; t < nq; t += kThreads) {
         const uint32_t e = queue[t];
         const int32_t ca = (int32_t)(e & 0xffffu), cb = (int32_t)(e >> 16);
-        const uint32_t wa = cell[ca], wb = cell[cb];
-        if (cells_touch(pxy, score, (int32_t)(wa & 0xffffu), (int32_t)(cell[ca + 1] & 0xffffu),
-                        (int32_t)(wb & 0xffffu), (int32_t)(cell[cb + 1] & 0xffffu), r))
-            uf_unite<kGroup>(parent, (int32_t)(wa >> 16), (int32_t)(wb >> 16));
+        if (!cells_touch(pxy, score, (int32_t)(cell[ca] & 0xffffu), (int32_t)(cell[ca + 1] & 0xffffu),
+                         (int32_t)(cell[cb] & 0xffffu), (int32_t)(cell[cb + 1] & 0xffffu), r))
+            queue[t] = kDeadPair;
+    }
+}
+
+// Hook step of the connected-components rounds for node a and its neighbours
+// nb[k] (bit k of m): their parents (roots as of the last jump step, or
+// parents lowered since, all within the components of these nodes) are
+// joined under the smallest of them by an atomic minimum, which keeps
+// parent[x] <= x.  Returns true if any two differed.
+template <int NO>
+__device__ __forceinline__ bool hook_node(int32_t *parent, int32_t a, const int32_t (&nb)[NO], uint32_t m) {
+    const int32_t pa = ld_rlx<kGroup>(parent + a);
+    int32_t pb[NO];
+    int32_t lo = pa;
+#pragma unroll
+    for (int k = 0; k < NO; ++k) {
+        pb[k] = ((m >> k) & 1u) ? ld_rlx<kGroup>(parent + nb[k]) : pa;
+        lo = min(lo, pb[k]);
+    }
+    bool any = false;
+    if (pa != lo) {
+        __hip_atomic_fetch_min(parent + pa, lo, __ATOMIC_RELAXED, kGroup);
+        any = true;
+    }
+#pragma unroll
+    for (int k = 0; k < NO; ++k)
+        if (pb[k] != lo) {
+            __hip_atomic_fetch_min(parent + pb[k], lo, __ATOMIC_RELAXED, kGroup);
+            any = true;
+        }
+    return any;
+}
+
+// Jump step: node a's parent becomes its root (read-only walk; concurrent
+// writers only store roots, so every walk ends at the same root).
+__device__ __forceinline__ void jump_node(int32_t *parent, int32_t a) {
+    int32_t x = ld_rlx<kGroup>(parent + a);
+    for (;;) {
+        const int32_t p = ld_rlx<kGroup>(parent + x);
+        if (p == x) break;
+        x = p;
+    }
+    st_rlx<kGroup>(parent + a, x);
+}
+
+// Core cells per lane whose node, neighbour nodes and edge bits stay in
+// registers through the connected-components rounds.
+constexpr int kRegCells = 3;
+
+// State of one frame that the union stages share.
+struct UnionCtx {
+    uint32_t *cell;  // the node half holds roots after the adjacent stage
+    int32_t *parent;
+    const uint32_t *pxy;
+    const uint8_t *score;
+    const uint16_t *clist;
+    uint16_t *emask;  // edge bits per core cell; 4-byte aligned
+    uint32_t *queue;  // open pairs: core-cell index j | offset index k << 16
+    int qcap;
+    int *nq;
+    int *hook3;
+    const int *fdx, *fdy;
+    Grid g;
+    Radius r;
+    int32_t ncl;
+    float inv_ncx;
+};
+
+__device__ __forceinline__ CoreCell load_core_cell(const UnionCtx &u, int32_t j, bool have) {
+    CoreCell A{};
+    if (have) {
+        A.ca = u.clist[j];
+        A.ay = div_small(A.ca, u.g.ncx, u.inv_ncx);
+        A.ax = A.ca - A.ay * u.g.ncx;
+        const uint32_t wa = u.cell[A.ca];
+        A.a0 = (int32_t)(wa & 0xffffu);
+        A.a1 = (int32_t)(u.cell[A.ca + 1] & 0xffffu);
+        A.node = (int32_t)(wa >> 16);
+        A.head = cell_head(u.pxy, u.score, A.a0, A.a1);
+    }
+    return A;
+}
+
+// cell_edges for the register stages: also returns every neighbour's node in
+// nb[k] (A's own node where there is none), and queues open pairs as
+// (j | k << 16) for resolve_queue_coop.
+template <int NO, bool far>
+__device__ __forceinline__ uint32_t cell_edges_nb(bool have, const CoreCell &A, int32_t j, const UnionCtx &u, int o0,
+                                                  int o1, int32_t (&nb)[NO]) {
+    const int32_t ra = far && have ? ld_rlx<kGroup>(u.parent + A.node) : 0;
+    uint32_t touch = 0, open = 0;
+    int32_t cbs[NO];
+#pragma unroll
+    for (int k = 0; k < NO; ++k) {
+        nb[k] = A.node;
+        cbs[k] = 0;
+        const int o = o0 + k;
+        if (!have || o >= o1) continue;
+        const int32_t bx = A.ax + u.fdx[o], by = A.ay + u.fdy[o];
+        if ((bx < 0) | (bx >= u.g.ncx) | (by >= u.g.ncy)) continue;
+        const int32_t cb = by * u.g.ncx + bx;
+        cbs[k] = cb;
+        const uint32_t wb = u.cell[cb];
+        const int32_t n = (int32_t)(wb >> 16);
+        if (n == (int32_t)kNone) continue;
+        nb[k] = n;
+        if (far && ld_rlx<kGroup>(u.parent + n) == ra) continue;
+        const int32_t b0 = (int32_t)(wb & 0xffffu), b1 = (int32_t)(u.cell[cb + 1] & 0xffffu);
+        const CellHead B = cell_head(u.pxy, u.score, b0, b1);
+        if (heads_touch(A.head, B, u.r)) touch |= 1u << k;
+        else if ((A.a1 - A.a0 > 2) | (b1 - b0 > 2)) open |= 1u << k;
+    }
+    int total;
+    const int pre = wave_prefix16(__popc(open), &total);
+    if (total == 0) return touch;  // wave-uniform
+    int base = 0;
+    if ((threadIdx.x & 63) == 0) base = atomicAdd(u.nq, total);
+    base = __shfl(base, 0, 64);
+    int at = base + pre;
+#pragma unroll
+    for (int k = 0; k < NO; ++k) {
+        if (!((open >> k) & 1u)) continue;
+        const int32_t cb = cbs[k];
+        if (at < u.qcap) {
+            u.queue[at] = (uint32_t)j | ((uint32_t)k << 16);
+        } else if (cells_touch(u.pxy, u.score, A.a0, A.a1, (int32_t)(u.cell[cb] & 0xffffu),
+                               (int32_t)(u.cell[cb + 1] & 0xffffu), u.r)) {
+            touch |= 1u << k;
+        }
+        ++at;
+    }
+    return touch;
+}
+
+// True if core point va has a core neighbour among the sorted points q0,
+// q0 + step, ... below q1 (four loads in flight at a time).
+__device__ __forceinline__ bool core_near_strided(const UnionCtx &u, uint32_t va, int32_t q0, int32_t q1,
+                                                  int32_t step) {
+    int32_t q = q0;
+    for (; q + 3 * step < q1; q += 4 * step) {
+        const uint32_t w0 = u.pxy[q], w1 = u.pxy[q + step], w2 = u.pxy[q + 2 * step], w3 = u.pxy[q + 3 * step];
+        const bool h = ((u.score[q] != 0) & (sq_dist_pk(va, w0, u.r.e1) <= u.r.e2)) |
+                       ((u.score[q + step] != 0) & (sq_dist_pk(va, w1, u.r.e1) <= u.r.e2)) |
+                       ((u.score[q + 2 * step] != 0) & (sq_dist_pk(va, w2, u.r.e1) <= u.r.e2)) |
+                       ((u.score[q + 3 * step] != 0) & (sq_dist_pk(va, w3, u.r.e1) <= u.r.e2));
+        if (h) return true;
+    }
+    for (; q < q1; q += step)
+        if ((u.score[q] != 0) & (sq_dist_pk(va, u.pxy[q], u.r.e1) <= u.r.e2)) return true;
+    return false;
+}
+
+// Most lanes that share one queued pair in resolve_queue_coop.
+constexpr int kMaxPairLanes = 8;
+
+// Tests the queued pairs (j | k << 16) in one pass where they fit: G lanes
+// per pair (a power of two, at most kMaxPairLanes, with nq G <= kThreads where
+// possible).  Lane i of a group takes core cell j's points i, i + G, ... and
+// scans all of cell B (at offset o0 + k) for a core within eps, stopping at
+// its first hit; a hit in the group sets bit k of cell j's edge bits.
+// Wave-uniform call.
+__device__ __forceinline__ void resolve_queue_coop(const UnionCtx &u, int nq, int o0) {
+    uint32_t *mask32 = reinterpret_cast<uint32_t *>(u.emask);
+    const int tid = threadIdx.x, lane = tid & 63;
+    int G = 1;
+    while (G < kMaxPairLanes && nq * 2 * G <= kThreads) G *= 2;
+    const int gl = lane & (G - 1);
+    const uint64_t gmask = ((1ull << G) - 1ull) << (lane & ~(G - 1));
+    for (int t0 = (tid - lane) / G; t0 < nq; t0 += kThreads / G) {
+        const int t = t0 + lane / G;
+        bool hit = false;
+        int32_t j = 0, k = 0;
+        if (t < nq) {
+            const uint32_t e = u.queue[t];
+            j = (int32_t)(e & 0xffffu);
+            k = (int32_t)(e >> 16);
+            const int32_t ca = u.clist[j];
+            const int32_t ay = div_small(ca, u.g.ncx, u.inv_ncx), ax = ca - ay * u.g.ncx;
+            const int32_t cb = (ay + u.fdy[o0 + k]) * u.g.ncx + ax + u.fdx[o0 + k];
+            const int32_t a1 = (int32_t)(u.cell[ca + 1] & 0xffffu);
+            const int32_t b0 = (int32_t)(u.cell[cb] & 0xffffu), b1 = (int32_t)(u.cell[cb + 1] & 0xffffu);
+            for (int32_t qa = (int32_t)(u.cell[ca] & 0xffffu) + gl; qa < a1 && !hit; qa += G)
+                if (u.score[qa]) hit = core_near_strided(u, u.pxy[qa], b0, b1, 1);
+        }
+        const uint64_t hits = __ballot(hit);
+        if (gl == 0 && (hits & gmask)) atomicOr(mask32 + (j >> 1), (1u << k) << (16 * (j & 1)));
+    }
+}
+
+// Far-stage candidates of core cell A (cell ca at column ax, row ay, root ra
+// in the cell table): the neighbours at offsets o0 + k, k < NO, o0 + k < o1,
+// that hold a core and have another root; nb[k] gets that root (ra where
+// there is none).  Candidates go to the queue as (j | k << 16), or, beyond its
+// capacity, are tested here (bit k of the result).  Wave-uniform call.
+template <int NO>
+__device__ __forceinline__ uint32_t far_candidates(bool have, int32_t ca, int32_t ax, int32_t ay, int32_t ra,
+                                                   int32_t j, const UnionCtx &u, int o0, int o1,
+                                                   int32_t (&nb)[NO]) {
+    uint32_t cand = 0;
+    int32_t cbs[NO];
+#pragma unroll
+    for (int k = 0; k < NO; ++k) {
+        nb[k] = ra;
+        cbs[k] = 0;
+        const int o = o0 + k;
+        if (!have || o >= o1) continue;
+        const int32_t bx = ax + u.fdx[o], by = ay + u.fdy[o];
+        if ((bx < 0) | (bx >= u.g.ncx) | (by >= u.g.ncy)) continue;
+        const int32_t cb = by * u.g.ncx + bx;
+        const int32_t rb = (int32_t)(u.cell[cb] >> 16);
+        if ((rb == (int32_t)kNone) | (rb == ra)) continue;
+        nb[k] = rb;
+        cbs[k] = cb;
+        cand |= 1u << k;
+    }
+    int total;
+    const int pre = wave_prefix16(__popc(cand), &total);
+    if (total == 0) return 0;  // wave-uniform
+    int base = 0;
+    if ((threadIdx.x & 63) == 0) base = atomicAdd(u.nq, total);
+    base = __shfl(base, 0, 64);
+    int at = base + pre;
+    uint32_t touch = 0;
+#pragma unroll
+    for (int k = 0; k < NO; ++k) {
+        if (!((cand >> k) & 1u)) continue;
+        if (at < u.qcap) {
+            u.queue[at] = (uint32_t)j | ((uint32_t)k << 16);
+        } else {
+            const int32_t cb = cbs[k];
+            if (cells_touch(u.pxy, u.score, (int32_t)(u.cell[ca] & 0xffffu), (int32_t)(u.cell[ca + 1] & 0xffffu),
+                            (int32_t)(u.cell[cb] & 0xffffu), (int32_t)(u.cell[cb + 1] & 0xffffu), u.r))
+                touch |= 1u << k;
+        }
+        ++at;
+    }
+    return touch;
+}
+
+// Connected-components rounds over every lane's core cells (j = tid +
+// c kThreads; node, neighbour nodes nb and edge bits m in registers): hook
+// every edge's two roots under the smaller, then every node jumps to its
+// root, until a round hooks nothing.  `round` numbers the rounds across
+// stages (hook3[round % 3] says whether round `round` hooked; three slots, so
+// that one is cleared while the previous one may still be read).
+// Wave-uniform call.
+template <int NO>
+__device__ __forceinline__ void cc_rounds(const UnionCtx &u, const int32_t (&node)[kRegCells],
+                                          const int32_t (&nb)[kRegCells][NO], const uint32_t (&m)[kRegCells],
+                                          int &round) {
+    const int tid = threadIdx.x;
+    // a round that hooks leaves fewer roots, so ncl + 1 rounds always
+    // suffice; the bound only guarantees that the loop ends
+    const int last = round + u.ncl + 1;
+    for (;; ++round) {
+        if (tid == 0) u.hook3[(round + 1) % 3] = 0;
+        bool any = false;
+#pragma unroll
+        for (int c = 0; c < kRegCells; ++c)
+            if (m[c]) any |= hook_node<NO>(u.parent, node[c], nb[c], m[c]);
+        if (any) u.hook3[round % 3] = 1;
+        __syncthreads();
+        if (!u.hook3[round % 3] || round >= last) break;  // every edge joins equal roots
+#pragma unroll
+        for (int c = 0; c < kRegCells; ++c)
+            if (tid + c * kThreads < u.ncl) jump_node(u.parent, node[c]);
+        __syncthreads();
+    }
+    ++round;
+}
+
+// The cell unions with every lane's core cells (j = tid + c kThreads) in
+// registers.  Adjacent stage: edges from the first two points of both cells,
+// open pairs tested by resolve_queue_coop, then rounds.  Each core cell's
+// root then replaces its node in the cell table (any member of a tree serves
+// as its node from here on).  Far stage: only pairs with different roots are
+// candidates, all tested by resolve_queue_coop, then rounds.  Wave-uniform
+// call.
+__device__ __forceinline__ void union_regs(const UnionCtx &u, int nadj, int nfwd, int &round) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    int32_t ca[kRegCells], node[kRegCells];
+    {
+        int32_t nb[kRegCells][4];
+        uint32_t m[kRegCells];
+        if (tid == 0) *u.nq = 0;
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < kRegCells; ++c) {
+            const int32_t j = tid + c * kThreads;
+            const bool have = j < u.ncl;
+            ca[c] = 0;
+            node[c] = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) nb[c][k] = 0;
+            if (tid - lane + c * kThreads >= u.ncl) continue;  // wave-uniform
+            const CoreCell A = load_core_cell(u, j, have);
+            ca[c] = A.ca;
+            node[c] = A.node;
+            const uint32_t t = cell_edges_nb<4, false>(have, A, j, u, 0, nadj, nb[c]);
+            if (have) u.emask[j] = (uint16_t)t;
+        }
+        __syncthreads();
+        resolve_queue_coop(u, min(*u.nq, u.qcap), 0);
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < kRegCells; ++c) m[c] = tid + c * kThreads < u.ncl ? u.emask[tid + c * kThreads] : 0u;
+        cc_rounds<4>(u, node, nb, m, round);
+    }
+#pragma unroll
+    for (int c = 0; c < kRegCells; ++c)
+        if (tid + c * kThreads < u.ncl)
+            u.cell[ca[c]] = (u.cell[ca[c]] & 0xffffu) | ((uint32_t)ld_rlx<kGroup>(u.parent + node[c]) << 16);
+    if (tid == 0) *u.nq = 0;
+    __syncthreads();
+    {
+        int32_t nb[kRegCells][8];
+        uint32_t m[kRegCells];
+#pragma unroll
+        for (int c = 0; c < kRegCells; ++c) {
+            const int32_t j = tid + c * kThreads;
+            const bool have = j < u.ncl;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) nb[c][k] = 0;
+            if (tid - lane + c * kThreads >= u.ncl) continue;  // wave-uniform
+            const int32_t ay = div_small(ca[c], u.g.ncx, u.inv_ncx), ax = ca[c] - ay * u.g.ncx;
+            const int32_t ra = have ? (int32_t)(u.cell[ca[c]] >> 16) : 0;
+            const uint32_t t = far_candidates<8>(have, ca[c], ax, ay, ra, j, u, nadj, nfwd, nb[c]);
+            if (have) u.emask[j] = (uint16_t)t;
+        }
+        __syncthreads();
+        resolve_queue_coop(u, min(*u.nq, u.qcap), nadj);
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < kRegCells; ++c) m[c] = tid + c * kThreads < u.ncl ? u.emask[tid + c * kThreads] : 0u;
+        cc_rounds<8>(u, node, nb, m, round);
     }
 }
 
@@ -429,6 +780,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     __shared__ int s_ncells;
     __shared__ int s_nadj, s_nfwd;
     __shared__ int s_nq;
+    __shared__ int s_hook[3];
     __shared__ int s_fdx[kMaxOffsets];
     __shared__ int s_fdy[kMaxOffsets];
     __shared__ int s_nsten;
@@ -650,54 +1002,111 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     // 6. union-find over core points (the smaller index always becomes the root)
     if (g.dense_ok) {
         // All cores of a cell are neighbours, so a cell's cores form one node
-        // (its smallest core index).  Adjacent cells first, then a flatten,
-        // then the farther cells: in clustered frames nearly every farther
-        // pair is joined by then, which the recorded roots show at once.  A
-        // lane takes one core cell (wave-uniform loops).  The work list is
-        // free here and holds the queue of open cell pairs.
+        // (its smallest core index), and the graph is one of core cells.
+        // First its edges to adjacent cells, then connected components in
+        // synchronous rounds (hook every edge's two roots under the smaller,
+        // then every node jumps to its root) until a round hooks nothing;
+        // then the same for the farther cells, whose pairs mostly have equal
+        // roots by then and are skipped.  A lane takes one core cell in the
+        // edge passes (wave-uniform loops).  The work list is free here: it
+        // holds each core cell's edge bits, then the queue of open pairs.
         const int32_t ncl = s_ncells;
         const float inv_ncx = 1.0f / (float)g.ncx;
-        uint32_t *queue = reinterpret_cast<uint32_t *>(list);
-        const int qcap = cap / 2;
-        auto core_cell = [&](int32_t j, bool have) {
-            CoreCell A{};
-            if (have) {
-                A.ca = clist[j];
-                A.ay = div_small(A.ca, g.ncx, inv_ncx);
-                A.ax = A.ca - A.ay * g.ncx;
-                const uint32_t wa = cell[A.ca];
-                A.a0 = (int32_t)(wa & 0xffffu);
-                A.a1 = (int32_t)(cell[A.ca + 1] & 0xffffu);
-                A.node = (int32_t)(wa >> 16);
-                A.head = cell_head(pxy, score, A.a0, A.a1);
-            }
-            return A;
-        };
         const int nadj = s_nadj, nfwd = s_nfwd;
-        if (tid == 0) s_nq = 0;
-        __syncthreads();
-        for (int32_t j0 = tid - lane; j0 < ncl; j0 += kThreads) {
-            const bool have = j0 + lane < ncl;
-            union_heads<4, false>(have, core_cell(j0 + lane, have), cell, parent, pxy, score, g, r, s_fdx, s_fdy, 0,
-                                  nadj, queue, &s_nq, qcap);
+        // Edge bits (ncl entries; 4-byte aligned on the register stage, which
+        // sets bits with 32-bit atomics), then the 4-byte aligned queue in
+        // what is left of the list's cap entries (ncl <= cap: a core cell
+        // holds a core point).
+        const int shift0 = (int)((reinterpret_cast<uintptr_t>(list) >> 1) & 1u);
+        const bool regs = a.union_regs && ncl <= kRegCells * kThreads && shift0 + ncl + 1 <= cap;
+        uint16_t *emask = list + (regs ? shift0 : 0);
+        uint16_t *qbase = emask + ncl;
+        if (reinterpret_cast<uintptr_t>(qbase) & 2u) ++qbase;
+        uint32_t *queue = reinterpret_cast<uint32_t *>(qbase);
+        const int qcap = max((int)((list + cap - qbase) / 2), 0);
+        int round = 0;
+        if (tid == 0) s_hook[0] = 0;
+        if (regs) {
+            const UnionCtx u{cell, parent, pxy, score, clist, emask, queue, qcap, &s_nq, s_hook,
+                             s_fdx, s_fdy, g, r, ncl, inv_ncx};
+            union_regs(u, nadj, nfwd, round);
+        } else {
+            // more core cells than registers hold: the same stages with the
+            // edge bits re-read from LDS in every round, and queued pairs
+            // kept as (cell A | cell B << 16) and hooked from the queue
+            auto core_cell = [&](int32_t j, bool have) {
+                CoreCell A{};
+                if (have) {
+                    A.ca = clist[j];
+                    A.ay = div_small(A.ca, g.ncx, inv_ncx);
+                    A.ax = A.ca - A.ay * g.ncx;
+                    const uint32_t wa = cell[A.ca];
+                    A.a0 = (int32_t)(wa & 0xffffu);
+                    A.a1 = (int32_t)(cell[A.ca + 1] & 0xffffu);
+                    A.node = (int32_t)(wa >> 16);
+                    A.head = cell_head(pxy, score, A.a0, A.a1);
+                }
+                return A;
+            };
+            auto components = [&](int o0, int nq) {
+                const int last = round + ncl + 1;  // as in the register stage
+                for (;; ++round) {
+                    if (tid == 0) s_hook[(round + 1) % 3] = 0;
+                    bool any = false;
+                    for (int32_t j = tid; j < ncl; j += kThreads) {
+                        const uint32_t m = emask[j];
+                        if (!m) continue;
+                        const int32_t ca = clist[j];
+                        const int32_t ay = div_small(ca, g.ncx, inv_ncx), ax = ca - ay * g.ncx;
+                        int32_t nb[8];
+#pragma unroll
+                        for (int k = 0; k < 8; ++k)
+                            nb[k] = ((m >> k) & 1u)
+                                        ? (int32_t)cnode((ay + s_fdy[o0 + k]) * g.ncx + ax + s_fdx[o0 + k])
+                                        : 0;
+                        any |= hook_node<8>(parent, (int32_t)cnode(ca), nb, m);
+                    }
+                    for (int t = tid; t < nq; t += kThreads) {
+                        const uint32_t e = queue[t];
+                        if (e == kDeadPair) continue;
+                        const int32_t nb[1] = {(int32_t)cnode(e >> 16)};
+                        any |= hook_node<1>(parent, (int32_t)cnode(e & 0xffffu), nb, 1u);
+                    }
+                    if (any) s_hook[round % 3] = 1;
+                    __syncthreads();
+                    if (!s_hook[round % 3] || round >= last) break;  // every edge joins equal roots
+                    for (int32_t j = tid; j < ncl; j += kThreads) jump_node(parent, (int32_t)cnode(clist[j]));
+                    __syncthreads();
+                }
+                ++round;
+            };
+            if (tid == 0) s_nq = 0;
+            __syncthreads();
+            for (int32_t j0 = tid - lane; j0 < ncl; j0 += kThreads) {
+                const bool have = j0 + lane < ncl;
+                const uint32_t m = cell_edges<4, false>(have, core_cell(j0 + lane, have), cell, parent, pxy, score,
+                                                        g, r, s_fdx, s_fdy, 0, nadj, queue, &s_nq, qcap);
+                if (have) emask[j0 + lane] = (uint16_t)m;
+            }
+            __syncthreads();
+            int nq = min(s_nq, qcap);
+            resolve_queue(queue, nq, cell, pxy, score, r);
+            __syncthreads();
+            components(0, nq);
+            if (tid == 0) s_nq = 0;
+            __syncthreads();
+            for (int32_t j0 = tid - lane; j0 < ncl; j0 += kThreads) {
+                const bool have = j0 + lane < ncl;
+                const uint32_t m = cell_edges<8, true>(have, core_cell(j0 + lane, have), cell, parent, pxy, score,
+                                                       g, r, s_fdx, s_fdy, nadj, nfwd, queue, &s_nq, qcap);
+                if (have) emask[j0 + lane] = (uint16_t)m;
+            }
+            __syncthreads();
+            nq = min(s_nq, qcap);
+            resolve_queue(queue, nq, cell, pxy, score, r);
+            __syncthreads();
+            components(nadj, nq);
         }
-        __syncthreads();
-        union_queue(queue, min(s_nq, qcap), cell, parent, pxy, score, r);
-        __syncthreads();
-        for (int32_t j = tid; j < ncl; j += kThreads) {
-            const int32_t node = (int32_t)cnode(clist[j]);
-            st_rlx<kGroup>(parent + node, uf_root<kGroup>(parent, node));
-        }
-        if (tid == 0) s_nq = 0;
-        __syncthreads();
-        for (int32_t j0 = tid - lane; j0 < ncl; j0 += kThreads) {
-            const bool have = j0 + lane < ncl;
-            union_heads<8, true>(have, core_cell(j0 + lane, have), cell, parent, pxy, score, g, r, s_fdx, s_fdy, nadj,
-                                 nfwd, queue, &s_nq, qcap);
-        }
-        __syncthreads();
-        union_queue(queue, min(s_nq, qcap), cell, parent, pxy, score, r);
-        __syncthreads();
     } else {
         // coarsened grid: point-level unions (each pair once: the later point
         // of a cell, or the point in the earlier cell, does the work)

@@ -25,7 +25,7 @@ __device__ __forceinline__ void st_rlx(int32_t *p, int32_t v) {
 // Root of x with path halving.  Invariant kept by every writer:
 // parent[x] <= x, and parent[x] is an ancestor of x.
 template <int Scope>
-__device__ int32_t uf_find(int32_t *parent, int32_t x) {
+__device__ __forceinline__ int32_t uf_find(int32_t *parent, int32_t x) {
     for (;;) {
         int32_t p = ld_rlx<Scope>(parent + x);
         if (p == x) return x;
@@ -38,7 +38,7 @@ __device__ int32_t uf_find(int32_t *parent, int32_t x) {
 
 // Root of x without writes (safe while other threads set parent[i] = root).
 template <int Scope>
-__device__ int32_t uf_root(const int32_t *parent, int32_t x) {
+__device__ __forceinline__ int32_t uf_root(const int32_t *parent, int32_t x) {
     for (;;) {
         int32_t p = ld_rlx<Scope>(parent + x);
         if (p == x) return x;
@@ -48,7 +48,7 @@ __device__ int32_t uf_root(const int32_t *parent, int32_t x) {
 
 // Merge the trees of a and b, hooking the larger root under the smaller.
 template <int Scope>
-__device__ void uf_unite(int32_t *parent, int32_t a, int32_t b) {
+__device__ __forceinline__ void uf_unite(int32_t *parent, int32_t a, int32_t b) {
     for (;;) {
         a = uf_find<Scope>(parent, a);
         b = uf_find<Scope>(parent, b);

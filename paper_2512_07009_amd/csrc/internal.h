@@ -24,6 +24,8 @@ struct ClusterArgs {
     int32_t cap_cells;        // cell-table entries available on chip
     int32_t big_path;         // 1: frames above cap_points go to the multi-workgroup
                               // path; 0: the on-chip kernel clusters them in place
+    int32_t union_regs;       // 1: the on-chip unions keep up to 3072 core cells'
+                              // edges in registers; 0: always re-read them from LDS
     int32_t *labels;          // [total]
     uint8_t *kind;            // [total]
     int32_t *n_clusters;      // [n_frames] or nullptr

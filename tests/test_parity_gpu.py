@@ -135,6 +135,45 @@ def test_frame_above_lds_capacity_gpu():
     assert_cluster_equal(got, xy, off, 160, 5, tag="big frame")
 
 
+def _lattice_frame(seed, nx, ny, eps_q):
+    """One point per cell of side floor(E / sqrt 2) on an nx x ny lattice,
+    jittered inside its cell: every point is a core cell of its own."""
+    side = int(np.floor(np.sqrt(eps_q * eps_q / 2.0)))
+    while 2 * (side + 1) ** 2 <= eps_q * eps_q:
+        side += 1
+    rng = np.random.default_rng(seed)
+    gx, gy = np.meshgrid(np.arange(nx), np.arange(ny))
+    pts = np.stack([gx.ravel() * side, gy.ravel() * side], 1)
+    jit = rng.integers(0, max(side // 4, 1), pts.shape)
+    jit[0] = 0  # the bounding-box corner stays on a cell corner
+    return (pts + jit).astype(np.int32)
+
+
+def test_union_many_core_cells_gpu():
+    """A frame with more core cells than the register-held union stage takes
+    (one point per cell, 4500 cells) goes through the general stage."""
+    big = _lattice_frame(3, 75, 60, 640)
+    small = _lattice_frame(4, 20, 10, 640)
+    xy, off = wl.pack([small, big, small[:50]])
+    got = run_cluster(xy, off, 640, 4)
+    assert_cluster_equal(got, xy, off, 640, 4, tag="lattice")
+
+
+@pytest.mark.parametrize("eps_q,min_pts", [(640, 4), (960, 5), (400, 6)])
+def test_union_lds_stage_gpu(eps_q, min_pts, monkeypatch):
+    """FLOCK_CLUSTER_UNION=lds forces the general union stage for every frame."""
+    monkeypatch.setenv("FLOCK_CLUSTER_UNION", "lds")
+    for seed in range(2):
+        xy, off = wl.random_batch(31 * eps_q + seed, 24, 900)
+        got = run_cluster(xy, off, eps_q, min_pts)
+        assert_cluster_equal(got, xy, off, eps_q, min_pts, tag=f"seed {seed}")
+    xy, off, w = wl.generate("batch64x2000_1080p")
+    frames = [0, 1, 2, 3]
+    sxy, soff = sub_batch(xy, off, frames)
+    got = run_cluster(sxy, soff, w.eps_q, w.min_pts)
+    assert_cluster_equal(got, sxy, soff, w.eps_q, w.min_pts, tag="batch64x2000_1080p")
+
+
 @pytest.mark.parametrize("max_fp", [0, 20000])
 def test_large_frame_path_gpu(max_fp):
     """Frames above the on-chip capacity use the multi-workgroup path: dense
