@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -109,6 +110,39 @@ int32_t diagonal_cell_side(int32_t e) {
     return s < 1 ? 1 : (int32_t)s;
 }
 
+// The on-chip kernel's neighbour-cell tables for cells of side `side`
+// (offsets (dx, dy), |dx|, |dy| <= reach <= 2, whose cells can hold points
+// within e: gap(|dx|)^2 + gap(|dy|)^2 <= e^2, gap(d) = (d - 1) side + 1 for
+// d > 0).  Whole stencil by gap distance, ties in row-major order; forward
+// half (dy > 0, or dy = 0 and dx > 0) with the adjacent cells first.
+void pack_stencil(int32_t e, int32_t side, flock::ClusterArgs *a) {
+    const int reach = e == 0 ? 0 : std::min(1 + (e - 1) / side, 7);
+    auto gap = [side](int d) -> int64_t { d = d < 0 ? -d : d; return d == 0 ? 0 : (int64_t)(d - 1) * side + 1; };
+    struct Off { int dx, dy; int64_t key; int idx; };
+    std::vector<Off> all, adj, far;
+    int rowcnt[3] = {0, 0, 0};
+    for (int idx = 0; idx < 25; ++idx) {
+        const int dx = idx % 5 - 2, dy = idx / 5 - 2;
+        if (std::abs(dx) > reach || std::abs(dy) > reach) continue;
+        const int64_t d = gap(dx) * gap(dx) + gap(dy) * gap(dy);
+        if (d > (int64_t)e * e) continue;
+        all.push_back({dx, dy, d, idx});
+        if (dy >= 0) rowcnt[dy]++;
+        if (dy > 0 || (dy == 0 && dx > 0)) (std::abs(dx) <= 1 && std::abs(dy) <= 1 ? adj : far).push_back({dx, dy, d, idx});
+    }
+    std::stable_sort(all.begin(), all.end(), [](const Off &x, const Off &y) { return x.key < y.key; });
+    auto code = [](const Off &o) { return (uint32_t)((o.dx + 2) | ((o.dy + 2) << 3)); };
+    for (uint32_t &w : a->sten_all) w = 0;
+    for (uint32_t &w : a->sten_fwd) w = 0;
+    for (size_t i = 0; i < all.size(); ++i) a->sten_all[i / 5] |= code(all[i]) << (6 * (i % 5));
+    std::vector<Off> fwd = adj;
+    fwd.insert(fwd.end(), far.begin(), far.end());
+    for (size_t i = 0; i < fwd.size(); ++i) a->sten_fwd[i / 5] |= code(fwd[i]) << (6 * (i % 5));
+    uint32_t meta = (uint32_t)all.size() | ((uint32_t)adj.size() << 8) | ((uint32_t)fwd.size() << 16);
+    for (int k = 0; k < 3; ++k) meta |= (uint32_t)(rowcnt[k] > 0 ? (rowcnt[k] - 1) / 2 : 0) << (24 + 2 * k);
+    a->sten_meta = meta;
+}
+
 struct ClusterPlan {
     int32_t cap_points;
     int32_t cap_cells;
@@ -201,6 +235,7 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     a.eps_q = eps_q;
     a.min_pts = min_pts;
     a.cell_side = diagonal_cell_side(eps_q);
+    pack_stencil(eps_q, a.cell_side, &a);
     a.cap_points = plan.cap_points;
     a.cap_cells = plan.cap_cells;
     a.labels = labels;

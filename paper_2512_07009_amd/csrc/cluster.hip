@@ -901,10 +901,32 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         g.dxmax = s_dxmax;
     }
 
-    // 3. counting sort by cell (wave 0 also builds the stencil tables)
+    // 3. counting sort by cell (the stencil tables come from the host for
+    //    cells of side cell_side; wave 0 builds them for a coarsened grid)
     for (int32_t c = tid; c <= g.ncell; c += kThreads) cell[c] = 0;
-    if (tid < 64)
+    if (g.dense_ok) {
+        if (tid < kMaxStencil) {
+            const uint32_t w = tid < 5 ? a.sten_all[0] : tid < 10 ? a.sten_all[1] : tid < 15 ? a.sten_all[2]
+                             : tid < 20 ? a.sten_all[3] : a.sten_all[4];
+            const uint32_t c6 = (w >> (6 * (tid % 5))) & 63u;
+            s_sdx[tid] = (int)(c6 & 7u) - 2;
+            s_sdy[tid] = (int)(c6 >> 3) - 2;
+        } else if (tid >= 32 && tid < 32 + kMaxOffsets) {
+            const int t = tid - 32;  // at most 12 forward offsets: entries 15 and up stay 0
+            const uint32_t w = t < 5 ? a.sten_fwd[0] : t < 10 ? a.sten_fwd[1] : t < 15 ? a.sten_fwd[2] : 0x12u;
+            const uint32_t c6 = (w >> (6 * (t % 5))) & 63u;
+            s_fdx[t] = (int)(c6 & 7u) - 2;
+            s_fdy[t] = (int)(c6 >> 3) - 2;
+        } else if (tid == 64) {
+            s_nsten = (int)(a.sten_meta & 0xffu);
+            s_nadj = (int)((a.sten_meta >> 8) & 0xffu);
+            s_nfwd = (int)((a.sten_meta >> 16) & 0xffu);
+#pragma unroll
+            for (int k = 0; k < 3; ++k) s_dxmax[k] = (int)((a.sten_meta >> (24 + 2 * k)) & 3u);
+        }
+    } else if (tid < 64) {
         build_stencil(g.reach, g.side, r, lane, s_dxmax, s_sdx, s_sdy, &s_nsten, s_fdx, s_fdy, &s_nadj, &s_nfwd);
+    }
     __syncthreads();
     uint32_t pv[kPtsPerThread];
     uint16_t prank[kPtsPerThread];
@@ -957,24 +979,33 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     }
     __syncthreads();
     // 4b. count the listed points' neighbours, nearest rows first, stopping
-    //     at min_pts
+    //     at min_pts; the bounds of all 2 reach + 1 <= 5 row spans are
+    //     loaded before the first scan
     {
         const int32_t nl = s_nlist;
+        const int dxm0 = g.dxmax[0], dxm1 = g.reach >= 1 ? g.dxmax[1] : 0, dxm2 = g.reach >= 2 ? g.dxmax[2] : 0;
         for (int32_t j = tid; j < nl; j += kThreads) {
             const int32_t p = list[j];
             const uint32_t v = pxy[p];
             int32_t cx, cy;
             cell_id(v, g, &cx, &cy);
-            int32_t cnt = 0;
-            for (int k = 0; k <= 2 * g.reach && cnt < a.min_pts; ++k) {
-                const int dy = (k & 1) ? -((k + 1) >> 1) : (k >> 1);  // 0, -1, 1, -2, 2, ...
+            int32_t q0[5], q1[5];
+#pragma unroll
+            for (int k = 0; k < 5; ++k) {
+                const int dy = (k & 1) ? -((k + 1) >> 1) : (k >> 1);  // 0, -1, 1, -2, 2
+                const int ady = dy < 0 ? -dy : dy;
+                const int dxm = ady == 0 ? dxm0 : ady == 1 ? dxm1 : dxm2;
                 const int32_t ry = cy + dy;
-                if (ry < 0 || ry >= g.ncy) continue;
-                const int dxm = g.dxmax[dy < 0 ? -dy : dy];
-                const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
-                cnt += count_span(pxy, cstart(ry * g.ncx + rx0), cstart(ry * g.ncx + rx1 + 1), v, r,
-                                  a.min_pts - cnt);
+                const bool ok = (k <= 2 * g.reach) & (ry >= 0) & (ry < g.ncy);
+                const int32_t row = min(max(ry, 0), g.ncy - 1) * g.ncx;
+                q0[k] = cstart(row + max(cx - dxm, 0));
+                const int32_t e = cstart(row + min(cx + dxm, g.ncx - 1) + 1);
+                q1[k] = ok ? e : q0[k];
             }
+            int32_t cnt = 0;
+#pragma unroll
+            for (int k = 0; k < 5; ++k)
+                if (cnt < a.min_pts) cnt += count_span(pxy, q0[k], q1[k], v, r, a.min_pts - cnt);
             if (cnt >= a.min_pts) score[p] = 1;
         }
     }

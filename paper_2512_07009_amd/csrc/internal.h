@@ -26,6 +26,12 @@ struct ClusterArgs {
                               // path; 0: the on-chip kernel clusters them in place
     int32_t union_regs;       // 1: the on-chip unions keep up to 3072 core cells'
                               // edges in registers; 0: always re-read them from LDS
+    // Neighbour-cell tables for cells of side cell_side (as the on-chip
+    // kernel's build_stencil makes them), packed 6 bits per cell offset
+    // ((dx + 2) | (dy + 2) << 3), five per word:
+    uint32_t sten_all[5];     // the whole stencil, nearest cells first
+    uint32_t sten_fwd[3];     // its forward half, adjacent cells first
+    uint32_t sten_meta;       // nsten | nadj << 8 | nfwd << 16 | dxmax[k] << (24 + 2 k)
     int32_t *labels;          // [total]
     uint8_t *kind;            // [total]
     int32_t *n_clusters;      // [n_frames] or nullptr
