@@ -7,8 +7,10 @@ The arithmetic lives in ``oracle.c`` (plain C, fp64 for the density, int64 for
 distances); this module only compiles it with gcc and marshals numpy arrays.
 The definitions it follows are stated at the top of ``oracle.c``:
 standard DBSCAN (Ester et al., 1996) as the point-level reading of the
-paper's connected-component clustering (Section 2.3), and the direct-sum
-Gaussian density grid of Algorithm 1 (Section 3.6).
+paper's connected-component clustering (Section 2.3), the direct-sum
+Gaussian density grid of Algorithm 1 (Section 3.6), and the heatmap
+analytics of Section 2.3 and Algorithm 1 (threshold, connected components of
+grid cells, entropy, clustering degree).
 """
 
 from __future__ import annotations
@@ -62,6 +64,9 @@ def _load():
         lib.oracle_density_cells.argtypes = [p, p, i32, i32, i32, i32, i32, ctypes.c_double,
                                              p, p, p, ctypes.c_int64, p, i32]
         lib.oracle_density_cells.restype = i32
+        lib.oracle_heatmap_frames.argtypes = [p, i32, i32, i32, ctypes.c_double, ctypes.c_float, i32,
+                                              p, p, p, p, p, p, i32]
+        lib.oracle_heatmap_frames.restype = i32
         _lib = lib
     return _lib
 
@@ -157,3 +162,31 @@ def density_cells(xy, offsets, width_px: int, height_px: int, grid_w: int, grid_
                                      n_threads or default_threads())
     _check(r, "density_cells")
     return out
+
+
+def heatmap_frames(density, cell_area: float, threshold: float, connectivity: int = 8,
+                   n_threads: int | None = None):
+    """Heatmap analytics of float32 density grids [F, grid_h, grid_w].
+
+    Returns a dict: labels int32[F, h, w] (smallest cell index of the
+    component, -1 cold), n_components int32[F], entropy float64[F],
+    degree float64[F], comp_cells int32[F, h, w] and comp_mass float64[F, h, w]
+    (at label cells, 0 elsewhere).
+    """
+    d = np.ascontiguousarray(np.asarray(density, dtype=np.float32))
+    if d.ndim != 3:
+        raise ValueError("density must be [F, grid_h, grid_w]")
+    F, gh, gw = d.shape
+    labels = np.zeros(d.shape, np.int32)
+    comp_cells = np.zeros(d.shape, np.int32)
+    comp_mass = np.zeros(d.shape, np.float64)
+    ncomp = np.zeros(F, np.int32)
+    ent = np.zeros(F, np.float64)
+    deg = np.zeros(F, np.float64)
+    r = _load().oracle_heatmap_frames(_ptr(d), F, gw, gh, float(cell_area), float(threshold),
+                                      int(connectivity), _ptr(labels), _ptr(ncomp), _ptr(ent),
+                                      _ptr(deg), _ptr(comp_cells), _ptr(comp_mass),
+                                      n_threads or default_threads())
+    _check(r, "heatmap_frames")
+    return {"labels": labels, "n_components": ncomp, "entropy": ent, "degree": deg,
+            "comp_cells": comp_cells, "comp_mass": comp_mass}

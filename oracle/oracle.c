@@ -39,8 +39,31 @@
  *     This is the direct double sum in fp64 with libm exp, one grid cell at a
  *     time; it makes no use of the sum's separability.
  *
- * Threads only split independent work items (whole frames for clustering,
- * whole grid rows for density); each item is computed exactly as above.
+ *  3. Heatmap analytics of each frame's density grid (the clustering module
+ *     of Section 2.3 thresholds the density heatmaps and applies connected
+ *     component analysis; Algorithm 1 then computes the heatmap, its entropy
+ *     and a clustering degree).  Readings, since the paper fixes none of the
+ *     details:
+ *       - the heatmap is the density grid D itself, normalised to
+ *         p = D / S with S = sum of the positive cells (cells with D <= 0
+ *         carry no mass);
+ *       - a cell is hot when D >= threshold (threshold > 0, in birds/px^2);
+ *       - clusters are the connected components of the hot cells under
+ *         4-neighbourhood (shared edge) or 8-neighbourhood (shared edge or
+ *         corner), found by breadth-first expansion from each unvisited hot
+ *         cell in ascending row-major index, so a component's label is its
+ *         smallest frame-local index gy * grid_w + gx; cold cells get -1;
+ *       - per component: its cell count and its mass, cell_area times the sum
+ *         of D over its cells (expected birds), stored at the label cell;
+ *       - entropy H = -sum over positive cells of p ln p (natural log), 0 for
+ *         a frame with S = 0;
+ *       - clustering degree = (sum of D over hot cells) / S, the share of the
+ *         frame's density mass that lies in clusters (0 when S = 0).
+ *     All sums are fp64 in row-major order.
+ *
+ * Threads only split independent work items (whole frames for clustering
+ * and heatmaps, whole grid rows for density); each item is computed exactly
+ * as above.
  */
 
 #include <math.h>
@@ -341,4 +364,139 @@ int32_t oracle_density_cells(const int32_t *xy, const int32_t *offsets, int32_t 
     job.n_items = m;
     job.mode = 2;
     return run_job(&job, n_threads);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Heatmap analytics of one frame                                           */
+/* ------------------------------------------------------------------------ */
+
+/* density: [grid_h][grid_w] fp32; labels, comp_cells: [grid_h][grid_w];
+ * comp_mass: [grid_h][grid_w] fp64; returns the number of components. */
+int32_t oracle_heatmap_frame(const float *density, int32_t grid_w, int32_t grid_h, double cell_area,
+                             float threshold, int32_t connectivity, int32_t *labels,
+                             int32_t *comp_cells, double *comp_mass, double *entropy,
+                             double *degree)
+{
+    if (grid_w < 1 || grid_h < 1 || !(threshold > 0.0f) || (connectivity != 4 && connectivity != 8))
+        return ORACLE_EINVAL;
+    const int64_t cells = (int64_t)grid_w * grid_h;
+    int64_t *queue = (int64_t *)malloc((size_t)cells * sizeof(int64_t));
+    if (!queue) return ORACLE_ENOMEM;
+    for (int64_t c = 0; c < cells; ++c) {
+        labels[c] = -1;
+        comp_cells[c] = 0;
+        comp_mass[c] = 0.0;
+    }
+    int32_t n_comp = 0;
+    for (int64_t seed = 0; seed < cells; ++seed) {
+        if (!(density[seed] >= threshold) || labels[seed] >= 0) continue;
+        /* breadth-first expansion over hot neighbours */
+        int64_t head = 0, tail = 0;
+        queue[tail++] = seed;
+        labels[seed] = (int32_t)seed;
+        while (head < tail) {
+            const int64_t c = queue[head++];
+            const int32_t gx = (int32_t)(c % grid_w), gy = (int32_t)(c / grid_w);
+            for (int32_t dy = -1; dy <= 1; ++dy)
+                for (int32_t dx = -1; dx <= 1; ++dx) {
+                    if (dx == 0 && dy == 0) continue;
+                    if (connectivity == 4 && dx != 0 && dy != 0) continue;
+                    const int32_t nx = gx + dx, ny = gy + dy;
+                    if (nx < 0 || nx >= grid_w || ny < 0 || ny >= grid_h) continue;
+                    const int64_t nc = (int64_t)ny * grid_w + nx;
+                    if (density[nc] >= threshold && labels[nc] < 0) {
+                        labels[nc] = (int32_t)seed;
+                        queue[tail++] = nc;
+                    }
+                }
+        }
+        ++n_comp;
+    }
+    free(queue);
+    /* per-component cells and mass, at the label cell */
+    for (int64_t c = 0; c < cells; ++c) {
+        if (labels[c] < 0) continue;
+        comp_cells[labels[c]] += 1;
+        comp_mass[labels[c]] += (double)density[c];
+    }
+    for (int64_t c = 0; c < cells; ++c) comp_mass[c] *= cell_area;
+    /* entropy of p = D / S and the hot share of S */
+    double S = 0.0, hot = 0.0;
+    for (int64_t c = 0; c < cells; ++c) {
+        if (density[c] > 0.0f) S += (double)density[c];
+        if (labels[c] >= 0) hot += (double)density[c];
+    }
+    double H = 0.0;
+    if (S > 0.0) {
+        for (int64_t c = 0; c < cells; ++c) {
+            if (!(density[c] > 0.0f)) continue;
+            const double pc = (double)density[c] / S;
+            H -= pc * log(pc);
+        }
+    }
+    *entropy = H;
+    *degree = S > 0.0 ? hot / S : 0.0;
+    return n_comp;
+}
+
+/* Batch of n_frames grids, frames split over threads. */
+typedef struct {
+    const float *density;
+    int32_t n_frames, grid_w, grid_h, connectivity;
+    double cell_area;
+    float threshold;
+    int32_t *labels, *n_components, *comp_cells;
+    double *comp_mass, *entropy, *degree;
+    int32_t next, rc;
+    pthread_mutex_t mu;
+} heat_job_t;
+
+static void *heat_worker(void *arg)
+{
+    heat_job_t *job = (heat_job_t *)arg;
+    const int64_t cells = (int64_t)job->grid_w * job->grid_h;
+    for (;;) {
+        pthread_mutex_lock(&job->mu);
+        const int32_t f = job->next++;
+        pthread_mutex_unlock(&job->mu);
+        if (f >= job->n_frames) break;
+        const int32_t r = oracle_heatmap_frame(job->density + f * cells, job->grid_w, job->grid_h,
+                                               job->cell_area, job->threshold, job->connectivity,
+                                               job->labels + f * cells, job->comp_cells + f * cells,
+                                               job->comp_mass + f * cells, job->entropy + f,
+                                               job->degree + f);
+        pthread_mutex_lock(&job->mu);
+        if (r < 0) job->rc = r;
+        else job->n_components[f] = r;
+        pthread_mutex_unlock(&job->mu);
+    }
+    return NULL;
+}
+
+int32_t oracle_heatmap_frames(const float *density, int32_t n_frames, int32_t grid_w, int32_t grid_h,
+                              double cell_area, float threshold, int32_t connectivity,
+                              int32_t *labels, int32_t *n_components, double *entropy,
+                              double *degree, int32_t *comp_cells, double *comp_mass,
+                              int32_t n_threads)
+{
+    if (n_frames < 0 || grid_w < 1 || grid_h < 1 || !(threshold > 0.0f) ||
+        (connectivity != 4 && connectivity != 8))
+        return ORACLE_EINVAL;
+    heat_job_t job;
+    memset(&job, 0, sizeof job);
+    job.density = density; job.n_frames = n_frames; job.grid_w = grid_w; job.grid_h = grid_h;
+    job.connectivity = connectivity; job.cell_area = cell_area; job.threshold = threshold;
+    job.labels = labels; job.n_components = n_components; job.comp_cells = comp_cells;
+    job.comp_mass = comp_mass; job.entropy = entropy; job.degree = degree;
+    pthread_mutex_init(&job.mu, NULL);
+    if (n_threads < 1) n_threads = 1;
+    if (n_threads > 64) n_threads = 64;
+    pthread_t th[64];
+    int32_t started = 0;
+    for (int32_t t = 0; t < n_threads; ++t)
+        if (pthread_create(&th[t], NULL, heat_worker, &job) == 0) ++started;
+    if (started == 0) heat_worker(&job);
+    for (int32_t t = 0; t < started; ++t) pthread_join(th[t], NULL);
+    pthread_mutex_destroy(&job.mu);
+    return job.rc;
 }

@@ -16,6 +16,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "oracle.c")
 DBSCAN_PINS = "tests/test_oracle_dbscan.py"
 KDE_PINS = "tests/test_oracle_kde.py"
+HEAT_PINS = "tests/test_oracle_heatmap.py"
 
 MUTANTS = [
     # (name, old text, new text, which pin file must fail)
@@ -53,6 +54,21 @@ MUTANTS = [
      "const double cy = ((double)gy + 0.5) * (double)width_px", KDE_PINS),
     ("kde_row_layout", "double *row = job->density + ((int64_t)f * job->grid_h + gy) * job->grid_w;",
      "double *row = job->density + ((int64_t)f * job->grid_w + gy) * job->grid_h;", KDE_PINS),
+    ("heat_strict_threshold", "if (!(density[seed] >= threshold) || labels[seed] >= 0) continue;",
+     "if (!(density[seed] > threshold) || labels[seed] >= 0) continue;", HEAT_PINS),
+    ("heat_4_as_8", "if (connectivity == 4 && dx != 0 && dy != 0) continue;", "", HEAT_PINS),
+    ("heat_seeds_descending", "for (int64_t seed = 0; seed < cells; ++seed) {",
+     "for (int64_t seed = cells - 1; seed >= 0; --seed) {", HEAT_PINS),
+    ("heat_entropy_log2", "H -= pc * log(pc);", "H -= pc * log2(pc);", HEAT_PINS),
+    ("heat_entropy_unnormalised", "const double pc = (double)density[c] / S;",
+     "const double pc = (double)density[c];", HEAT_PINS),
+    ("heat_degree_counts", "if (labels[c] >= 0) hot += (double)density[c];",
+     "if (labels[c] >= 0) hot += 1.0;", HEAT_PINS),
+    ("heat_degree_not_normalised", "*degree = S > 0.0 ? hot / S : 0.0;", "*degree = S > 0.0 ? hot : 0.0;",
+     HEAT_PINS),
+    ("heat_mass_no_area", "for (int64_t c = 0; c < cells; ++c) comp_mass[c] *= cell_area;", "", HEAT_PINS),
+    ("heat_mass_at_cell", "comp_mass[labels[c]] += (double)density[c];", "comp_mass[c] += (double)density[c];",
+     HEAT_PINS),
 ]
 
 
