@@ -47,6 +47,7 @@ MFMA_F16_PEAK_TFLOPS = 2500.0
 KERNEL_SOURCES = {
     "cluster": "paper_2512_07009_amd/csrc/cluster.hip",
     "density": "paper_2512_07009_amd/csrc/density.hip",
+    "heatmap": "paper_2512_07009_amd/csrc/heatmap.hip",
 }
 
 
@@ -244,6 +245,28 @@ def main():
     ms_per_step = wall / K * 1e3
     value = F / (wall / K)
 
+    # 3. heatmap analytics of the step's density grids (its own entry point,
+    #    not part of `value`): hot cells at twice the frame-average density
+    cells = w.grid_w * w.grid_h
+    area = (w.width_px / w.grid_w) * (w.height_px / w.grid_h)
+    heat_thr = 2.0 * T / (F * w.width_px * w.height_px)
+    hout = {"labels": torch.empty((F, w.grid_h, w.grid_w), dtype=torch.int32, device=dev),
+            "n_components": torch.empty(F, dtype=torch.int32, device=dev),
+            "entropy": torch.empty(F, dtype=torch.float64, device=dev),
+            "degree": torch.empty(F, dtype=torch.float64, device=dev),
+            "comp_cells": torch.empty((F, w.grid_h, w.grid_w), dtype=torch.int32, device=dev),
+            "comp_mass": torch.empty((F, w.grid_h, w.grid_w), dtype=torch.float64, device=dev)}
+    for _ in range(3):
+        flock.heatmap_frames(dens, area, heat_thr, 8, out=hout, stream=stream)
+    hev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize(dev)
+    hev[0].record(stream)
+    for _ in range(K):
+        flock.heatmap_frames(dens, area, heat_thr, 8, out=hout, stream=stream)
+    hev[1].record(stream)
+    torch.cuda.synchronize(dev)
+    t_heat = hev[0].elapsed_time(hev[1]) / K * 1e-3
+
     # algorithmic work per launch
     cluster_bytes = 13 * T + 8 * F + 4          # xy 8 + labels 4 + kind 1 per bird; offsets, n_clusters
     density_flops = 2.0 * w.grid_w * w.grid_h * T
@@ -255,6 +278,12 @@ def main():
           "unit": "TFLOP/s", "per_launch_us": t_density * 1e6, "algorithmic_flops": density_flops}
     de["frac"] = de["achieved"] / de["peak"]
     de["traffic"] = committed_traffic("density", w.name)
+    heat_bytes = 20 * F * cells + 20 * F  # density 4 + labels 4 + cells 4 + mass 8 per cell; 20 B per frame
+    he = {"bound": "hbm", "achieved": heat_bytes / t_heat / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+          "per_launch_us": t_heat * 1e6, "algorithmic_bytes": heat_bytes,
+          "threshold": heat_thr, "connectivity": 8, "in_value": False}
+    he["frac"] = he["achieved"] / he["peak"]
+    he["traffic"] = committed_traffic("heatmap", w.name)
     dominant = ("cluster_frames", cl) if t_cluster >= t_density else ("density_frames", de)
     roof = {k: dominant[1][k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")}
     roof["kernel"] = dominant[0]
@@ -284,7 +313,7 @@ def main():
         "timing": graph_note or ("value: HIP graph replay of the faster of the two-stream and one-stream steps; "
                                  "kernel durations: HIP events in the eager run of the same mode"),
         "roofline": roof,
-        "kernels": {"cluster_frames": cl, "density_frames": de},
+        "kernels": {"cluster_frames": cl, "density_frames": de, "heatmap_frames": he},
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")

@@ -140,6 +140,55 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
  * four arguments, whatever the frame extent and sigma. */
 size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h);
 
+/*
+ * heatmap_frames - heatmap analytics of every frame's density grid.
+ *
+ * The clustering module of Section 2.3 thresholds the density heatmaps and
+ * applies connected component analysis; Algorithm 1 computes the heatmap,
+ * its entropy and a clustering degree per frame.  The paper fixes none of
+ * the details; this entry point computes, per frame f and cell
+ * c = gy * grid_w + gx:
+ *   hot          density[f][c] >= threshold;
+ *   labels       connected hot cells under the 4-neighbourhood (shared edge)
+ *                or the 8-neighbourhood (shared edge or corner) form a
+ *                component, labelled by its smallest cell index; cold cells
+ *                get -1;
+ *   comp_cells, comp_mass   at each component's label cell, its number of
+ *                cells and cell_area_px2 * (sum of its density) (expected
+ *                birds); 0 at every other cell;
+ *   n_components number of components;
+ *   entropy      -sum p ln p over the cells with density > 0,
+ *                p = density / S, S the sum of those cells (0 if S = 0);
+ *   degree       (sum of density over hot cells) / S (0 if S = 0): the share
+ *                of the frame's density mass that lies in components.
+ *
+ * Arguments:
+ *   density          device in, float[n_frames][grid_h][grid_w], finite and
+ *                    >= 0 (the output of density_frames).
+ *   grid_w, grid_h   1 .. 4096 each.
+ *   cell_area_px2    area of one cell in px^2 (W H / (grid_w grid_h)), >= 0.
+ *   threshold        birds / px^2, finite and > 0.
+ *   connectivity     4 or 8.
+ *   labels, comp_cells   device out, int32[n_frames][grid_h][grid_w].
+ *   comp_mass        device out, double[n_frames][grid_h][grid_w], 8-byte
+ *                    aligned.
+ *   n_components     device out, int32[n_frames].
+ *   entropy, degree  device out, double[n_frames].
+ *   workspace        as for cluster_frames, sized by heatmap_frames_workspace.
+ * Every output is deterministic: sums are taken in a fixed order, and the
+ * component masses are summed as 64-bit integers of a per-frame fixed-point
+ * scale (each cell rounded to within 2^(lg - 62) of the frame's largest cell,
+ * lg = ceil(log2(grid_w grid_h))).
+ */
+flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid_w, int32_t grid_h,
+                            double cell_area_px2, float threshold, int32_t connectivity,
+                            int32_t *labels, int32_t *n_components, double *entropy, double *degree,
+                            int32_t *comp_cells, double *comp_mass, void *workspace,
+                            size_t workspace_bytes, void *stream);
+
+/* Bytes of workspace heatmap_frames needs for this batch shape. */
+size_t heatmap_frames_workspace(int32_t n_frames, int32_t grid_w, int32_t grid_h);
+
 /* Text of the last error on this thread ("" if none); valid until the next
  * library call on this thread. */
 const char *flock_last_error(void);

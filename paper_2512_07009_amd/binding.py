@@ -50,6 +50,11 @@ def lib() -> ctypes.CDLL:
         L.cluster_frames_workspace.restype = sz
         L.density_frames_workspace.argtypes = [i32, i32, i32, i32]
         L.density_frames_workspace.restype = sz
+        L.heatmap_frames.argtypes = [p, i32, i32, i32, ctypes.c_double, ctypes.c_float, i32,
+                                     p, p, p, p, p, p, p, sz, p]
+        L.heatmap_frames.restype = i32
+        L.heatmap_frames_workspace.argtypes = [i32, i32, i32]
+        L.heatmap_frames_workspace.restype = sz
         L.flock_last_error.argtypes = []
         L.flock_last_error.restype = ctypes.c_char_p
         L.flock_version.argtypes = []
@@ -153,6 +158,39 @@ def density_frames(xy: torch.Tensor, offsets: torch.Tensor, width_px: int, heigh
                                   ws_bytes, _stream(stream))
     _check(st)
     return dens
+
+
+def heatmap_frames(density: torch.Tensor, cell_area_px2: float, threshold: float, connectivity: int = 8,
+                   out=None, stream=None):
+    """Heatmap analytics of float32 density grids [F, grid_h, grid_w] on the device.
+
+    Returns a dict of device tensors: labels int32[F, h, w] (smallest cell
+    index of the component, -1 for cold cells), n_components int32[F],
+    entropy float64[F], degree float64[F], comp_cells int32[F, h, w] and
+    comp_mass float64[F, h, w] (at label cells, 0 elsewhere).
+    out: optional dict of such tensors to write into.
+    """
+    if not density.is_cuda or density.dtype != torch.float32 or density.dim() != 3 \
+            or not density.is_contiguous():
+        raise ValueError("density must be a contiguous float32 device tensor [F, grid_h, grid_w]")
+    F, gh, gw = density.shape
+    dev = density.device
+    if out is None:
+        out = {"labels": torch.empty((F, gh, gw), dtype=torch.int32, device=dev),
+               "n_components": torch.empty(F, dtype=torch.int32, device=dev),
+               "entropy": torch.empty(F, dtype=torch.float64, device=dev),
+               "degree": torch.empty(F, dtype=torch.float64, device=dev),
+               "comp_cells": torch.empty((F, gh, gw), dtype=torch.int32, device=dev),
+               "comp_mass": torch.empty((F, gh, gw), dtype=torch.float64, device=dev)}
+    ws_bytes = lib().heatmap_frames_workspace(F, gw, gh)
+    ws = _workspace(ws_bytes, dev, stream)
+    with torch.cuda.device(dev):
+        st = lib().heatmap_frames(_ptr(density), F, gw, gh, float(cell_area_px2), float(threshold),
+                                  int(connectivity), _ptr(out["labels"]), _ptr(out["n_components"]),
+                                  _ptr(out["entropy"]), _ptr(out["degree"]), _ptr(out["comp_cells"]),
+                                  _ptr(out["comp_mass"]), _ptr(ws), ws_bytes, _stream(stream))
+    _check(st)
+    return out
 
 
 def version() -> str:

@@ -332,4 +332,73 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     return FLOCK_OK;
 }
 
+size_t heatmap_frames_workspace(int32_t n_frames, int32_t grid_w, int32_t grid_h) {
+    g_error.clear();
+    return flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h);
+}
+
+flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid_w, int32_t grid_h,
+                            double cell_area_px2, float threshold, int32_t connectivity, int32_t *labels,
+                            int32_t *n_components, double *entropy, double *degree, int32_t *comp_cells,
+                            double *comp_mass, void *workspace, size_t workspace_bytes, void *stream) {
+    g_error.clear();
+    if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
+    if (grid_w < 1 || grid_h < 1 || grid_w > 4096 || grid_h > 4096)
+        return fail(FLOCK_EINVAL, "grid %d x %d outside 1..4096", grid_w, grid_h);
+    if (!std::isfinite(cell_area_px2) || cell_area_px2 < 0.0)
+        return fail(FLOCK_EINVAL, "cell_area_px2 must be finite and >= 0");
+    if (!std::isfinite(threshold) || !(threshold > 0.0f))
+        return fail(FLOCK_EINVAL, "threshold must be finite and > 0");
+    if (connectivity != 4 && connectivity != 8)
+        return fail(FLOCK_EINVAL, "connectivity = %d, expected 4 or 8", connectivity);
+    if (n_frames == 0) return FLOCK_OK;
+    if (!density || !labels || !n_components || !entropy || !degree || !comp_cells || !comp_mass)
+        return fail(FLOCK_EINVAL, "density and every output must be non-NULL");
+    if (!aligned(density, 4) || !aligned(labels, 4) || !aligned(n_components, 4) || !aligned(comp_cells, 4))
+        return fail(FLOCK_EINVAL, "density, labels, n_components and comp_cells must be 4-byte aligned");
+    if (!aligned(entropy, 8) || !aligned(degree, 8) || !aligned(comp_mass, 8))
+        return fail(FLOCK_EINVAL, "entropy, degree and comp_mass must be 8-byte aligned");
+    const long long tiles = (long long)((grid_w + 31) / 32) * ((grid_h + 31) / 32) * n_frames;
+    const long long cells = (long long)grid_w * grid_h * n_frames;
+    if (tiles > 0x7fffffffLL || (cells + 255) / 256 > 0x7fffffffLL)
+        return fail(FLOCK_EUNSUPPORTED, "batch too large for one launch");
+
+    const DeviceInfo *dev = nullptr;
+    flock_status st = device_info(&dev);
+    if (st != FLOCK_OK) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const size_t need = flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h);
+    if (workspace && workspace_bytes < need)
+        return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
+    if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
+    void *ws = workspace;
+    hipError_t err = hipSuccess;
+    if (!ws) {
+        err = hipMallocAsync(&ws, need, s);
+        if (err != hipSuccess) return hip_fail(err, "workspace allocation");
+    }
+    flock::HeatArgs a;
+    a.density = density;
+    a.n_frames = n_frames;
+    a.grid_w = grid_w;
+    a.grid_h = grid_h;
+    a.tiles_x = a.tiles_y = 0;
+    a.cell_area = cell_area_px2;
+    a.threshold = threshold;
+    a.connectivity = connectivity;
+    a.labels = labels;
+    a.n_components = n_components;
+    a.entropy = entropy;
+    a.degree = degree;
+    a.comp_cells = comp_cells;
+    a.comp_mass = comp_mass;
+    err = flock::launch_heatmap(a, ws, s);
+    if (!workspace) {
+        const hipError_t ferr = hipFreeAsync(ws, s);
+        if (err == hipSuccess) err = ferr;
+    }
+    if (err != hipSuccess) return hip_fail(err, "heatmap kernels");
+    return FLOCK_OK;
+}
+
 }  // extern "C"

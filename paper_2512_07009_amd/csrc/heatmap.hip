@@ -1,0 +1,350 @@
+// heatmap.hip - heatmap analytics of density grids on gfx950.
+//
+// What is computed (the clustering module of Section 2.3 thresholds the
+// density heatmaps and applies connected component analysis; Algorithm 1
+// computes the heatmap, its entropy and a clustering degree per frame):
+//   hot cell     density >= threshold;
+//   component    connected hot cells under the 4-neighbourhood (shared edge)
+//                or the 8-neighbourhood (shared edge or corner), labelled by
+//                its smallest row-major cell index gy * grid_w + gx; cold
+//                cells get -1;
+//   per component  cells and mass = cell_area * sum of density, stored at
+//                the label cell (0 elsewhere);
+//   entropy      -sum p ln p over positive cells, p = density / S, S the sum
+//                of the positive cells (0 when S = 0);
+//   degree       (sum of density over hot cells) / S (0 when S = 0).
+//
+// Design (HBM-bound: a few bytes per cell):
+//   1. heat_tile_kernel, one 256-thread workgroup per 32 x 32 tile: loads the
+//      tile once, unites hot neighbours inside the tile in LDS (smallest
+//      index hooking), writes each hot cell's tile root (frame index) into
+//      `labels` as a forest, clears the component outputs and writes the
+//      tile's partial sums (S, sum D ln D, hot sum, largest D) in a fixed
+//      order;
+//   2. heat_merge_kernel: threads on tile boundary cells unite hot pairs that
+//      cross a tile edge in the global forest (agent-scope CAS hooking, the
+//      smaller root wins); extra workgroups add each frame's tile partials in
+//      tile order into entropy and degree and pick the frame's fixed-point
+//      scale;
+//   3. heat_label_kernel, per tile again: each hot cell walks to its root and
+//      stores it; cells and fixed-point mass are summed per root in an LDS
+//      table, then added once per (tile, root) to the root's outputs (integer
+//      atomics, so the sums do not depend on their order);
+//   4. heat_mass_kernel: the root cells turn their fixed-point mass into
+//      cell_area * sum.
+// Every output is a deterministic function of the input.
+
+#include <climits>
+#include <cmath>
+
+#include "cluster_common.h"
+#include "internal.h"
+
+namespace flock {
+namespace {
+
+using namespace cl;
+
+constexpr int kHT = 32;                 // tile side, cells
+constexpr int kHThreads = 256;          // 4 cells per thread
+constexpr int kHRows = kHThreads / kHT; // rows per pass
+constexpr int kHTable = 1024;           // LDS table slots for (root -> sums) per tile
+
+struct TilePart {
+    double s, e, hot;  // sum D, sum D ln D over positive cells; sum D over hot cells
+    uint32_t maxbits;  // largest positive D, as its float bits (0 if none)
+    uint32_t pad;
+};
+
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u(uint32_t v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, 64));
+    return v;
+}
+
+struct TileGeom {
+    int f, x0, y0, w, h;
+};
+
+__device__ __forceinline__ TileGeom tile_of(const HeatArgs &a, long long b) {
+    const long long per = (long long)a.tiles_x * a.tiles_y;
+    TileGeom t;
+    t.f = (int)(b / per);
+    const int r = (int)(b - (long long)t.f * per);
+    t.y0 = (r / a.tiles_x) * kHT;
+    t.x0 = (r % a.tiles_x) * kHT;
+    t.w = min(kHT, a.grid_w - t.x0);
+    t.h = min(kHT, a.grid_h - t.y0);
+    return t;
+}
+
+__global__ __launch_bounds__(kHThreads) void heat_tile_kernel(HeatArgs a, TilePart *part) {
+    __shared__ int32_t par[kHT * kHT];
+    __shared__ uint8_t hotm[kHT * kHT];
+    __shared__ double s_red[3][kHThreads / 64];
+    __shared__ uint32_t s_max[kHThreads / 64];
+    const TileGeom t = tile_of(a, blockIdx.x);
+    const int tid = threadIdx.x, lx = tid % kHT, ly0 = tid / kHT;
+    const size_t cells = (size_t)a.grid_w * a.grid_h;
+    const float *D = a.density + (size_t)t.f * cells;
+
+    double s = 0.0, e = 0.0, hs = 0.0;
+    uint32_t mb = 0;
+    float v[kHT / kHRows];
+    bool hot[kHT / kHRows];
+#pragma unroll
+    for (int k = 0; k < kHT / kHRows; ++k) {
+        const int ly = ly0 + kHRows * k, l = ly * kHT + lx;
+        const bool in = lx < t.w && ly < t.h;
+        const size_t c = (size_t)(t.y0 + ly) * a.grid_w + t.x0 + lx;
+        v[k] = in ? D[c] : 0.0f;
+        hot[k] = in && v[k] >= a.threshold;
+        par[l] = l;
+        hotm[l] = hot[k];
+        if (v[k] > 0.0f) {
+            s += (double)v[k];
+            e += (double)v[k] * log((double)v[k]);
+            mb = max(mb, __float_as_uint(v[k]));
+        }
+        if (hot[k]) hs += (double)v[k];
+        if (in) {
+            a.comp_cells[(size_t)t.f * cells + c] = 0;
+            a.comp_mass[(size_t)t.f * cells + c] = 0.0;
+        }
+    }
+    __syncthreads();
+    // unite hot neighbours inside the tile: right, down, and for the
+    // 8-neighbourhood down-left and down-right
+#pragma unroll
+    for (int k = 0; k < kHT / kHRows; ++k) {
+        if (!hot[k]) continue;
+        const int ly = ly0 + kHRows * k, l = ly * kHT + lx;
+        if (lx + 1 < t.w && hotm[l + 1]) uf_unite<kGroup>(par, l, l + 1);
+        if (ly + 1 < t.h) {
+            if (hotm[l + kHT]) uf_unite<kGroup>(par, l, l + kHT);
+            if (a.connectivity == 8) {
+                if (lx > 0 && hotm[l + kHT - 1]) uf_unite<kGroup>(par, l, l + kHT - 1);
+                if (lx + 1 < t.w && hotm[l + kHT + 1]) uf_unite<kGroup>(par, l, l + kHT + 1);
+            }
+        }
+    }
+    __syncthreads();
+    // each hot cell's tile root (a smaller tile index is a smaller frame
+    // index) starts the global forest; cold cells are -1
+    int32_t *L = a.labels + (size_t)t.f * cells;
+#pragma unroll
+    for (int k = 0; k < kHT / kHRows; ++k) {
+        const int ly = ly0 + kHRows * k;
+        if (!(lx < t.w && ly < t.h)) continue;
+        const size_t c = (size_t)(t.y0 + ly) * a.grid_w + t.x0 + lx;
+        int32_t lab = -1;
+        if (hot[k]) {
+            const int r = uf_root<kGroup>(par, ly * kHT + lx);
+            lab = (t.y0 + r / kHT) * a.grid_w + t.x0 + r % kHT;
+        }
+        L[c] = lab;
+    }
+    // the tile's partial sums, in a fixed order
+    s = wave_sum_d(s);
+    e = wave_sum_d(e);
+    hs = wave_sum_d(hs);
+    mb = wave_max_u(mb);
+    const int wave = tid >> 6;
+    if ((tid & 63) == 0) {
+        s_red[0][wave] = s;
+        s_red[1][wave] = e;
+        s_red[2][wave] = hs;
+        s_max[wave] = mb;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        TilePart p{0.0, 0.0, 0.0, 0u, 0u};
+        for (int w = 0; w < kHThreads / 64; ++w) {
+            p.s += s_red[0][w];
+            p.e += s_red[1][w];
+            p.hot += s_red[2][w];
+            p.maxbits = max(p.maxbits, s_max[w]);
+        }
+        part[blockIdx.x] = p;
+    }
+}
+
+// Crossing forward edges of cell (gx, gy): right, down, down-left,
+// down-right (the last two for the 8-neighbourhood), where the neighbour
+// lies in another tile.
+__device__ __forceinline__ void merge_cell(const HeatArgs &a, int f, int gx, int gy) {
+    const size_t cells = (size_t)a.grid_w * a.grid_h;
+    const float *D = a.density + (size_t)f * cells;
+    const int32_t c = gy * a.grid_w + gx;
+    if (!(D[c] >= a.threshold)) return;
+    int32_t *L = a.labels + (size_t)f * cells;
+    const bool xe = (gx % kHT) == kHT - 1, x0 = (gx % kHT) == 0, ye = (gy % kHT) == kHT - 1;
+    auto take = [&](int nx, int ny) {
+        const int32_t n = ny * a.grid_w + nx;
+        if (D[n] >= a.threshold) uf_unite<kAgent>(L, c, n);
+    };
+    if (xe && gx + 1 < a.grid_w) take(gx + 1, gy);
+    if (gy + 1 < a.grid_h) {
+        if (ye) take(gx, gy + 1);
+        if (a.connectivity == 8) {
+            if (gx > 0 && (x0 || ye)) take(gx - 1, gy + 1);
+            if (gx + 1 < a.grid_w && (xe || ye)) take(gx + 1, gy + 1);
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void heat_merge_kernel(HeatArgs a, const TilePart *part, int32_t *shift,
+                                                         long long merge_blocks) {
+    const int tid = threadIdx.x;
+    if ((long long)blockIdx.x < merge_blocks) {
+        // boundary cells of every frame: for each inner vertical tile edge
+        // its two columns, for each inner horizontal edge its upper row
+        const long long nv = 2LL * (a.tiles_x - 1) * a.grid_h, nh = (long long)(a.tiles_y - 1) * a.grid_w;
+        const long long per = nv + nh;
+        const long long i = (long long)blockIdx.x * 256 + tid;
+        if (i >= per * a.n_frames) return;
+        const int f = (int)(i / per);
+        const long long j = i - (long long)f * per;
+        int gx, gy;
+        if (j < nv) {
+            const long long k = j / (2LL * a.grid_h);
+            const int side = (int)((j / a.grid_h) % 2);
+            gx = (int)(kHT * (k + 1) - 1 + side);
+            gy = (int)(j % a.grid_h);
+        } else {
+            const long long jj = j - nv;
+            gy = (int)(kHT * (jj / a.grid_w + 1) - 1);
+            gx = (int)(jj % a.grid_w);
+        }
+        merge_cell(a, f, gx, gy);
+        return;
+    }
+    // one workgroup per frame: tile partials in tile order (strided per lane,
+    // then a fixed shuffle tree), entropy, degree, the fixed-point scale
+    const int f = (int)((long long)blockIdx.x - merge_blocks);
+    if (tid >= 64) return;
+    const long long per = (long long)a.tiles_x * a.tiles_y;
+    const TilePart *P = part + (size_t)f * per;
+    double s = 0.0, e = 0.0, hs = 0.0;
+    uint32_t mb = 0;
+    for (long long k = tid; k < per; k += 64) {
+        s += P[k].s;
+        e += P[k].e;
+        hs += P[k].hot;
+        mb = max(mb, P[k].maxbits);
+    }
+    s = wave_sum_d(s);
+    e = wave_sum_d(e);
+    hs = wave_sum_d(hs);
+    mb = wave_max_u(mb);
+    if (tid == 0) {
+        a.entropy[f] = s > 0.0 ? log(s) - e / s : 0.0;
+        a.degree[f] = s > 0.0 ? hs / s : 0.0;
+        a.n_components[f] = 0;
+        // every positive D is below 2^(E + 1), E its float exponent; with
+        // 2^lg >= cells, D * 2^sh with sh = 62 - (E + 1) - lg keeps any sum of
+        // cells below 2^62
+        const int E = mb ? (int)((mb >> 23) & 0xffu) - 127 : 0;
+        int lg = 0;
+        while ((1LL << lg) < (long long)a.grid_w * a.grid_h) ++lg;
+        shift[f] = 62 - (max(E, -126) + 1) - lg;
+    }
+}
+
+__device__ __forceinline__ uint32_t slot_hash(int32_t root) { return ((uint32_t)root * 2654435761u) >> 22; }
+
+__global__ __launch_bounds__(kHThreads) void heat_label_kernel(HeatArgs a, const int32_t *shift) {
+    __shared__ int32_t keys[kHTable];
+    __shared__ int32_t cnt[kHTable];
+    __shared__ unsigned long long mass[kHTable];
+    const TileGeom t = tile_of(a, blockIdx.x);
+    const int tid = threadIdx.x, lx = tid % kHT, ly0 = tid / kHT;
+    for (int k = tid; k < kHTable; k += kHThreads) {
+        keys[k] = -1;
+        cnt[k] = 0;
+        mass[k] = 0ull;
+    }
+    __syncthreads();
+    const size_t cells = (size_t)a.grid_w * a.grid_h;
+    const float *D = a.density + (size_t)t.f * cells;
+    int32_t *L = a.labels + (size_t)t.f * cells;
+    const int sh = shift[t.f];
+#pragma unroll
+    for (int k = 0; k < kHT / kHRows; ++k) {
+        const int ly = ly0 + kHRows * k;
+        if (!(lx < t.w && ly < t.h)) continue;
+        const int32_t c = (t.y0 + ly) * a.grid_w + t.x0 + lx;
+        const float v = D[c];
+        if (!(v >= a.threshold)) continue;
+        // read-only walk: concurrent writers only store roots
+        const int32_t root = uf_root<kAgent>(L, c);
+        st_rlx<kAgent>(L + c, root);
+        if (root == c) atomicAdd(a.n_components + t.f, 1);
+        const unsigned long long q = (unsigned long long)llrint(ldexp((double)v, sh));
+        // this root's slot in the tile table (linear probing; a tile has at
+        // most kHT * kHT = kHTable distinct roots, so a slot is always found)
+        uint32_t h = slot_hash(root);
+        for (;;) {
+            const int32_t old = atomicCAS(keys + h, -1, root);
+            if (old == -1 || old == root) break;
+            h = (h + 1) & (kHTable - 1);
+        }
+        atomicAdd(cnt + h, 1);
+        atomicAdd(mass + h, q);
+    }
+    __syncthreads();
+    int32_t *CC = a.comp_cells + (size_t)t.f * cells;
+    unsigned long long *CM = reinterpret_cast<unsigned long long *>(a.comp_mass + (size_t)t.f * cells);
+    for (int k = tid; k < kHTable; k += kHThreads) {
+        const int32_t root = keys[k];
+        if (root < 0) continue;
+        atomicAdd(CC + root, cnt[k]);
+        atomicAdd(CM + root, mass[k]);
+    }
+}
+
+__global__ __launch_bounds__(256) void heat_mass_kernel(HeatArgs a, const int32_t *shift) {
+    const size_t cells = (size_t)a.grid_w * a.grid_h;
+    const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= cells * (size_t)a.n_frames) return;
+    const int f = (int)(i / cells);
+    const int32_t c = (int32_t)(i - (size_t)f * cells);
+    if (a.labels[i] != c) return;  // not a component's label cell
+    const unsigned long long q = reinterpret_cast<const unsigned long long *>(a.comp_mass)[i];
+    a.comp_mass[i] = ldexp((double)q, -shift[f]) * a.cell_area;
+}
+
+}  // namespace
+
+size_t heatmap_workspace_bytes(int32_t n_frames, int32_t grid_w, int32_t grid_h) {
+    if (n_frames <= 0 || grid_w < 1 || grid_h < 1) return 0;
+    const long long tiles = (long long)((grid_w + kHT - 1) / kHT) * ((grid_h + kHT - 1) / kHT);
+    const size_t parts = ((size_t)n_frames * tiles * sizeof(TilePart) + 255) & ~(size_t)255;
+    return parts + (((size_t)n_frames * sizeof(int32_t) + 255) & ~(size_t)255);
+}
+
+hipError_t launch_heatmap(HeatArgs a, void *workspace, hipStream_t stream) {
+    a.tiles_x = (a.grid_w + kHT - 1) / kHT;
+    a.tiles_y = (a.grid_h + kHT - 1) / kHT;
+    const long long tiles = (long long)a.tiles_x * a.tiles_y * a.n_frames;
+    TilePart *part = static_cast<TilePart *>(workspace);
+    const size_t parts = ((size_t)tiles * sizeof(TilePart) + 255) & ~(size_t)255;
+    int32_t *shift = reinterpret_cast<int32_t *>(static_cast<unsigned char *>(workspace) + parts);
+    const long long per = 2LL * (a.tiles_x - 1) * a.grid_h + (long long)(a.tiles_y - 1) * a.grid_w;
+    const long long merge_blocks = (per * a.n_frames + 255) / 256;
+    const long long cells = (long long)a.grid_w * a.grid_h * a.n_frames;
+    hipLaunchKernelGGL(heat_tile_kernel, dim3((unsigned)tiles), dim3(kHThreads), 0, stream, a, part);
+    hipLaunchKernelGGL(heat_merge_kernel, dim3((unsigned)(merge_blocks + a.n_frames)), dim3(256), 0, stream, a,
+                       part, shift, merge_blocks);
+    hipLaunchKernelGGL(heat_label_kernel, dim3((unsigned)tiles), dim3(kHThreads), 0, stream, a, shift);
+    hipLaunchKernelGGL(heat_mass_kernel, dim3((unsigned)((cells + 255) / 256)), dim3(256), 0, stream, a, shift);
+    return hipGetLastError();
+}
+
+}  // namespace flock

@@ -80,4 +80,26 @@ DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit);
 size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h, int n_cus);
 hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, float *partial, hipStream_t stream);
 
+// ----------------------------------------------------------------------------
+// Heatmap analytics
+// ----------------------------------------------------------------------------
+struct HeatArgs {
+    const float *density;     // [n_frames][grid_h][grid_w]
+    int32_t n_frames;
+    int32_t grid_w, grid_h;
+    int32_t tiles_x, tiles_y; // set by launch_heatmap
+    double cell_area;
+    float threshold;
+    int32_t connectivity;     // 4 or 8
+    int32_t *labels;          // [n_frames][grid_h][grid_w]
+    int32_t *n_components;    // [n_frames]
+    double *entropy;          // [n_frames]
+    double *degree;           // [n_frames]
+    int32_t *comp_cells;      // [n_frames][grid_h][grid_w]
+    double *comp_mass;        // [n_frames][grid_h][grid_w]
+};
+
+size_t heatmap_workspace_bytes(int32_t n_frames, int32_t grid_w, int32_t grid_h);
+hipError_t launch_heatmap(HeatArgs a, void *workspace, hipStream_t stream);
+
 }  // namespace flock

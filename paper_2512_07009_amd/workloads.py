@@ -214,3 +214,27 @@ def lattice_frame(nx: int, ny: int, step_q: int, x0: int = 0, y0: int = 0):
     ties for the radius test when step_q equals the radius)."""
     gx, gy = np.meshgrid(np.arange(nx), np.arange(ny))
     return np.stack([x0 + step_q * gx.ravel(), y0 + step_q * gy.ravel()], axis=1).astype(np.int32)
+
+
+def heat_grids(seed: int, n_frames: int, grid_h: int, grid_w: int, n_blobs: int = 6,
+               peak: float = 1e-3, empty_frac: float = 0.1) -> np.ndarray:
+    """Seeded density-like grids float32[F, grid_h, grid_w] for the heatmap
+    analytics: per frame a few cone-shaped blobs (value peak * max(0, 1 - r/R),
+    random centre, radius R and height) over a faint random floor, some cells
+    exactly zero, and some frames all zero.  Not a kernel density estimate:
+    only grids of the right shape and value range."""
+    rng = np.random.default_rng(seed)
+    gy, gx = np.meshgrid(np.arange(grid_h, dtype=np.float64), np.arange(grid_w, dtype=np.float64), indexing="ij")
+    out = np.zeros((n_frames, grid_h, grid_w), np.float32)
+    for f in range(n_frames):
+        if rng.random() < empty_frac:
+            continue
+        g = rng.random((grid_h, grid_w)) * peak * 0.05
+        g[rng.random((grid_h, grid_w)) < 0.2] = 0.0
+        for _ in range(int(rng.integers(1, n_blobs + 1))):
+            cx, cy = rng.uniform(0, grid_w), rng.uniform(0, grid_h)
+            rad = rng.uniform(1.5, max(2.0, 0.3 * max(grid_w, grid_h)))
+            amp = peak * rng.uniform(0.2, 1.0)
+            g += amp * np.maximum(0.0, 1.0 - np.hypot(gx - cx, gy - cy) / rad)
+        out[f] = g.astype(np.float32)
+    return out

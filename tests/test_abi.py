@@ -81,7 +81,35 @@ def test_density_rejects_bad_arguments(kwargs, needle):
     assert needle in binding.lib().flock_last_error().decode()
 
 
+def _heatmap(n_frames=1, gw=128, gh=72, area=225.0, thr=1e-4, conn=8, dens=FAKE, labels=FAKE, ncomp=FAKE,
+             ent=FAKE, deg=FAKE, cells=FAKE, mass=FAKE):
+    return binding.lib().heatmap_frames(dens, n_frames, gw, gh, area, thr, conn, labels, ncomp, ent, deg,
+                                        cells, mass, None, 0, None)
+
+
+@pytest.mark.parametrize("kwargs,needle", [
+    (dict(n_frames=-1), "n_frames"),
+    (dict(gw=0), "grid"),
+    (dict(gh=4097), "grid"),
+    (dict(area=-1.0), "cell_area"),
+    (dict(area=math.inf), "cell_area"),
+    (dict(thr=0.0), "threshold"),
+    (dict(thr=-1.0), "threshold"),
+    (dict(thr=math.nan), "threshold"),
+    (dict(conn=6), "connectivity"),
+    (dict(dens=None), "non-NULL"),
+    (dict(mass=None), "non-NULL"),
+    (dict(mass=FAKE4), "aligned"),
+    (dict(ent=FAKE4), "aligned"),
+])
+def test_heatmap_rejects_bad_arguments(kwargs, needle):
+    assert _heatmap(**kwargs) == binding.FLOCK_EINVAL
+    assert needle in binding.lib().flock_last_error().decode()
+
+
 def test_empty_batches_are_noops_without_a_device():
+    assert _heatmap(n_frames=0, dens=None, labels=None, ncomp=None, ent=None, deg=None, cells=None,
+                    mass=None) == 0
     assert _cluster(n_frames=0, total=0, xy=None, offsets=None, labels=None, kind=None, ncl=None) == 0
     assert _density(n_frames=0, total=0, xy=None, offsets=None, out=None) == 0
     assert binding.lib().flock_last_error().decode() == ""
@@ -91,6 +119,8 @@ def test_workspace_queries():
     lib = binding.lib()
     assert lib.cluster_frames_workspace(64, 128000, 2000) >= 0
     assert lib.density_frames_workspace(64, 128000, 128, 72) >= 0
+    assert lib.heatmap_frames_workspace(64, 128, 72) > 0
+    assert lib.heatmap_frames_workspace(0, 128, 72) == 0
 
 
 def test_eps_to_quanta():
