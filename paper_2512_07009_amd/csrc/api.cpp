@@ -367,13 +367,19 @@ flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid
     flock_status st = device_info(&dev);
     if (st != FLOCK_OK) return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const size_t need = flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h);
+    // one workgroup per frame when the grid's forest fits in LDS
+    // (FLOCK_HEATMAP_PATH=tiled takes the tiled kernels for every grid)
+    const char *hp = std::getenv("FLOCK_HEATMAP_PATH");
+    const bool tiled = hp && std::strcmp(hp, "tiled") == 0;
+    const bool resident = !tiled && flock::heatmap_frame_lds_bytes(grid_w, grid_h) + 1024 <= dev->lds_per_block;
+    const size_t need = resident ? flock::heatmap_frame_workspace_bytes(n_frames)
+                                 : flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h);
     if (workspace && workspace_bytes < need)
         return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
     if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
     void *ws = workspace;
     hipError_t err = hipSuccess;
-    if (!ws) {
+    if (!ws && need > 0) {
         err = hipMallocAsync(&ws, need, s);
         if (err != hipSuccess) return hip_fail(err, "workspace allocation");
     }
@@ -392,8 +398,8 @@ flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid
     a.degree = degree;
     a.comp_cells = comp_cells;
     a.comp_mass = comp_mass;
-    err = flock::launch_heatmap(a, ws, s);
-    if (!workspace) {
+    err = flock::launch_heatmap(a, ws, resident, s);
+    if (!workspace && need > 0) {
         const hipError_t ferr = hipFreeAsync(ws, s);
         if (err == hipSuccess) err = ferr;
     }

@@ -14,7 +14,10 @@
 //                of the positive cells (0 when S = 0);
 //   degree       (sum of density over hot cells) / S (0 when S = 0).
 //
-// Design (HBM-bound: a few bytes per cell):
+// Design (HBM-bound: a few bytes per cell).  Grids whose int32 forest fits
+// in LDS (grid_w * grid_h <= about 39k cells) take heat_frame_kernel, one
+// workgroup per frame (described there).  Larger grids take four tiled
+// kernels:
 //   1. heat_tile_kernel, one 256-thread workgroup per 32 x 32 tile: loads the
 //      tile once, unites hot neighbours inside the tile in LDS (smallest
 //      index hooking), writes each hot cell's tile root (frame index) into
@@ -320,6 +323,160 @@ __global__ __launch_bounds__(256) void heat_mass_kernel(HeatArgs a, const int32_
     a.comp_mass[i] = ldexp((double)q, -shift[f]) * a.cell_area;
 }
 
+// ---------------------------------------------------------------------------
+// Frame-resident path: one workgroup per frame, the whole grid's forest in LDS
+// ---------------------------------------------------------------------------
+
+constexpr int kFThreads = 1024;
+constexpr int kFWaves = kFThreads / 64;
+
+// Inclusive prefix sum over the wave (64-bit values).
+__device__ __forceinline__ unsigned long long wave_incl_scan_u64(unsigned long long v) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const unsigned long long t = __shfl_up(v, o, 64);
+        if (lane >= o) v += t;
+    }
+    return v;
+}
+
+// One frame per 1024-thread workgroup (grid_w * grid_h int32 parents in LDS):
+//   A. one coalesced pass over the grid: hot flags (parent = own index, -1
+//      cold), the partial sums, outputs cleared; a fixed-order block sum
+//      gives entropy, degree and the fixed-point scale;
+//   B. horizontal runs of hot cells, one row per wave at a time and 64 cells
+//      per ballot: every cell of a run points at the run's first cell;
+//   C. joins between consecutive rows, once per overlap: the vertical pair
+//      (c, c + w) unless the pair to its left already joins the same runs,
+//      and for the 8-neighbourhood a diagonal pair only where no edge-sharing
+//      path through c's row neighbour or the cell below exists;
+//   D. labels by read-only walks; per wave, runs of lanes with equal roots
+//      add their cells and fixed-point mass with one global atomic each.
+// heat_mass_kernel then converts the label cells' mass (after the kernel
+// boundary every atomic is complete; a device-scope fence inside the kernel
+// would instead write back the L2 once per workgroup).
+__global__ __launch_bounds__(kFThreads) void heat_frame_kernel(HeatArgs a, int32_t *shift) {
+    extern __shared__ int32_t P[];
+    __shared__ double s_red[3][kFWaves];
+    __shared__ uint32_t s_max[kFWaves];
+    __shared__ int s_shift, s_ncomp;
+    const int f = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int gw = a.grid_w, gh = a.grid_h;
+    const int cells = gw * gh;
+    const float *D = a.density + (size_t)f * cells;
+    int32_t *L = a.labels + (size_t)f * cells;
+    int32_t *CC = a.comp_cells + (size_t)f * cells;
+    double *CM = a.comp_mass + (size_t)f * cells;
+    unsigned long long *CMu = reinterpret_cast<unsigned long long *>(CM);
+
+    // A
+    double s = 0.0, e = 0.0, hs = 0.0;
+    uint32_t mb = 0;
+    for (int c = tid; c < cells; c += kFThreads) {
+        const float v = D[c];
+        const bool hot = v >= a.threshold;
+        P[c] = hot ? c : -1;
+        if (v > 0.0f) {
+            s += (double)v;
+            e += (double)v * log((double)v);
+            mb = max(mb, __float_as_uint(v));
+        }
+        if (hot) hs += (double)v;
+        CC[c] = 0;
+        CM[c] = 0.0;
+    }
+    s = wave_sum_d(s);
+    e = wave_sum_d(e);
+    hs = wave_sum_d(hs);
+    mb = wave_max_u(mb);
+    if (lane == 0) {
+        s_red[0][wave] = s;
+        s_red[1][wave] = e;
+        s_red[2][wave] = hs;
+        s_max[wave] = mb;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        double S = 0.0, E = 0.0, HS = 0.0;
+        uint32_t M = 0;
+        for (int w = 0; w < kFWaves; ++w) {
+            S += s_red[0][w];
+            E += s_red[1][w];
+            HS += s_red[2][w];
+            M = max(M, s_max[w]);
+        }
+        a.entropy[f] = S > 0.0 ? log(S) - E / S : 0.0;
+        a.degree[f] = S > 0.0 ? HS / S : 0.0;
+        const int Ex = M ? (int)((M >> 23) & 0xffu) - 127 : 0;
+        int lg = 0;
+        while ((1LL << lg) < (long long)cells) ++lg;
+        s_shift = 62 - (max(Ex, -126) + 1) - lg;
+        shift[f] = s_shift;
+        s_ncomp = 0;
+    }
+    // B (reads and writes only this wave's rows)
+    for (int row = wave; row < gh; row += kFWaves) {
+        int carry = -1;  // first cell of the run still open at the end of the last chunk
+        for (int x0 = 0; x0 < gw; x0 += 64) {
+            const int x = x0 + lane, c = row * gw + x;
+            const bool hot = x < gw && P[c] >= 0;
+            const uint64_t hm = __ballot(hot);
+            const uint64_t cold_below = ~hm & ((1ull << lane) - 1ull);
+            const int start = cold_below ? row * gw + x0 + (63 - __clzll(cold_below)) + 1
+                                         : (carry >= 0 ? carry : row * gw + x0);
+            if (hot) P[c] = start;
+            const int s63 = __shfl(start, 63, 64);
+            carry = ((hm >> 63) & 1ull) ? s63 : -1;
+        }
+    }
+    __syncthreads();
+    // C
+    auto hotc = [&](int c) { return ld_rlx<kGroup>(P + c) >= 0; };
+    for (int c = tid; c < cells - gw; c += kFThreads) {
+        if (!hotc(c)) continue;
+        const int gx = c % gw, d = c + gw;
+        const bool dh = hotc(d);
+        const bool lh = gx > 0 && hotc(c - 1), rh = gx + 1 < gw && hotc(c + 1);
+        if (dh && !(lh && hotc(d - 1))) uf_unite<kGroup>(P, c, d);
+        if (a.connectivity == 8 && !dh) {
+            if (gx + 1 < gw && !rh && hotc(d + 1)) uf_unite<kGroup>(P, c, d + 1);
+            if (gx > 0 && !lh && hotc(d - 1)) uf_unite<kGroup>(P, c, d - 1);
+        }
+    }
+    __syncthreads();
+    // D (loop bound rounded up to whole waves: the shuffles need every lane)
+    const int sh = s_shift;
+    const int cells_up = (cells + 63) & ~63;
+    for (int c = tid; c < cells_up; c += kFThreads) {
+        const bool in = c < cells;
+        const int32_t p0 = in ? P[c] : -1;
+        const int32_t r = p0 >= 0 ? uf_root<kGroup>(P, c) : -1;
+        unsigned long long q = 0ull;
+        if (r >= 0) {
+            L[c] = r;
+            q = (unsigned long long)llrint(ldexp((double)D[c], sh));
+            if (r == c) atomicAdd(&s_ncomp, 1);
+        } else if (in) {
+            L[c] = -1;
+        }
+        const int32_t prev = __shfl_up(r, 1, 64);
+        const bool head = lane == 0 || prev != r;
+        const uint64_t heads = __ballot(head);
+        const uint64_t after = lane == 63 ? 0ull : heads >> (lane + 1);
+        const int next = after ? lane + 1 + __ffsll((long long)after) - 1 : 64;  // next run's first lane
+        const unsigned long long incl = wave_incl_scan_u64(q);
+        const unsigned long long at_end = __shfl(incl, next - 1, 64);
+        const unsigned long long before = __shfl(incl, lane > 0 ? lane - 1 : 0, 64);
+        if (head && r >= 0) {
+            atomicAdd(CC + r, next - lane);
+            atomicAdd(CMu + r, at_end - (lane > 0 ? before : 0ull));
+        }
+    }
+    __syncthreads();
+    if (tid == 0) a.n_components[f] = s_ncomp;
+}
+
 }  // namespace
 
 size_t heatmap_workspace_bytes(int32_t n_frames, int32_t grid_w, int32_t grid_h) {
@@ -329,7 +486,22 @@ size_t heatmap_workspace_bytes(int32_t n_frames, int32_t grid_w, int32_t grid_h)
     return parts + (((size_t)n_frames * sizeof(int32_t) + 255) & ~(size_t)255);
 }
 
-hipError_t launch_heatmap(HeatArgs a, void *workspace, hipStream_t stream) {
+size_t heatmap_frame_lds_bytes(int32_t grid_w, int32_t grid_h) { return (size_t)grid_w * grid_h * sizeof(int32_t); }
+
+size_t heatmap_frame_workspace_bytes(int32_t n_frames) {
+    return n_frames > 0 ? (((size_t)n_frames * sizeof(int32_t) + 255) & ~(size_t)255) : 0;
+}
+
+hipError_t launch_heatmap(HeatArgs a, void *workspace, bool resident, hipStream_t stream) {
+    if (resident) {
+        int32_t *shift = static_cast<int32_t *>(workspace);
+        const long long cells = (long long)a.grid_w * a.grid_h * a.n_frames;
+        hipLaunchKernelGGL(heat_frame_kernel, dim3((unsigned)a.n_frames), dim3(kFThreads),
+                           heatmap_frame_lds_bytes(a.grid_w, a.grid_h), stream, a, shift);
+        hipLaunchKernelGGL(heat_mass_kernel, dim3((unsigned)((cells + 255) / 256)), dim3(256), 0, stream, a,
+                           shift);
+        return hipGetLastError();
+    }
     a.tiles_x = (a.grid_w + kHT - 1) / kHT;
     a.tiles_y = (a.grid_h + kHT - 1) / kHT;
     const long long tiles = (long long)a.tiles_x * a.tiles_y * a.n_frames;

@@ -100,6 +100,13 @@ struct HeatArgs {
 };
 
 size_t heatmap_workspace_bytes(int32_t n_frames, int32_t grid_w, int32_t grid_h);
-hipError_t launch_heatmap(HeatArgs a, void *workspace, hipStream_t stream);
+// Dynamic LDS of the frame-resident kernel (one workgroup per frame), and
+// its workspace (the per-frame fixed-point scales).
+size_t heatmap_frame_lds_bytes(int32_t grid_w, int32_t grid_h);
+size_t heatmap_frame_workspace_bytes(int32_t n_frames);
+// resident: one workgroup per frame with the grid in LDS (needs
+// heatmap_frame_lds_bytes within the device's limit); else the tiled kernels,
+// which use the workspace.
+hipError_t launch_heatmap(HeatArgs a, void *workspace, bool resident, hipStream_t stream);
 
 }  // namespace flock

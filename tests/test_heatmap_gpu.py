@@ -40,9 +40,18 @@ def check(grids, area, thr, conn, tag=""):
 SHAPES = [(1, 1, 1), (2, 3, 5), (3, 33, 31), (2, 64, 64), (4, 45, 70), (3, 72, 128), (1, 131, 257)]
 
 
+@pytest.fixture(params=["auto", "tiled"])
+def path(request, monkeypatch):
+    """auto: grids that fit in LDS take the one-workgroup-per-frame kernel;
+    tiled: FLOCK_HEATMAP_PATH=tiled forces the tiled kernels for every grid."""
+    if request.param == "tiled":
+        monkeypatch.setenv("FLOCK_HEATMAP_PATH", "tiled")
+    return request.param
+
+
 @pytest.mark.parametrize("conn", [4, 8])
 @pytest.mark.parametrize("F,h,w", SHAPES)
-def test_random_grids_gpu(F, h, w, conn):
+def test_random_grids_gpu(F, h, w, conn, path):
     g = wl.heat_grids(100 * h + w + conn, F, h, w)
     pos = g[g > 0]
     for q in (0.3, 0.7, 0.95):
@@ -51,7 +60,7 @@ def test_random_grids_gpu(F, h, w, conn):
 
 
 @pytest.mark.parametrize("conn", [4, 8])
-def test_tile_boundaries_gpu(conn):
+def test_tile_boundaries_gpu(conn, path):
     """Checkerboards and stripes put components across every tile edge and
     corner; one all-hot frame is a single component spanning all tiles."""
     h, w = 70, 100
@@ -62,7 +71,7 @@ def test_tile_boundaries_gpu(conn):
     check(g, 1.0, 0.5, conn, tag="patterns")
 
 
-def test_edge_cases_gpu():
+def test_edge_cases_gpu(path):
     g = np.zeros((3, 40, 50), np.float32)
     g[1] = 0.01
     g[2, 5, 7] = 0.02
@@ -86,7 +95,7 @@ def test_workload_grid_shapes_gpu(name):
     check(g, area, float(np.quantile(pos, 0.8)), 8, tag=name)
 
 
-def test_deterministic_gpu():
+def test_deterministic_gpu(path):
     g = wl.heat_grids(7, 6, 90, 140)
     thr = float(np.quantile(g[g > 0], 0.6))
     a = run(g, 1.0, thr, 8)
