@@ -10,7 +10,8 @@ standard DBSCAN (Ester et al., 1996) as the point-level reading of the
 paper's connected-component clustering (Section 2.3), the direct-sum
 Gaussian density grid of Algorithm 1 (Section 3.6), and the heatmap
 analytics of Section 2.3 and Algorithm 1 (threshold, connected components of
-grid cells, entropy, clustering degree).
+grid cells, entropy, clustering degree), and region-of-interest filtering
+with per-frame region counts (Section 2.2, Algorithm 1).
 """
 
 from __future__ import annotations
@@ -67,6 +68,10 @@ def _load():
         lib.oracle_heatmap_frames.argtypes = [p, i32, i32, i32, ctypes.c_double, ctypes.c_float, i32,
                                               p, p, p, p, p, p, i32]
         lib.oracle_heatmap_frames.restype = i32
+        lib.oracle_point_in_polygon.argtypes = [p, i32, i32, i32]
+        lib.oracle_point_in_polygon.restype = i32
+        lib.oracle_roi_filter.argtypes = [p, p, i32, p, i32, p, p, p, p]
+        lib.oracle_roi_filter.restype = i32
         _lib = lib
     return _lib
 
@@ -190,3 +195,31 @@ def heatmap_frames(density, cell_area: float, threshold: float, connectivity: in
     _check(r, "heatmap_frames")
     return {"labels": labels, "n_components": ncomp, "entropy": ent, "degree": deg,
             "comp_cells": comp_cells, "comp_mass": comp_mass}
+
+
+def point_in_polygon(poly, x: int, y: int) -> bool:
+    """Closed polygon (even-odd rule) test of one point, exact integers."""
+    pg = np.ascontiguousarray(np.asarray(poly, dtype=np.int32).reshape(-1, 2))
+    return bool(_load().oracle_point_in_polygon(_ptr(pg), pg.shape[0], int(x), int(y)))
+
+
+def roi_filter(xy, offsets, poly):
+    """Birds inside the ROI polygon (closed, even-odd), in input order.
+
+    Returns a dict: counts int32[F], xy int32[K, 2], offsets int32[F + 1]
+    (CSR of the kept birds), index int32[K] (their input indices).
+    """
+    a = _xy(xy)
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32))
+    pg = np.ascontiguousarray(np.asarray(poly, dtype=np.int32).reshape(-1, 2))
+    F = off.shape[0] - 1
+    if int(off[-1]) != a.shape[0]:
+        raise ValueError("offsets do not describe xy")
+    counts = np.zeros(max(F, 0), np.int32)
+    oxy = np.zeros_like(a)
+    ooff = np.zeros(F + 1, np.int32)
+    oidx = np.zeros(a.shape[0], np.int32)
+    k = _load().oracle_roi_filter(_ptr(a), _ptr(off), F, _ptr(pg), pg.shape[0], _ptr(counts), _ptr(oxy),
+                                  _ptr(ooff), _ptr(oidx))
+    _check(k, "roi_filter")
+    return {"counts": counts, "xy": oxy[:k].copy(), "offsets": ooff, "index": oidx[:k].copy()}

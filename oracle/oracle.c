@@ -61,6 +61,16 @@
  *         frame's density mass that lies in clusters (0 when S = 0).
  *     All sums are fp64 in row-major order.
  *
+ *  4. Region-of-interest filtering and per-frame region counts (the wall
+ *     pipeline counts the birds in a region near the wall, Section 2.2;
+ *     Algorithm 1 filters the birds to the ROI).  Reading: the ROI is a
+ *     polygon with integer vertices in quanta; a bird is inside when its
+ *     point lies in the closed polygon, boundary included, under the
+ *     even-odd rule (for a simple polygon: its interior plus its edges).
+ *     Kept birds keep their input order; per frame the count of kept birds.
+ *     The test is exact integer arithmetic (int64 products of coordinates
+ *     below 2^24).
+ *
  * Threads only split independent work items (whole frames for clustering
  * and heatmaps, whole grid rows for density); each item is computed exactly
  * as above.
@@ -499,4 +509,69 @@ int32_t oracle_heatmap_frames(const float *density, int32_t n_frames, int32_t gr
     for (int32_t t = 0; t < started; ++t) pthread_join(th[t], NULL);
     pthread_mutex_destroy(&job.mu);
     return job.rc;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Region of interest                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Point (px, py) on the closed segment from (ax, ay) to (bx, by). */
+static int on_segment(int64_t px, int64_t py, int64_t ax, int64_t ay, int64_t bx, int64_t by)
+{
+    const int64_t cross = (bx - ax) * (py - ay) - (by - ay) * (px - ax);
+    if (cross != 0) return 0;
+    const int64_t lo_x = ax < bx ? ax : bx, hi_x = ax < bx ? bx : ax;
+    const int64_t lo_y = ay < by ? ay : by, hi_y = ay < by ? by : ay;
+    return px >= lo_x && px <= hi_x && py >= lo_y && py <= hi_y;
+}
+
+/* 1 if (px, py) lies in the closed polygon (even-odd rule), else 0.
+ * poly: n vertices (x, y); the last vertex joins the first. */
+int32_t oracle_point_in_polygon(const int32_t *poly, int32_t n, int32_t px, int32_t py)
+{
+    int inside = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        const int32_t j = (i + 1) % n;
+        const int64_t ax = poly[2 * i], ay = poly[2 * i + 1];
+        const int64_t bx = poly[2 * j], by = poly[2 * j + 1];
+        if (on_segment(px, py, ax, ay, bx, by)) return 1;
+        /* does the edge cross the ray from (px, py) towards +x?  An edge
+         * counts when exactly one end lies strictly above the ray's line
+         * (so a vertex on the line is counted once), and the crossing point
+         * lies to the right of px:
+         *     px < ax + (py - ay) (bx - ax) / (by - ay)                     */
+        if ((ay > py) != (by > py)) {
+            const int64_t lhs = (int64_t)(px - ax) * (by - ay);
+            const int64_t rhs = (int64_t)(py - ay) * (bx - ax);
+            const int right = (by > ay) ? (lhs < rhs) : (lhs > rhs);
+            if (right) inside = !inside;
+        }
+    }
+    return inside;
+}
+
+/* Batch: keep[i] = 1 for birds inside the ROI; counts[f] = kept birds of
+ * frame f; kept birds are also written in order to out_xy / out_index with
+ * CSR out_offsets[F + 1]. */
+int32_t oracle_roi_filter(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
+                          const int32_t *poly, int32_t n_vertices, int32_t *counts,
+                          int32_t *out_xy, int32_t *out_offsets, int32_t *out_index)
+{
+    if (!offsets_ok(offsets, n_frames) || n_vertices < 3 || !poly) return ORACLE_EINVAL;
+    int32_t k = 0;
+    if (n_frames >= 0) out_offsets[0] = 0;
+    for (int32_t f = 0; f < n_frames; ++f) {
+        int32_t c = 0;
+        for (int32_t i = offsets[f]; i < offsets[f + 1]; ++i) {
+            if (!oracle_point_in_polygon(poly, n_vertices, xy[2 * i], xy[2 * i + 1])) continue;
+            out_xy[2 * k] = xy[2 * i];
+            out_xy[2 * k + 1] = xy[2 * i + 1];
+            out_index[k] = i;
+            ++k;
+            ++c;
+        }
+        counts[f] = c;
+        out_offsets[f + 1] = k;
+    }
+    return k;
 }

@@ -17,6 +17,7 @@ SRC = os.path.join(ROOT, "oracle", "oracle.c")
 DBSCAN_PINS = "tests/test_oracle_dbscan.py"
 KDE_PINS = "tests/test_oracle_kde.py"
 HEAT_PINS = "tests/test_oracle_heatmap.py"
+ROI_PINS = "tests/test_oracle_roi.py"
 
 MUTANTS = [
     # (name, old text, new text, which pin file must fail)
@@ -69,6 +70,15 @@ MUTANTS = [
     ("heat_mass_no_area", "for (int64_t c = 0; c < cells; ++c) comp_mass[c] *= cell_area;", "", HEAT_PINS),
     ("heat_mass_at_cell", "comp_mass[labels[c]] += (double)density[c];", "comp_mass[c] += (double)density[c];",
      HEAT_PINS),
+    ("roi_open_boundary", "if (on_segment(px, py, ax, ay, bx, by)) return 1;", "", ROI_PINS),
+    ("roi_segment_unbounded", "return px >= lo_x && px <= hi_x && py >= lo_y && py <= hi_y;", "return 1;",
+     ROI_PINS),
+    ("roi_vertex_on_ray_twice", "if ((ay > py) != (by > py)) {", "if ((ay >= py) != (by > py)) {", ROI_PINS),
+    ("roi_no_flip", "const int right = (by > ay) ? (lhs < rhs) : (lhs > rhs);", "const int right = lhs < rhs;",
+     ROI_PINS),
+    ("roi_axes_swapped", "if (!oracle_point_in_polygon(poly, n_vertices, xy[2 * i], xy[2 * i + 1])) continue;",
+     "if (!oracle_point_in_polygon(poly, n_vertices, xy[2 * i + 1], xy[2 * i])) continue;", ROI_PINS),
+    ("roi_counts_cumulative", "counts[f] = c;", "counts[f] = k;", ROI_PINS),
 ]
 
 
