@@ -48,6 +48,7 @@ KERNEL_SOURCES = {
     "cluster": "paper_2512_07009_amd/csrc/cluster.hip",
     "density": "paper_2512_07009_amd/csrc/density.hip",
     "heatmap": "paper_2512_07009_amd/csrc/heatmap.hip",
+    "roi": "paper_2512_07009_amd/csrc/roi.hip",
 }
 
 
@@ -267,6 +268,26 @@ def main():
     torch.cuda.synchronize(dev)
     t_heat = hev[0].elapsed_time(hev[1]) / K * 1e-3
 
+    # 4. region-of-interest filter and counts (its own entry point, not part of
+    #    `value`): a strip along the left wall, a five-vertex polygon
+    Wq, Hq = 16 * w.width_px, 16 * w.height_px
+    roi_poly = [[0, 0], [Wq // 8, 0], [Wq // 6, Hq // 2], [Wq // 8, Hq], [0, Hq]]
+    rout = {"counts": torch.empty(F, dtype=torch.int32, device=dev),
+            "xy": torch.empty((T, 2), dtype=torch.int32, device=dev),
+            "offsets": torch.empty(F + 1, dtype=torch.int32, device=dev),
+            "index": torch.empty(T, dtype=torch.int32, device=dev)}
+    for _ in range(3):
+        flock.roi_filter_frames(dxy, doff, roi_poly, out=rout, stream=stream)
+    rev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize(dev)
+    rev[0].record(stream)
+    for _ in range(K):
+        flock.roi_filter_frames(dxy, doff, roi_poly, out=rout, stream=stream)
+    rev[1].record(stream)
+    torch.cuda.synchronize(dev)
+    t_roi = rev[0].elapsed_time(rev[1]) / K * 1e-3
+    kept = int(rout["offsets"][-1].item())
+
     # algorithmic work per launch
     cluster_bytes = 13 * T + 8 * F + 4          # xy 8 + labels 4 + kind 1 per bird; offsets, n_clusters
     density_flops = 2.0 * w.grid_w * w.grid_h * T
@@ -284,6 +305,12 @@ def main():
           "threshold": heat_thr, "connectivity": 8, "in_value": False}
     he["frac"] = he["achieved"] / he["peak"]
     he["traffic"] = committed_traffic("heatmap", w.name)
+    roi_bytes = 8 * T + 12 * kept + 12 * F + 8  # xy in; kept xy + index out; offsets in, counts + offsets out
+    ro = {"bound": "hbm", "achieved": roi_bytes / t_roi / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+          "per_launch_us": t_roi * 1e6, "algorithmic_bytes": roi_bytes, "kept_birds": kept,
+          "roi_vertices": len(roi_poly), "in_value": False}
+    ro["frac"] = ro["achieved"] / ro["peak"]
+    ro["traffic"] = committed_traffic("roi", w.name)
     dominant = ("cluster_frames", cl) if t_cluster >= t_density else ("density_frames", de)
     roof = {k: dominant[1][k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")}
     roof["kernel"] = dominant[0]
@@ -313,7 +340,7 @@ def main():
         "timing": graph_note or ("value: HIP graph replay of the faster of the two-stream and one-stream steps; "
                                  "kernel durations: HIP events in the eager run of the same mode"),
         "roofline": roof,
-        "kernels": {"cluster_frames": cl, "density_frames": de, "heatmap_frames": he},
+        "kernels": {"cluster_frames": cl, "density_frames": de, "heatmap_frames": he, "roi_filter_frames": ro},
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")

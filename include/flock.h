@@ -189,6 +189,42 @@ flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid
 /* Bytes of workspace heatmap_frames needs for this batch shape. */
 size_t heatmap_frames_workspace(int32_t n_frames, int32_t grid_w, int32_t grid_h);
 
+/*
+ * roi_filter_frames - birds inside a region of interest, and per-frame counts.
+ *
+ * The wall pipeline counts the birds in a region near the wall (Section
+ * 2.2), and Algorithm 1 filters the birds to the region of interest before
+ * the density.  A bird is kept when its point (x_q, y_q) lies in the closed
+ * polygon roi_xy (edges and vertices included; even-odd rule, which for a
+ * simple polygon is its interior plus its boundary), tested exactly in
+ * integers.  Kept birds keep their input order.
+ *
+ * Arguments:
+ *   xy, offsets, n_frames, total   the batch, as for cluster_frames.
+ *   roi_xy        host in, int32[n_vertices][2], vertices in 1/16 px with
+ *                 |coordinate| <= 2^24, in either orientation; the last
+ *                 vertex joins the first.  Copied during the call.
+ *   n_vertices    3 .. 64.
+ *   counts        device out, int32[n_frames]: kept birds per frame.
+ *   out_xy        device out, int32[total][2] capacity: the kept birds, frame
+ *                 after frame (the first out_offsets[n_frames] rows written).
+ *   out_offsets   device out, int32[n_frames + 1]: CSR offsets of out_xy.
+ *   out_index     device out, int32[total] capacity, or NULL: the input index
+ *                 of each kept bird.
+ *   workspace     as for cluster_frames, sized by roi_filter_frames_workspace.
+ * Offsets must describe the batch (checked only with FLOCK_VALIDATE); with
+ * invalid offsets the outputs are unspecified but every access stays in
+ * bounds.
+ */
+flock_status roi_filter_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
+                               const int32_t *roi_xy, int32_t n_vertices, int32_t *counts, int32_t *out_xy,
+                               int32_t *out_offsets, int32_t *out_index, void *workspace,
+                               size_t workspace_bytes, void *stream);
+
+/* Bytes of workspace roi_filter_frames needs for this batch (a flag per bird,
+ * plus a count and a base per block of 2048 birds). */
+size_t roi_filter_frames_workspace(int32_t n_frames, int32_t total);
+
 /* Text of the last error on this thread ("" if none); valid until the next
  * library call on this thread. */
 const char *flock_last_error(void);

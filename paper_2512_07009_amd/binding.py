@@ -55,6 +55,10 @@ def lib() -> ctypes.CDLL:
         L.heatmap_frames.restype = i32
         L.heatmap_frames_workspace.argtypes = [i32, i32, i32]
         L.heatmap_frames_workspace.restype = sz
+        L.roi_filter_frames.argtypes = [p, p, i32, i32, p, i32, p, p, p, p, p, sz, p]
+        L.roi_filter_frames.restype = i32
+        L.roi_filter_frames_workspace.argtypes = [i32, i32]
+        L.roi_filter_frames_workspace.restype = sz
         L.flock_last_error.argtypes = []
         L.flock_last_error.restype = ctypes.c_char_p
         L.flock_version.argtypes = []
@@ -189,6 +193,34 @@ def heatmap_frames(density: torch.Tensor, cell_area_px2: float, threshold: float
                                   int(connectivity), _ptr(out["labels"]), _ptr(out["n_components"]),
                                   _ptr(out["entropy"]), _ptr(out["degree"]), _ptr(out["comp_cells"]),
                                   _ptr(out["comp_mass"]), _ptr(ws), ws_bytes, _stream(stream))
+    _check(st)
+    return out
+
+
+def roi_filter_frames(xy: torch.Tensor, offsets: torch.Tensor, roi_xy, with_index: bool = True, out=None,
+                      stream=None):
+    """Birds inside the closed ROI polygon roi_xy (host, [V, 2] int quanta).
+
+    Returns a dict of device tensors: counts int32[F], xy int32[T, 2]
+    (capacity; the first offsets[F] rows are the kept birds, frame after
+    frame), offsets int32[F + 1], index int32[T] (capacity; input index of
+    each kept bird) or None.
+    """
+    import numpy as np
+    F, T = _batch(xy, offsets)
+    poly = np.ascontiguousarray(np.asarray(roi_xy, dtype=np.int32).reshape(-1, 2))
+    dev = xy.device
+    if out is None:
+        out = {"counts": torch.empty(max(F, 0), dtype=torch.int32, device=dev),
+               "xy": torch.empty((T, 2), dtype=torch.int32, device=dev),
+               "offsets": torch.empty(F + 1, dtype=torch.int32, device=dev),
+               "index": torch.empty(T, dtype=torch.int32, device=dev) if with_index else None}
+    ws_bytes = lib().roi_filter_frames_workspace(F, T)
+    ws = _workspace(ws_bytes, dev, stream)
+    with torch.cuda.device(dev):
+        st = lib().roi_filter_frames(_ptr(xy), _ptr(offsets), F, T, poly.ctypes.data_as(ctypes.c_void_p),
+                                     poly.shape[0], _ptr(out["counts"]), _ptr(out["xy"]), _ptr(out["offsets"]),
+                                     _ptr(out.get("index")), _ptr(ws), ws_bytes, _stream(stream))
     _check(st)
     return out
 

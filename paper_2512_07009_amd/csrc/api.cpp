@@ -332,6 +332,75 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     return FLOCK_OK;
 }
 
+size_t roi_filter_frames_workspace(int32_t n_frames, int32_t total) {
+    g_error.clear();
+    return n_frames > 0 ? flock::roi_workspace_bytes(total) : 0;  // flags, block counts and bases
+}
+
+flock_status roi_filter_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
+                               const int32_t *roi_xy, int32_t n_vertices, int32_t *counts, int32_t *out_xy,
+                               int32_t *out_offsets, int32_t *out_index, void *workspace,
+                               size_t workspace_bytes, void *stream) {
+    g_error.clear();
+    if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
+    if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
+    if (n_vertices < 3 || n_vertices > flock::kRoiMaxVertices)
+        return fail(FLOCK_EINVAL, "n_vertices = %d outside 3..%d", n_vertices, flock::kRoiMaxVertices);
+    if (!roi_xy) return fail(FLOCK_EINVAL, "roi_xy must be non-NULL");
+    flock::RoiArgs a;
+    for (int v = 0; v < n_vertices; ++v) {
+        const int32_t x = roi_xy[2 * v], y = roi_xy[2 * v + 1];
+        if (x < -(1 << 24) || x > (1 << 24) || y < -(1 << 24) || y > (1 << 24))
+            return fail(FLOCK_EINVAL, "roi vertex %d = (%d, %d) outside |coordinate| <= 2^24", v, x, y);
+        a.vx[v] = x;
+        a.vy[v] = y;
+    }
+    for (int v = n_vertices; v < flock::kRoiMaxVertices; ++v) a.vx[v] = a.vy[v] = 0;
+    if (n_frames == 0) return FLOCK_OK;
+    if (!offsets || !counts || !out_offsets) return fail(FLOCK_EINVAL, "offsets, counts and out_offsets must be non-NULL");
+    if ((long long)total / flock::kRoiBlock + 1 > 0x7fffffffLL / 64)
+        return fail(FLOCK_EUNSUPPORTED, "batch too large for one launch");
+    if (total > 0 && (!xy || !out_xy)) return fail(FLOCK_EINVAL, "xy and out_xy must be non-NULL with total > 0");
+    if (!aligned(xy, 8) || !aligned(out_xy, 8)) return fail(FLOCK_EINVAL, "xy and out_xy must be 8-byte aligned");
+    if (!aligned(offsets, 4) || !aligned(counts, 4) || !aligned(out_offsets, 4) || !aligned(out_index, 4))
+        return fail(FLOCK_EINVAL, "offsets, counts, out_offsets and out_index must be 4-byte aligned");
+
+    const DeviceInfo *dev = nullptr;
+    flock_status st = device_info(&dev);
+    if (st != FLOCK_OK) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (validate_requested()) {
+        st = validate_batch(xy, offsets, n_frames, total, s);
+        if (st != FLOCK_OK) return st;
+    }
+    const size_t need = flock::roi_workspace_bytes(total);
+    if (workspace && workspace_bytes < need)
+        return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
+    if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
+    void *ws = workspace;
+    hipError_t err = hipSuccess;
+    if (!ws && need > 0) {
+        err = hipMallocAsync(&ws, need, s);
+        if (err != hipSuccess) return hip_fail(err, "workspace allocation");
+    }
+    a.xy = xy;
+    a.offsets = offsets;
+    a.n_frames = n_frames;
+    a.total = total;
+    a.n_vertices = n_vertices;
+    a.counts = counts;
+    a.out_xy = out_xy;
+    a.out_offsets = out_offsets;
+    a.out_index = out_index;
+    err = flock::launch_roi(a, ws, s);
+    if (!workspace && need > 0) {
+        const hipError_t ferr = hipFreeAsync(ws, s);
+        if (err == hipSuccess) err = ferr;
+    }
+    if (err != hipSuccess) return hip_fail(err, "roi kernels");
+    return FLOCK_OK;
+}
+
 size_t heatmap_frames_workspace(int32_t n_frames, int32_t grid_w, int32_t grid_h) {
     g_error.clear();
     return flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h);

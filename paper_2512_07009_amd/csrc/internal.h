@@ -109,4 +109,26 @@ size_t heatmap_frame_workspace_bytes(int32_t n_frames);
 // which use the workspace.
 hipError_t launch_heatmap(HeatArgs a, void *workspace, bool resident, hipStream_t stream);
 
+// ----------------------------------------------------------------------------
+// Region of interest
+// ----------------------------------------------------------------------------
+constexpr int kRoiMaxVertices = 64;
+constexpr int kRoiBlock = 2048;  // birds per block of the ROI kernels
+
+struct RoiArgs {
+    const int32_t *xy;        // [total][2]
+    const int32_t *offsets;   // [n_frames + 1]
+    int32_t n_frames;
+    int32_t total;
+    int32_t n_vertices;       // 3 .. kRoiMaxVertices
+    int32_t vx[kRoiMaxVertices], vy[kRoiMaxVertices];  // polygon, quanta
+    int32_t *counts;          // [n_frames]
+    int32_t *out_xy;          // [total][2] capacity
+    int32_t *out_offsets;     // [n_frames + 1]
+    int32_t *out_index;       // [total] capacity, or nullptr
+};
+
+size_t roi_workspace_bytes(int32_t total);
+hipError_t launch_roi(const RoiArgs &a, void *workspace, hipStream_t stream);
+
 }  // namespace flock

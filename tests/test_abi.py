@@ -107,7 +107,35 @@ def test_heatmap_rejects_bad_arguments(kwargs, needle):
     assert needle in binding.lib().flock_last_error().decode()
 
 
+SQUARE = (ctypes.c_int32 * 8)(0, 0, 160, 0, 160, 160, 0, 160)
+FAR = (ctypes.c_int32 * 8)(0, 0, 1 << 25, 0, 160, 160, 0, 160)
+
+
+def _roi(n_frames=1, total=4, poly=SQUARE, nv=4, xy=FAKE, offsets=FAKE, counts=FAKE, oxy=FAKE, ooff=FAKE,
+         oidx=FAKE):
+    return binding.lib().roi_filter_frames(xy, offsets, n_frames, total, poly, nv, counts, oxy, ooff, oidx,
+                                           None, 0, None)
+
+
+@pytest.mark.parametrize("kwargs,needle", [
+    (dict(n_frames=-1), "n_frames"),
+    (dict(total=-1), "total"),
+    (dict(nv=2), "n_vertices"),
+    (dict(nv=65), "n_vertices"),
+    (dict(poly=None), "roi_xy"),
+    (dict(poly=FAR), "2^24"),
+    (dict(offsets=None), "non-NULL"),
+    (dict(ooff=None), "non-NULL"),
+    (dict(oxy=None), "non-NULL"),
+    (dict(xy=FAKE4), "aligned"),
+])
+def test_roi_rejects_bad_arguments(kwargs, needle):
+    assert _roi(**kwargs) == binding.FLOCK_EINVAL
+    assert needle in binding.lib().flock_last_error().decode()
+
+
 def test_empty_batches_are_noops_without_a_device():
+    assert _roi(n_frames=0, total=0, xy=None, offsets=None, counts=None, oxy=None, ooff=None, oidx=None) == 0
     assert _heatmap(n_frames=0, dens=None, labels=None, ncomp=None, ent=None, deg=None, cells=None,
                     mass=None) == 0
     assert _cluster(n_frames=0, total=0, xy=None, offsets=None, labels=None, kind=None, ncl=None) == 0
@@ -121,6 +149,8 @@ def test_workspace_queries():
     assert lib.density_frames_workspace(64, 128000, 128, 72) >= 0
     assert lib.heatmap_frames_workspace(64, 128, 72) > 0
     assert lib.heatmap_frames_workspace(0, 128, 72) == 0
+    assert lib.roi_filter_frames_workspace(64, 128000) >= 128000
+    assert lib.roi_filter_frames_workspace(0, 0) == 0
 
 
 def test_eps_to_quanta():
