@@ -356,6 +356,10 @@ flock_status roi_filter_frames(const int32_t *xy, const int32_t *offsets, int32_
         a.vy[v] = y;
     }
     for (int v = n_vertices; v < flock::kRoiMaxVertices; ++v) a.vx[v] = a.vy[v] = 0;
+    a.bx0 = *std::min_element(a.vx, a.vx + n_vertices);
+    a.bx1 = *std::max_element(a.vx, a.vx + n_vertices);
+    a.by0 = *std::min_element(a.vy, a.vy + n_vertices);
+    a.by1 = *std::max_element(a.vy, a.vy + n_vertices);
     if (n_frames == 0) return FLOCK_OK;
     if (!offsets || !counts || !out_offsets) return fail(FLOCK_EINVAL, "offsets, counts and out_offsets must be non-NULL");
     if ((long long)total / flock::kRoiBlock + 1 > 0x7fffffffLL / 64)

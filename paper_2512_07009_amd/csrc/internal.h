@@ -122,6 +122,7 @@ struct RoiArgs {
     int32_t total;
     int32_t n_vertices;       // 3 .. kRoiMaxVertices
     int32_t vx[kRoiMaxVertices], vy[kRoiMaxVertices];  // polygon, quanta
+    int32_t bx0, by0, bx1, by1;                          // its bounding box
     int32_t *counts;          // [n_frames]
     int32_t *out_xy;          // [total][2] capacity
     int32_t *out_offsets;     // [n_frames + 1]

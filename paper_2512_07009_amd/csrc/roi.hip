@@ -18,6 +18,8 @@
 //      of the boundary bird (its block's base plus the flags before it in the
 //      block) gives out_offsets, and neighbouring boundaries give counts.
 
+#include <climits>
+
 #include "internal.h"
 
 namespace flock {
@@ -26,18 +28,29 @@ namespace {
 constexpr int kRThreadsR = 256;
 constexpr int kRWaves = kRThreadsR / 64;
 
-// Closed polygon test, even-odd rule.  An edge on which the point lies
-// decides at once (inside).  Otherwise each edge whose ends lie on
-// different sides of the horizontal line through the point (one strictly
-// above it, so that a vertex on the line is counted once) toggles the
-// result when it meets the line to the right of the point.
-__device__ __forceinline__ bool in_polygon(const int2 *poly, int n, int px, int py) {
+// Closed polygon test, even-odd rule.  A point outside the polygon's
+// bounding box is outside, and edges whose y range excludes the point are
+// skipped.  Otherwise an edge on which the point lies decides
+// at once (inside), and each edge whose ends lie on different sides of the
+// horizontal line through the point (one strictly above it, so that a vertex
+// on the line is counted once) toggles the result when it meets the line to
+// the right of the point.  Coordinates and vertices are within 2^24 in
+// magnitude, so every difference is below 2^25 and the cross product
+// ex qy - ey qx below 2^51: exact in fp64 (two exact products, an exact
+// difference), one fp64 multiply per product where a 64-bit integer product
+// takes several instructions.
+__device__ __forceinline__ bool in_polygon(const RoiArgs &a, const int2 *poly, int px, int py) {
+    if (px < a.bx0 || px > a.bx1 || py < a.by0 || py > a.by1) return false;
+    const int n = a.n_vertices;
     bool in = false;
     for (int i = 0; i < n; ++i) {
         const int2 A = poly[i], B = poly[i + 1 == n ? 0 : i + 1];
-        const long long ex = (long long)B.x - A.x, ey = (long long)B.y - A.y;
-        const long long qx = (long long)px - A.x, qy = (long long)py - A.y;
-        const long long cr = ex * qy - ey * qx;
+        // an edge whose y range excludes py neither holds the point nor
+        // crosses its line (both ends lie on one side)
+        if (py < min(A.y, B.y) || py > max(A.y, B.y)) continue;
+        const double ex = (double)(B.x - A.x), ey = (double)(B.y - A.y);
+        const double qx = (double)(px - A.x), qy = (double)(py - A.y);
+        const double cr = ex * qy - ey * qx;
         if (cr == 0 && px >= min(A.x, B.x) && px <= max(A.x, B.x) && py >= min(A.y, B.y) && py <= max(A.y, B.y))
             return true;
         const bool a_above = A.y > py, b_above = B.y > py;
@@ -66,15 +79,26 @@ __global__ __launch_bounds__(kRThreadsR) void roi_flag_kernel(RoiArgs a, uint8_t
     const int tid = threadIdx.x;
     const long long i0 = (long long)blockIdx.x * kRBlock;
     const int2 *P = reinterpret_cast<const int2 *>(a.xy);
-    int cnt = 0;
+    // all loads first, so that their latencies overlap
+    int2 pts[kRPer];
 #pragma unroll
     for (int k = 0; k < kRPer; ++k) {
         const long long i = i0 + k * kRThreadsR + tid;
-        if (i >= a.total) break;
-        const int2 p = P[i];
-        const bool in = in_polygon(poly, a.n_vertices, p.x, p.y);
-        flag[i] = in;
-        cnt += in;
+        pts[k] = i < a.total ? P[i] : make_int2(INT_MIN, INT_MIN);
+    }
+    // then every test, then every store (a store between two tests made the
+    // compiler wait for it before the next test's loads)
+    bool in[kRPer];
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) {
+        in[k] = in_polygon(a, poly, pts[k].x, pts[k].y);  // a padding lane's point is outside every box
+        cnt += in[k];
+    }
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) {
+        const long long i = i0 + k * kRThreadsR + tid;
+        if (i < a.total) flag[i] = in[k];
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
@@ -114,30 +138,44 @@ __global__ __launch_bounds__(1024) void roi_scan_kernel(const int32_t *bcount, i
 
 __global__ __launch_bounds__(kRThreadsR) void roi_write_kernel(RoiArgs a, const uint8_t *flag,
                                                               const int32_t *bbase) {
-    __shared__ int s_tot[kRWaves];
+    __shared__ int s_tot[kRPer][kRWaves];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const long long i0 = (long long)blockIdx.x * kRBlock;
     const int2 *P = reinterpret_cast<const int2 *>(a.xy);
     int2 *O = reinterpret_cast<int2 *>(a.out_xy);
-    int32_t at = bbase[blockIdx.x];
+    // every chunk's flags and ballots first, one barrier for all wave totals
+    bool in[kRPer];
+    uint64_t m[kRPer];
+#pragma unroll
     for (int k = 0; k < kRPer; ++k) {
         const long long i = i0 + k * kRThreadsR + tid;
-        const bool in = i < a.total && flag[i];
-        const uint64_t m = __ballot(in);
-        if (lane == 0) s_tot[wave] = __popcll(m);
-        __syncthreads();
+        in[k] = i < a.total && flag[i];
+    }
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) {
+        m[k] = __ballot(in[k]);
+        if (lane == 0) s_tot[k][wave] = __popcll(m[k]);
+    }
+    __syncthreads();
+    // the kept birds' coordinates are loaded before any store
+    int2 pt[kRPer];
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) pt[k] = in[k] ? P[i0 + k * kRThreadsR + tid] : make_int2(0, 0);
+    int32_t at = bbase[blockIdx.x];
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) {
         int before = 0, chunk = 0;
+#pragma unroll
         for (int w = 0; w < kRWaves; ++w) {
-            before += w < wave ? s_tot[w] : 0;
-            chunk += s_tot[w];
+            before += w < wave ? s_tot[k][w] : 0;
+            chunk += s_tot[k][w];
         }
-        if (in) {
-            const int32_t r = at + before + __popcll(m & ((1ull << lane) - 1ull));
-            O[r] = P[i];
-            if (a.out_index) a.out_index[r] = (int32_t)i;
+        if (in[k]) {
+            const int32_t r = at + before + __popcll(m[k] & ((1ull << lane) - 1ull));
+            O[r] = pt[k];
+            if (a.out_index) a.out_index[r] = (int32_t)(i0 + k * kRThreadsR + tid);
         }
         at += chunk;
-        __syncthreads();  // s_tot is rewritten by the next chunk
     }
 }
 
@@ -148,8 +186,23 @@ __device__ __forceinline__ int32_t out_position(const RoiArgs &a, const uint8_t 
     const int lane = threadIdx.x & 63;
     const int32_t b = i0 / kRBlock;
     const int32_t s0 = b * kRBlock;
+    // 16 flags per lane and load (a block is 2048 = 2 x 64 x 16 flags); the
+    // flag buffer is padded to 256 bytes, and bytes at or past i0 are masked
     int c = 0;
-    for (int32_t i = s0 + lane; i < i0; i += 64) c += flag[i];
+#pragma unroll
+    for (int j = 0; j < kRBlock / (64 * 16); ++j) {
+        const int32_t base = s0 + 16 * (lane + 64 * j);
+        if (base >= i0) continue;
+        const uint4 w = *reinterpret_cast<const uint4 *>(flag + base);
+        const int valid = min(16, i0 - base);
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int nb = min(max(valid - 4 * q, 0), 4);  // valid bytes in this word
+            const uint32_t keep = nb >= 4 ? 0xffffffffu : ((1u << (8 * nb)) - 1u);
+            c += (int)(((ws[q] & keep) * 0x01010101u) >> 24);  // bytes are 0 or 1
+        }
+    }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
     return bbase[b] + c;  // bbase has nb + 1 entries, and i0 = total gives b <= nb
