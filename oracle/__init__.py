@@ -10,8 +10,9 @@ standard DBSCAN (Ester et al., 1996) as the point-level reading of the
 paper's connected-component clustering (Section 2.3), the direct-sum
 Gaussian density grid of Algorithm 1 (Section 3.6), and the heatmap
 analytics of Section 2.3 and Algorithm 1 (threshold, connected components of
-grid cells, entropy, clustering degree), and region-of-interest filtering
-with per-frame region counts (Section 2.2, Algorithm 1).
+grid cells, entropy, clustering degree), region-of-interest filtering with
+per-frame region counts (Section 2.2, Algorithm 1), and drinker-line
+proximity (Section 2.3).
 """
 
 from __future__ import annotations
@@ -72,6 +73,10 @@ def _load():
         lib.oracle_point_in_polygon.restype = i32
         lib.oracle_roi_filter.argtypes = [p, p, i32, p, i32, p, p, p, p]
         lib.oracle_roi_filter.restype = i32
+        lib.oracle_near_segment.argtypes = [i32] * 7
+        lib.oracle_near_segment.restype = i32
+        lib.oracle_drinkers.argtypes = [p, p, i32, p, i32, i32, p, p, p]
+        lib.oracle_drinkers.restype = i32
         _lib = lib
     return _lib
 
@@ -223,3 +228,30 @@ def roi_filter(xy, offsets, poly):
                                   _ptr(ooff), _ptr(oidx))
     _check(k, "roi_filter")
     return {"counts": counts, "xy": oxy[:k].copy(), "offsets": ooff, "index": oidx[:k].copy()}
+
+
+def near_segment(x: int, y: int, seg, t: int) -> bool:
+    """Is point (x, y) strictly closer than t to the closed segment (ax, ay, bx, by)?"""
+    ax, ay, bx, by = (int(v) for v in seg)
+    return bool(_load().oracle_near_segment(int(x), int(y), ax, ay, bx, by, int(t)))
+
+
+def drinkers(xy, offsets, lines, t: int):
+    """Birds strictly closer than t quanta to some drinker-line segment.
+
+    Returns a dict: drinking uint8[T], line int32[T] (smallest index of such a
+    segment, -1 if none), counts int32[F].
+    """
+    a = _xy(xy)
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int32))
+    ln = np.ascontiguousarray(np.asarray(lines, dtype=np.int32).reshape(-1, 4))
+    F = off.shape[0] - 1
+    if int(off[-1]) != a.shape[0]:
+        raise ValueError("offsets do not describe xy")
+    drinking = np.zeros(a.shape[0], np.uint8)
+    line = np.zeros(a.shape[0], np.int32)
+    counts = np.zeros(max(F, 0), np.int32)
+    r = _load().oracle_drinkers(_ptr(a), _ptr(off), F, _ptr(ln), ln.shape[0], int(t), _ptr(drinking),
+                                _ptr(line), _ptr(counts))
+    _check(r, "drinkers")
+    return {"drinking": drinking, "line": line, "counts": counts}

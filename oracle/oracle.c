@@ -71,6 +71,18 @@
  *     The test is exact integer arithmetic (int64 products of coordinates
  *     below 2^24).
  *
+ *  5. Drinker-line proximity (the drinker pipeline measures each bird's
+ *     distance to the nearest drinker line and classifies the bird as
+ *     drinking when that distance falls below a threshold, Section 2.3).
+ *     Reading: drinker lines are segments with integer end points in quanta;
+ *     the distance is the Euclidean distance from the bird's point to the
+ *     closed segment (its nearest point, end points included); a bird drinks
+ *     when the distance to some segment is strictly below the threshold T
+ *     (quanta).  Per bird: the flag and the smallest index of such a segment
+ *     (-1 if none); per frame: the number of drinking birds.  The comparison
+ *     is exact: squared distances to end points in int64, and for a point
+ *     projecting inside the segment cross^2 < T^2 |b - a|^2 in 128 bits.
+ *
  * Threads only split independent work items (whole frames for clustering
  * and heatmaps, whole grid rows for density); each item is computed exactly
  * as above.
@@ -574,4 +586,52 @@ int32_t oracle_roi_filter(const int32_t *xy, const int32_t *offsets, int32_t n_f
         out_offsets[f + 1] = k;
     }
     return k;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Drinker-line proximity                                                   */
+/* ------------------------------------------------------------------------ */
+
+/* 1 if point (px, py) is strictly closer than t to the closed segment
+ * (ax, ay)-(bx, by).  Coordinates within 2^24 in magnitude, 0 <= t < 2^24. */
+int32_t oracle_near_segment(int32_t px, int32_t py, int32_t ax, int32_t ay, int32_t bx, int32_t by, int32_t t)
+{
+    const int64_t ux = (int64_t)bx - ax, uy = (int64_t)by - ay;   /* segment direction */
+    const int64_t wx = (int64_t)px - ax, wy = (int64_t)py - ay;   /* a -> p */
+    const int64_t t2 = (int64_t)t * t;
+    const int64_t len2 = ux * ux + uy * uy;
+    const int64_t dot = ux * wx + uy * wy;
+    if (len2 == 0 || dot <= 0) return wx * wx + wy * wy < t2;      /* nearest point: a */
+    if (dot >= len2) {                                              /* nearest point: b */
+        const int64_t vx = (int64_t)px - bx, vy = (int64_t)py - by;
+        return vx * vx + vy * vy < t2;
+    }
+    /* nearest point inside the segment: distance^2 = cross^2 / len2 */
+    const int64_t cross = ux * wy - uy * wx;
+    const unsigned __int128 c2 = (unsigned __int128)(cross < 0 ? -cross : cross) * (unsigned __int128)(cross < 0 ? -cross : cross);
+    const unsigned __int128 lim = (unsigned __int128)t2 * (unsigned __int128)len2;
+    return c2 < lim;
+}
+
+/* lines: n_lines segments (ax, ay, bx, by).  Per bird: drinking flag and the
+ * smallest index of a segment within t (-1 if none); per frame: counts. */
+int32_t oracle_drinkers(const int32_t *xy, const int32_t *offsets, int32_t n_frames, const int32_t *lines,
+                        int32_t n_lines, int32_t t, uint8_t *drinking, int32_t *line, int32_t *counts)
+{
+    if (!offsets_ok(offsets, n_frames) || n_lines < 1 || !lines || t < 0) return ORACLE_EINVAL;
+    for (int32_t f = 0; f < n_frames; ++f) {
+        int32_t c = 0;
+        for (int32_t i = offsets[f]; i < offsets[f + 1]; ++i) {
+            int32_t hit = -1;
+            for (int32_t k = 0; k < n_lines && hit < 0; ++k)
+                if (oracle_near_segment(xy[2 * i], xy[2 * i + 1], lines[4 * k], lines[4 * k + 1],
+                                        lines[4 * k + 2], lines[4 * k + 3], t))
+                    hit = k;
+            drinking[i] = hit >= 0;
+            line[i] = hit;
+            c += hit >= 0;
+        }
+        counts[f] = c;
+    }
+    return ORACLE_OK;
 }

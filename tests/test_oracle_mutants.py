@@ -18,6 +18,7 @@ DBSCAN_PINS = "tests/test_oracle_dbscan.py"
 KDE_PINS = "tests/test_oracle_kde.py"
 HEAT_PINS = "tests/test_oracle_heatmap.py"
 ROI_PINS = "tests/test_oracle_roi.py"
+DRINK_PINS = "tests/test_oracle_drinkers.py"
 
 MUTANTS = [
     # (name, old text, new text, which pin file must fail)
@@ -79,6 +80,17 @@ MUTANTS = [
     ("roi_axes_swapped", "if (!oracle_point_in_polygon(poly, n_vertices, xy[2 * i], xy[2 * i + 1])) continue;",
      "if (!oracle_point_in_polygon(poly, n_vertices, xy[2 * i + 1], xy[2 * i])) continue;", ROI_PINS),
     ("roi_counts_cumulative", "counts[f] = c;", "counts[f] = k;", ROI_PINS),
+    ("drink_at_threshold", "if (len2 == 0 || dot <= 0) return wx * wx + wy * wy < t2;",
+     "if (len2 == 0 || dot <= 0) return wx * wx + wy * wy <= t2;", DRINK_PINS),
+    ("drink_no_clamp_a", "if (len2 == 0 || dot <= 0) return wx * wx + wy * wy < t2;",
+     "if (len2 == 0) return wx * wx + wy * wy < t2;", DRINK_PINS),
+    ("drink_no_clamp_b", "if (dot >= len2) {", "if (0) {", DRINK_PINS),
+    ("drink_threshold_not_squared", "const unsigned __int128 lim = (unsigned __int128)t2 * (unsigned __int128)len2;",
+     "const unsigned __int128 lim = (unsigned __int128)t * (unsigned __int128)len2;", DRINK_PINS),
+    ("drink_last_index", "for (int32_t k = 0; k < n_lines && hit < 0; ++k)", "for (int32_t k = 0; k < n_lines; ++k)",
+     DRINK_PINS),
+    ("drink_dy_from_x", "const int64_t wx = (int64_t)px - ax, wy = (int64_t)py - ay;",
+     "const int64_t wx = (int64_t)px - ax, wy = (int64_t)py - ax;", DRINK_PINS),
 ]
 
 
