@@ -49,6 +49,7 @@ KERNEL_SOURCES = {
     "density": "paper_2512_07009_amd/csrc/density.hip",
     "heatmap": "paper_2512_07009_amd/csrc/heatmap.hip",
     "roi": "paper_2512_07009_amd/csrc/roi.hip",
+    "drinker": "paper_2512_07009_amd/csrc/roi.hip",
 }
 
 
@@ -288,6 +289,24 @@ def main():
     t_roi = rev[0].elapsed_time(rev[1]) / K * 1e-3
     kept = int(rout["offsets"][-1].item())
 
+    # 5. drinker-line proximity (its own entry point, not part of `value`): two
+    #    drinker lines across the frame, 20 px
+    dlines = [[Wq // 10, Hq // 4, 9 * Wq // 10, Hq // 4], [Wq // 10, 3 * Hq // 4, 9 * Wq // 10, 3 * Hq // 4]]
+    dthr = 16 * 20
+    dout = {"drinking": torch.empty(T, dtype=torch.uint8, device=dev),
+            "line": torch.empty(T, dtype=torch.int32, device=dev),
+            "counts": torch.empty(F, dtype=torch.int32, device=dev)}
+    for _ in range(3):
+        flock.drinker_proximity_frames(dxy, doff, dlines, dthr, out=dout, stream=stream)
+    dev_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize(dev)
+    dev_ev[0].record(stream)
+    for _ in range(K):
+        flock.drinker_proximity_frames(dxy, doff, dlines, dthr, out=dout, stream=stream)
+    dev_ev[1].record(stream)
+    torch.cuda.synchronize(dev)
+    t_drink = dev_ev[0].elapsed_time(dev_ev[1]) / K * 1e-3
+
     # algorithmic work per launch
     cluster_bytes = 13 * T + 8 * F + 4          # xy 8 + labels 4 + kind 1 per bird; offsets, n_clusters
     density_flops = 2.0 * w.grid_w * w.grid_h * T
@@ -311,6 +330,12 @@ def main():
           "roi_vertices": len(roi_poly), "in_value": False}
     ro["frac"] = ro["achieved"] / ro["peak"]
     ro["traffic"] = committed_traffic("roi", w.name)
+    drink_bytes = 13 * T + 8 * F + 4  # xy in, flag and line out per bird; offsets in, counts out
+    dr = {"bound": "hbm", "achieved": drink_bytes / t_drink / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+          "per_launch_us": t_drink * 1e6, "algorithmic_bytes": drink_bytes, "lines": len(dlines),
+          "threshold_px": dthr / 16, "in_value": False}
+    dr["frac"] = dr["achieved"] / dr["peak"]
+    dr["traffic"] = committed_traffic("drinker", w.name)
     dominant = ("cluster_frames", cl) if t_cluster >= t_density else ("density_frames", de)
     roof = {k: dominant[1][k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")}
     roof["kernel"] = dominant[0]
@@ -340,7 +365,8 @@ def main():
         "timing": graph_note or ("value: HIP graph replay of the faster of the two-stream and one-stream steps; "
                                  "kernel durations: HIP events in the eager run of the same mode"),
         "roofline": roof,
-        "kernels": {"cluster_frames": cl, "density_frames": de, "heatmap_frames": he, "roi_filter_frames": ro},
+        "kernels": {"cluster_frames": cl, "density_frames": de, "heatmap_frames": he, "roi_filter_frames": ro,
+                    "drinker_proximity_frames": dr},
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")

@@ -225,6 +225,39 @@ flock_status roi_filter_frames(const int32_t *xy, const int32_t *offsets, int32_
  * plus a count and a base per block of 2048 birds). */
 size_t roi_filter_frames_workspace(int32_t n_frames, int32_t total);
 
+/*
+ * drinker_proximity_frames - birds near drinker lines, and per-frame counts.
+ *
+ * The drinker pipeline computes each bird's distance to the nearest drinker
+ * line and classifies the bird as drinking when the distance falls below a
+ * threshold (Section 2.3).  Drinker lines are closed segments; the distance
+ * is from the bird's point to the nearest point of a segment (end points
+ * included); a bird drinks when that distance is strictly below
+ * threshold_q for some segment.  The test is exact in integers.
+ *
+ * Arguments:
+ *   xy, offsets, n_frames, total   the batch, as for cluster_frames
+ *                    (coordinates 0 <= x, y < 2^24).
+ *   lines            host in, int32[n_lines][4] = (ax, ay, bx, by) in 1/16 px,
+ *                    |coordinate| <= 2^24.  Copied during the call.
+ *   n_lines          1 .. 64.
+ *   threshold_q      distance threshold in 1/16 px, 0 .. 2^24.
+ *   drinking         device out, uint8[total] (16-byte aligned): 1 if drinking.
+ *   line             device out, int32[total], or NULL: the smallest index of
+ *                    a segment strictly within the threshold, -1 if none.
+ *   counts           device out, int32[n_frames]: drinking birds per frame.
+ *   workspace        as for cluster_frames, sized by
+ *                    drinker_proximity_frames_workspace.
+ */
+flock_status drinker_proximity_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
+                                      int32_t total, const int32_t *lines, int32_t n_lines,
+                                      int32_t threshold_q, uint8_t *drinking, int32_t *line,
+                                      int32_t *counts, void *workspace, size_t workspace_bytes,
+                                      void *stream);
+
+/* Bytes of workspace drinker_proximity_frames needs for this batch. */
+size_t drinker_proximity_frames_workspace(int32_t n_frames, int32_t total);
+
 /* Text of the last error on this thread ("" if none); valid until the next
  * library call on this thread. */
 const char *flock_last_error(void);

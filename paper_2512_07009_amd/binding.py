@@ -59,6 +59,10 @@ def lib() -> ctypes.CDLL:
         L.roi_filter_frames.restype = i32
         L.roi_filter_frames_workspace.argtypes = [i32, i32]
         L.roi_filter_frames_workspace.restype = sz
+        L.drinker_proximity_frames.argtypes = [p, p, i32, i32, p, i32, i32, p, p, p, p, sz, p]
+        L.drinker_proximity_frames.restype = i32
+        L.drinker_proximity_frames_workspace.argtypes = [i32, i32]
+        L.drinker_proximity_frames_workspace.restype = sz
         L.flock_last_error.argtypes = []
         L.flock_last_error.restype = ctypes.c_char_p
         L.flock_version.argtypes = []
@@ -221,6 +225,33 @@ def roi_filter_frames(xy: torch.Tensor, offsets: torch.Tensor, roi_xy, with_inde
         st = lib().roi_filter_frames(_ptr(xy), _ptr(offsets), F, T, poly.ctypes.data_as(ctypes.c_void_p),
                                      poly.shape[0], _ptr(out["counts"]), _ptr(out["xy"]), _ptr(out["offsets"]),
                                      _ptr(out.get("index")), _ptr(ws), ws_bytes, _stream(stream))
+    _check(st)
+    return out
+
+
+def drinker_proximity_frames(xy: torch.Tensor, offsets: torch.Tensor, lines, threshold_q: int,
+                             with_line: bool = True, out=None, stream=None):
+    """Birds strictly closer than threshold_q (1/16 px) to some drinker-line
+    segment; lines: host [L, 4] int (ax, ay, bx, by) in 1/16 px.
+
+    Returns a dict of device tensors: drinking uint8[T], line int32[T]
+    (smallest index of such a segment, -1 if none) or None, counts int32[F].
+    """
+    import numpy as np
+    F, T = _batch(xy, offsets)
+    ln = np.ascontiguousarray(np.asarray(lines, dtype=np.int32).reshape(-1, 4))
+    dev = xy.device
+    if out is None:
+        out = {"drinking": torch.empty(T, dtype=torch.uint8, device=dev),
+               "line": torch.empty(T, dtype=torch.int32, device=dev) if with_line else None,
+               "counts": torch.empty(max(F, 0), dtype=torch.int32, device=dev)}
+    ws_bytes = lib().drinker_proximity_frames_workspace(F, T)
+    ws = _workspace(ws_bytes, dev, stream)
+    with torch.cuda.device(dev):
+        st = lib().drinker_proximity_frames(_ptr(xy), _ptr(offsets), F, T, ln.ctypes.data_as(ctypes.c_void_p),
+                                            ln.shape[0], int(threshold_q), _ptr(out["drinking"]),
+                                            _ptr(out.get("line")), _ptr(out["counts"]), _ptr(ws), ws_bytes,
+                                            _stream(stream))
     _check(st)
     return out
 

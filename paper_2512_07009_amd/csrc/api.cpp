@@ -405,6 +405,85 @@ flock_status roi_filter_frames(const int32_t *xy, const int32_t *offsets, int32_
     return FLOCK_OK;
 }
 
+size_t drinker_proximity_frames_workspace(int32_t n_frames, int32_t total) {
+    g_error.clear();
+    return n_frames > 0 ? flock::drink_workspace_bytes(total) : 0;  // block counts and bases
+}
+
+flock_status drinker_proximity_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
+                                      const int32_t *lines, int32_t n_lines, int32_t threshold_q,
+                                      uint8_t *drinking, int32_t *line, int32_t *counts, void *workspace,
+                                      size_t workspace_bytes, void *stream) {
+    g_error.clear();
+    if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
+    if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
+    if (n_lines < 1 || n_lines > flock::kDrinkMaxLines)
+        return fail(FLOCK_EINVAL, "n_lines = %d outside 1..%d", n_lines, flock::kDrinkMaxLines);
+    if (!lines) return fail(FLOCK_EINVAL, "lines must be non-NULL");
+    if (threshold_q < 0 || threshold_q > (1 << 24))
+        return fail(FLOCK_EINVAL, "threshold_q = %d outside 0..2^24", threshold_q);
+    flock::DrinkArgs a;
+    for (int l = 0; l < flock::kDrinkMaxLines; ++l) {
+        if (l >= n_lines) {
+            a.ax[l] = a.ay[l] = a.bx[l] = a.by[l] = 0;
+            continue;
+        }
+        for (int k = 0; k < 4; ++k) {
+            const int32_t v = lines[4 * l + k];
+            if (v < -(1 << 24) || v > (1 << 24))
+                return fail(FLOCK_EINVAL, "line %d coordinate %d outside |coordinate| <= 2^24", l, v);
+        }
+        a.ax[l] = lines[4 * l];
+        a.ay[l] = lines[4 * l + 1];
+        a.bx[l] = lines[4 * l + 2];
+        a.by[l] = lines[4 * l + 3];
+    }
+    if (n_frames == 0) return FLOCK_OK;
+    if (!offsets || !counts) return fail(FLOCK_EINVAL, "offsets and counts must be non-NULL");
+    if (total > 0 && (!xy || !drinking)) return fail(FLOCK_EINVAL, "xy and drinking must be non-NULL with total > 0");
+    if (!aligned(xy, 8)) return fail(FLOCK_EINVAL, "xy must be 8-byte aligned");
+    if (!aligned(drinking, 16)) return fail(FLOCK_EINVAL, "drinking must be 16-byte aligned");
+    if (!aligned(offsets, 4) || !aligned(counts, 4) || !aligned(line, 4))
+        return fail(FLOCK_EINVAL, "offsets, counts and line must be 4-byte aligned");
+    if ((long long)total / flock::kRoiBlock + 1 > 0x7fffffffLL / 64)
+        return fail(FLOCK_EUNSUPPORTED, "batch too large for one launch");
+
+    const DeviceInfo *dev = nullptr;
+    flock_status st = device_info(&dev);
+    if (st != FLOCK_OK) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (validate_requested()) {
+        st = validate_batch(xy, offsets, n_frames, total, s);
+        if (st != FLOCK_OK) return st;
+    }
+    const size_t need = flock::drink_workspace_bytes(total);
+    if (workspace && workspace_bytes < need)
+        return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
+    if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
+    void *ws = workspace;
+    hipError_t err = hipSuccess;
+    if (!ws) {
+        err = hipMallocAsync(&ws, need, s);
+        if (err != hipSuccess) return hip_fail(err, "workspace allocation");
+    }
+    a.xy = xy;
+    a.offsets = offsets;
+    a.n_frames = n_frames;
+    a.total = total;
+    a.n_lines = n_lines;
+    a.threshold = threshold_q;
+    a.drinking = drinking;
+    a.line = line;
+    a.counts = counts;
+    err = flock::launch_drinkers(a, ws, s);
+    if (!workspace) {
+        const hipError_t ferr = hipFreeAsync(ws, s);
+        if (err == hipSuccess) err = ferr;
+    }
+    if (err != hipSuccess) return hip_fail(err, "drinker kernels");
+    return FLOCK_OK;
+}
+
 size_t heatmap_frames_workspace(int32_t n_frames, int32_t grid_w, int32_t grid_h) {
     g_error.clear();
     return flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h);

@@ -132,4 +132,25 @@ struct RoiArgs {
 size_t roi_workspace_bytes(int32_t total);
 hipError_t launch_roi(const RoiArgs &a, void *workspace, hipStream_t stream);
 
+// ----------------------------------------------------------------------------
+// Drinker-line proximity
+// ----------------------------------------------------------------------------
+constexpr int kDrinkMaxLines = 64;
+
+struct DrinkArgs {
+    const int32_t *xy;        // [total][2]
+    const int32_t *offsets;   // [n_frames + 1]
+    int32_t n_frames;
+    int32_t total;
+    int32_t n_lines;          // 1 .. kDrinkMaxLines
+    int32_t threshold;        // quanta, 0 .. 2^24
+    int32_t ax[kDrinkMaxLines], ay[kDrinkMaxLines], bx[kDrinkMaxLines], by[kDrinkMaxLines];
+    uint8_t *drinking;        // [total], 16-byte aligned
+    int32_t *line;            // [total] or nullptr
+    int32_t *counts;          // [n_frames]
+};
+
+size_t drink_workspace_bytes(int32_t total);
+hipError_t launch_drinkers(const DrinkArgs &a, void *workspace, hipStream_t stream);
+
 }  // namespace flock

@@ -1,4 +1,5 @@
-// roi.hip - region-of-interest filter and per-frame region counts on gfx950.
+// roi.hip - region-of-interest filter and per-frame region counts, and
+// drinker-line proximity, on gfx950.
 //
 // What is computed (the wall pipeline counts the birds in a region near the
 // wall, Section 2.2; Algorithm 1 filters the birds to the region of
@@ -14,9 +15,11 @@
 //   3. roi_write_kernel: ballots and wave totals give each kept bird its rank
 //      in its block; coordinates and input index go to base + rank, so kept
 //      birds keep their input order;
-//   4. roi_offsets_kernel, one wave per frame boundary: the output position
+//   4. frame_counts_kernel, one wave per frame boundary: the output position
 //      of the boundary bird (its block's base plus the flags before it in the
 //      block) gives out_offsets, and neighbouring boundaries give counts.
+// Drinker-line proximity reuses steps 2 and 4 on its own flags (see
+// drink_flag_kernel).
 
 #include <climits>
 
@@ -179,21 +182,36 @@ __global__ __launch_bounds__(kRThreadsR) void roi_write_kernel(RoiArgs a, const 
     }
 }
 
-// Output position of input bird i0 (0 <= i0 <= total): its block's base plus
-// the kept birds before it in the block (wave-uniform call).
-__device__ __forceinline__ int32_t out_position(const RoiArgs &a, const uint8_t *flag, const int32_t *bbase,
-                                                int32_t i0) {
+// Per-frame counts of flagged birds, for the ROI filter (which also needs
+// the CSR offsets of its output) and the drinker flags.
+struct FrameCounts {
+    const uint8_t *flag;      // [total] 0 or 1, padded to 256 bytes
+    const int32_t *bbase;     // [nb + 1] flagged birds before each 2048-bird block
+    const int32_t *offsets;   // [n_frames + 1]
+    int32_t n_frames, total;
+    int32_t *counts;          // [n_frames]
+    int32_t *out_offsets;     // [n_frames + 1] or nullptr
+};
+
+// Flagged birds before input bird i0 (0 <= i0 <= total): its block's base
+// plus the flags before it in the block (wave-uniform call).
+__device__ __forceinline__ int32_t flagged_before(const FrameCounts &fc, int32_t i0) {
     const int lane = threadIdx.x & 63;
     const int32_t b = i0 / kRBlock;
     const int32_t s0 = b * kRBlock;
-    // 16 flags per lane and load (a block is 2048 = 2 x 64 x 16 flags); the
-    // flag buffer is padded to 256 bytes, and bytes at or past i0 are masked
+    // 16 flags per lane and load (a block is 2048 = 2 x 64 x 16 flags; the
+    // flag array is 16-byte aligned), bytes at or past i0 masked; the last
+    // partial word of the array is read byte by byte, never past total
     int c = 0;
 #pragma unroll
     for (int j = 0; j < kRBlock / (64 * 16); ++j) {
         const int32_t base = s0 + 16 * (lane + 64 * j);
         if (base >= i0) continue;
-        const uint4 w = *reinterpret_cast<const uint4 *>(flag + base);
+        if (base + 16 > fc.total) {
+            for (int32_t i = base; i < i0; ++i) c += fc.flag[i];
+            continue;
+        }
+        const uint4 w = *reinterpret_cast<const uint4 *>(fc.flag + base);
         const int valid = min(16, i0 - base);
         const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
@@ -205,20 +223,92 @@ __device__ __forceinline__ int32_t out_position(const RoiArgs &a, const uint8_t 
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, 64);
-    return bbase[b] + c;  // bbase has nb + 1 entries, and i0 = total gives b <= nb
+    return fc.bbase[b] + c;  // bbase has nb + 1 entries, and i0 = total gives b <= nb
 }
 
-__global__ __launch_bounds__(256) void roi_offsets_kernel(RoiArgs a, const uint8_t *flag, const int32_t *bbase) {
+// One wave per frame boundary f = 0 .. n_frames.
+__global__ __launch_bounds__(256) void frame_counts_kernel(FrameCounts fc) {
     const int f = (int)(((long long)blockIdx.x * 256 + threadIdx.x) >> 6);
-    if (f > a.n_frames) return;  // wave-uniform
+    if (f > fc.n_frames) return;  // wave-uniform
     // frame boundaries clamped into [0, total] (offsets are only validated
     // with FLOCK_VALIDATE; this keeps every read in bounds)
-    auto bound = [&](int g) { return g == a.n_frames ? a.total : min(max(a.offsets[g], 0), a.total); };
-    const int32_t v = out_position(a, flag, bbase, bound(f));
-    if ((threadIdx.x & 63) == 0) a.out_offsets[f] = v;
-    if (f < a.n_frames) {
-        const int32_t v1 = out_position(a, flag, bbase, bound(f + 1));
-        if ((threadIdx.x & 63) == 0) a.counts[f] = max(v1 - v, 0);
+    auto bound = [&](int g) { return g == fc.n_frames ? fc.total : min(max(fc.offsets[g], 0), fc.total); };
+    const int32_t v = flagged_before(fc, bound(f));
+    if (fc.out_offsets && (threadIdx.x & 63) == 0) fc.out_offsets[f] = v;
+    if (f < fc.n_frames) {
+        const int32_t v1 = flagged_before(fc, bound(f + 1));
+        if ((threadIdx.x & 63) == 0) fc.counts[f] = max(v1 - v, 0);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Drinker-line proximity
+// ---------------------------------------------------------------------------
+
+// Is (px, py) strictly closer than t to the closed segment s = (ax, ay, bx,
+// by)?  The nearest point of the segment is a when the projection of p
+// falls before a (or the segment is a point), b when it falls past b, and
+// otherwise the foot of the perpendicular, at squared distance
+// cross^2 / len2.  Coordinates within 2^24: squared end distances, len2 and
+// the projection fit int64, and cross^2 < t^2 len2 is compared as a 128-bit
+// product (high and low halves).
+__device__ __forceinline__ bool near_segment(int4 s, int px, int py, long long t2) {
+    const long long ux = (long long)s.z - s.x, uy = (long long)s.w - s.y;
+    const long long wx = (long long)px - s.x, wy = (long long)py - s.y;
+    const long long len2 = ux * ux + uy * uy, dot = ux * wx + uy * wy;
+    if (len2 == 0 || dot <= 0) return wx * wx + wy * wy < t2;
+    if (dot >= len2) {
+        const long long vx = (long long)px - s.z, vy = (long long)py - s.w;
+        return vx * vx + vy * vy < t2;
+    }
+    const long long cr = ux * wy - uy * wx;
+    const unsigned long long c = (unsigned long long)(cr < 0 ? -cr : cr);
+    const unsigned long long ch = __umul64hi(c, c), cl = c * c;
+    const unsigned long long lh = __umul64hi((unsigned long long)t2, (unsigned long long)len2),
+                             ll = (unsigned long long)t2 * (unsigned long long)len2;
+    return ch < lh || (ch == lh && cl < ll);
+}
+
+__global__ __launch_bounds__(kRThreadsR) void drink_flag_kernel(DrinkArgs a, int32_t *bcount) {
+    __shared__ int4 seg[kDrinkMaxLines];
+    __shared__ int s_cnt[kRWaves];
+    const int tid = threadIdx.x;
+    if (tid < a.n_lines) seg[tid] = make_int4(a.ax[tid], a.ay[tid], a.bx[tid], a.by[tid]);
+    __syncthreads();
+    const long long i0 = (long long)blockIdx.x * kRBlock;
+    const int2 *P = reinterpret_cast<const int2 *>(a.xy);
+    const long long t2 = (long long)a.threshold * a.threshold;
+    int2 pts[kRPer];
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) {
+        const long long i = i0 + k * kRThreadsR + tid;
+        pts[k] = i < a.total ? P[i] : make_int2(0, 0);
+    }
+    int32_t hit[kRPer];
+    int cnt = 0;
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) {
+        hit[k] = -1;
+        for (int l = 0; l < a.n_lines && hit[k] < 0; ++l)
+            if (near_segment(seg[l], pts[k].x, pts[k].y, t2)) hit[k] = l;
+        const long long i = i0 + k * kRThreadsR + tid;
+        cnt += (i < a.total) & (hit[k] >= 0);
+    }
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) {
+        const long long i = i0 + k * kRThreadsR + tid;
+        if (i >= a.total) continue;
+        a.drinking[i] = hit[k] >= 0;
+        if (a.line) a.line[i] = hit[k];
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+    if ((tid & 63) == 0) s_cnt[tid >> 6] = cnt;
+    __syncthreads();
+    if (tid == 0) {
+        int t = 0;
+        for (int w = 0; w < kRWaves; ++w) t += s_cnt[w];
+        bcount[blockIdx.x] = t;
     }
 }
 
@@ -238,9 +328,26 @@ hipError_t launch_roi(const RoiArgs &a, void *workspace, hipStream_t stream) {
     if (nb > 0) hipLaunchKernelGGL(roi_flag_kernel, dim3((unsigned)nb), dim3(kRThreadsR), 0, stream, a, flag, bcount);
     hipLaunchKernelGGL(roi_scan_kernel, dim3(1), dim3(1024), 0, stream, bcount, bbase, nb);
     if (nb > 0) hipLaunchKernelGGL(roi_write_kernel, dim3((unsigned)nb), dim3(kRThreadsR), 0, stream, a, flag, bbase);
+    const FrameCounts fc{flag, bbase, a.offsets, a.n_frames, a.total, a.counts, a.out_offsets};
     const long long waves = (long long)a.n_frames + 1;
-    hipLaunchKernelGGL(roi_offsets_kernel, dim3((unsigned)((waves * 64 + 255) / 256)), dim3(256), 0, stream, a, flag,
-                       bbase);
+    hipLaunchKernelGGL(frame_counts_kernel, dim3((unsigned)((waves * 64 + 255) / 256)), dim3(256), 0, stream, fc);
+    return hipGetLastError();
+}
+
+size_t drink_workspace_bytes(int32_t total) {
+    const size_t nb = total > 0 ? ((size_t)total + kRBlock - 1) / kRBlock : 0;
+    return (((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255);
+}
+
+hipError_t launch_drinkers(const DrinkArgs &a, void *workspace, hipStream_t stream) {
+    const int nb = (int)(((long long)a.total + kRBlock - 1) / kRBlock);
+    int32_t *bcount = static_cast<int32_t *>(workspace);
+    int32_t *bbase = bcount + nb;
+    if (nb > 0) hipLaunchKernelGGL(drink_flag_kernel, dim3((unsigned)nb), dim3(kRThreadsR), 0, stream, a, bcount);
+    hipLaunchKernelGGL(roi_scan_kernel, dim3(1), dim3(1024), 0, stream, bcount, bbase, nb);
+    const FrameCounts fc{a.drinking, bbase, a.offsets, a.n_frames, a.total, a.counts, nullptr};
+    const long long waves = (long long)a.n_frames + 1;
+    hipLaunchKernelGGL(frame_counts_kernel, dim3((unsigned)((waves * 64 + 255) / 256)), dim3(256), 0, stream, fc);
     return hipGetLastError();
 }
 

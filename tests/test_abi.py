@@ -134,7 +134,37 @@ def test_roi_rejects_bad_arguments(kwargs, needle):
     assert needle in binding.lib().flock_last_error().decode()
 
 
+LINES = (ctypes.c_int32 * 8)(0, 0, 160, 0, 0, 0, 0, 160)
+FAR_LINE = (ctypes.c_int32 * 4)(0, 0, -(1 << 25), 0)
+
+
+def _drink(n_frames=1, total=4, lines=LINES, nl=2, thr=64, xy=FAKE, offsets=FAKE, drinking=FAKE, line=FAKE,
+           counts=FAKE):
+    return binding.lib().drinker_proximity_frames(xy, offsets, n_frames, total, lines, nl, thr, drinking, line,
+                                                  counts, None, 0, None)
+
+
+@pytest.mark.parametrize("kwargs,needle", [
+    (dict(n_frames=-1), "n_frames"),
+    (dict(total=-1), "total"),
+    (dict(nl=0), "n_lines"),
+    (dict(nl=65), "n_lines"),
+    (dict(lines=None), "lines"),
+    (dict(lines=FAR_LINE, nl=1), "2^24"),
+    (dict(thr=-1), "threshold_q"),
+    (dict(thr=(1 << 24) + 1), "threshold_q"),
+    (dict(offsets=None), "non-NULL"),
+    (dict(drinking=None), "non-NULL"),
+    (dict(drinking=FAKE4), "16-byte"),
+    (dict(xy=FAKE4), "aligned"),
+])
+def test_drinkers_rejects_bad_arguments(kwargs, needle):
+    assert _drink(**kwargs) == binding.FLOCK_EINVAL
+    assert needle in binding.lib().flock_last_error().decode()
+
+
 def test_empty_batches_are_noops_without_a_device():
+    assert _drink(n_frames=0, total=0, xy=None, offsets=None, drinking=None, line=None, counts=None) == 0
     assert _roi(n_frames=0, total=0, xy=None, offsets=None, counts=None, oxy=None, ooff=None, oidx=None) == 0
     assert _heatmap(n_frames=0, dens=None, labels=None, ncomp=None, ent=None, deg=None, cells=None,
                     mass=None) == 0
@@ -151,6 +181,8 @@ def test_workspace_queries():
     assert lib.heatmap_frames_workspace(0, 128, 72) == 0
     assert lib.roi_filter_frames_workspace(64, 128000) >= 128000
     assert lib.roi_filter_frames_workspace(0, 0) == 0
+    assert lib.drinker_proximity_frames_workspace(64, 128000) > 0
+    assert lib.drinker_proximity_frames_workspace(0, 0) == 0
 
 
 def test_eps_to_quanta():

@@ -79,7 +79,8 @@ MUTANTS = [
      ROI_PINS),
     ("roi_axes_swapped", "if (!oracle_point_in_polygon(poly, n_vertices, xy[2 * i], xy[2 * i + 1])) continue;",
      "if (!oracle_point_in_polygon(poly, n_vertices, xy[2 * i + 1], xy[2 * i])) continue;", ROI_PINS),
-    ("roi_counts_cumulative", "counts[f] = c;", "counts[f] = k;", ROI_PINS),
+    ("roi_counts_cumulative", "counts[f] = c;\n        out_offsets[f + 1] = k;",
+     "counts[f] = k;\n        out_offsets[f + 1] = k;", ROI_PINS),
     ("drink_at_threshold", "if (len2 == 0 || dot <= 0) return wx * wx + wy * wy < t2;",
      "if (len2 == 0 || dot <= 0) return wx * wx + wy * wy <= t2;", DRINK_PINS),
     ("drink_no_clamp_a", "if (len2 == 0 || dot <= 0) return wx * wx + wy * wy < t2;",
