@@ -11,8 +11,9 @@ paper's connected-component clustering (Section 2.3), the direct-sum
 Gaussian density grid of Algorithm 1 (Section 3.6), and the heatmap
 analytics of Section 2.3 and Algorithm 1 (threshold, connected components of
 grid cells, entropy, clustering degree), region-of-interest filtering with
-per-frame region counts (Section 2.2, Algorithm 1), and drinker-line
-proximity (Section 2.3).
+per-frame region counts (Section 2.2, Algorithm 1), drinker-line proximity
+(Section 2.3), and the detection post-processing of Section 3.2 (mask
+components with area, box and centroid).
 """
 
 from __future__ import annotations
@@ -77,6 +78,9 @@ def _load():
         lib.oracle_near_segment.restype = i32
         lib.oracle_drinkers.argtypes = [p, p, i32, p, i32, i32, p, p, p]
         lib.oracle_drinkers.restype = i32
+        lib.oracle_mask_components.argtypes = [p, i32, i32, i32, ctypes.c_float, i32, p, p, p, ctypes.c_int64,
+                                               p, p, p, p, p, p]
+        lib.oracle_mask_components.restype = ctypes.c_int64
         _lib = lib
     return _lib
 
@@ -255,3 +259,37 @@ def drinkers(xy, offsets, lines, t: int):
                                 _ptr(line), _ptr(counts))
     _check(r, "drinkers")
     return {"drinking": drinking, "line": line, "counts": counts}
+
+
+def mask_components(prob, threshold: float, connectivity: int = 8):
+    """Connected components of prob > threshold in float32 masks [F, H, W].
+
+    Returns a dict: labels int32[F, H, W] (first pixel of the component in
+    raster order, -1 background), n_components int32[F], offsets int64[F + 1]
+    (CSR of the component list), label int32[K], area int32[K],
+    box int32[K, 4] (x, y, width, height), centroid float64[K, 2],
+    xy int32[K, 2] (centroid in 1/16 px, floor(16 * sum / area)),
+    score float32[K] (largest probability in the component).
+    """
+    p = np.ascontiguousarray(np.asarray(prob, dtype=np.float32))
+    if p.ndim != 3:
+        raise ValueError("prob must be [F, H, W]")
+    F, h, w = p.shape
+    labels = np.zeros(p.shape, np.int32)
+    ncomp = np.zeros(F, np.int32)
+    offs = np.zeros(F + 1, np.int64)
+    cap = int(p.size)
+    lab = np.zeros(cap, np.int32)
+    area = np.zeros(cap, np.int32)
+    box = np.zeros((cap, 4), np.int32)
+    cen = np.zeros((cap, 2), np.float64)
+    qxy = np.zeros((cap, 2), np.int32)
+    score = np.zeros(cap, np.float32)
+    k = _load().oracle_mask_components(_ptr(p), F, w, h, float(threshold), int(connectivity), _ptr(labels),
+                                       _ptr(ncomp), _ptr(offs), cap, _ptr(lab), _ptr(area), _ptr(box), _ptr(cen),
+                                       _ptr(qxy), _ptr(score))
+    _check(int(k), "mask_components")
+    k = int(k)
+    return {"labels": labels, "n_components": ncomp, "offsets": offs, "label": lab[:k].copy(),
+            "area": area[:k].copy(), "box": box[:k].copy(), "centroid": cen[:k].copy(),
+            "xy": qxy[:k].copy(), "score": score[:k].copy()}

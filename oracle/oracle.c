@@ -83,6 +83,21 @@
  *     is exact: squared distances to end points in int64, and for a point
  *     projecting inside the segment cross^2 < T^2 |b - a|^2 in 128 bits.
  *
+ *  6. Detection post-processing (Section 3.2: the segmentation output is
+ *     thresholded and grouped into connected regions with their statistics,
+ *     replacing skimage.regionprops by OpenCV's connectedComponentsWithStats).
+ *     Reading: a pixel is foreground when its probability is strictly above
+ *     the threshold; components are connected foreground pixels under the
+ *     4- or 8-neighbourhood, labelled by their first pixel in raster order
+ *     (smallest index y * W + x), background -1; components are listed per
+ *     frame in label order with area (pixels), bounding box (x, y, width,
+ *     height) and centroid (mean x, mean y of the pixel indices, as the
+ *     OpenCV routine reports it), the centroid in 1/16 px rounded down (the
+ *     position layout of the clustering input), and a confidence score, the
+ *     largest probability among the component's pixels (Section 2.3 gives
+ *     boxes confidence scores without saying how; this is a reading).  The
+ *     threshold is finite and >= 0 (the output is a probability).
+ *
  * Threads only split independent work items (whole frames for clustering
  * and heatmaps, whole grid rows for density); each item is computed exactly
  * as above.
@@ -634,4 +649,89 @@ int32_t oracle_drinkers(const int32_t *xy, const int32_t *offsets, int32_t n_fra
         counts[f] = c;
     }
     return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Detection post-processing: mask components with statistics              */
+/* ------------------------------------------------------------------------ */
+
+/* prob: [n_frames][h][w] fp32.  labels: [n_frames][h][w].  Components of
+ * all frames are listed frame after frame: comp_offsets[n_frames + 1];
+ * per component (up to capacity; the count is returned): label (frame
+ * pixel index), area, box (x, y, width, height), centroid (x, y), the
+ * centroid in 1/16 px as floor(16 * sum / area) in integers (the position
+ * layout the clustering consumes), and score, the largest probability of
+ * its pixels.  threshold must be finite and >= 0. */
+int64_t oracle_mask_components(const float *prob, int32_t n_frames, int32_t w, int32_t h, float threshold,
+                               int32_t connectivity, int32_t *labels, int32_t *n_components,
+                               int64_t *comp_offsets, int64_t capacity, int32_t *comp_label,
+                               int32_t *comp_area, int32_t *comp_box, double *comp_centroid, int32_t *comp_xy,
+                               float *comp_score)
+{
+    if (n_frames < 0 || w < 1 || h < 1 || (connectivity != 4 && connectivity != 8)) return ORACLE_EINVAL;
+    if (!(threshold >= 0.0f) || isinf(threshold)) return ORACLE_EINVAL;
+    const int64_t px = (int64_t)w * h;
+    int64_t *queue = (int64_t *)malloc((size_t)px * sizeof(int64_t));
+    if (!queue) return ORACLE_ENOMEM;
+    int64_t k = 0;
+    comp_offsets[0] = 0;
+    for (int32_t f = 0; f < n_frames; ++f) {
+        const float *P = prob + f * px;
+        int32_t *L = labels + f * px;
+        for (int64_t c = 0; c < px; ++c) L[c] = -1;
+        int32_t nc = 0;
+        /* seeds in raster order: each component is found first at its
+         * smallest pixel index, which becomes its label */
+        for (int64_t seed = 0; seed < px; ++seed) {
+            if (!(P[seed] > threshold) || L[seed] >= 0) continue;
+            int64_t head = 0, tail = 0, area = 0, sx = 0, sy = 0;
+            int32_t x0 = w, y0 = h, x1 = -1, y1 = -1;
+            float best = P[seed];
+            queue[tail++] = seed;
+            L[seed] = (int32_t)seed;
+            while (head < tail) {
+                const int64_t c = queue[head++];
+                const int32_t cx = (int32_t)(c % w), cy = (int32_t)(c / w);
+                ++area;
+                sx += cx;
+                sy += cy;
+                if (cx < x0) x0 = cx;
+                if (cx > x1) x1 = cx;
+                if (cy < y0) y0 = cy;
+                if (cy > y1) y1 = cy;
+                if (P[c] > best) best = P[c];
+                for (int32_t dy = -1; dy <= 1; ++dy)
+                    for (int32_t dx = -1; dx <= 1; ++dx) {
+                        if (dx == 0 && dy == 0) continue;
+                        if (connectivity == 4 && dx * dy != 0) continue;
+                        const int32_t nx = cx + dx, ny = cy + dy;
+                        if (nx < 0 || nx >= w || ny < 0 || ny >= h) continue;
+                        const int64_t n = (int64_t)ny * w + nx;
+                        if (P[n] > threshold && L[n] < 0) {
+                            L[n] = (int32_t)seed;
+                            queue[tail++] = n;
+                        }
+                    }
+            }
+            if (k < capacity) {
+                comp_label[k] = (int32_t)seed;
+                comp_area[k] = (int32_t)area;
+                comp_box[4 * k] = x0;
+                comp_box[4 * k + 1] = y0;
+                comp_box[4 * k + 2] = x1 - x0 + 1;
+                comp_box[4 * k + 3] = y1 - y0 + 1;
+                comp_centroid[2 * k] = (double)sx / (double)area;
+                comp_centroid[2 * k + 1] = (double)sy / (double)area;
+                comp_xy[2 * k] = (int32_t)((16 * sx) / area);
+                comp_xy[2 * k + 1] = (int32_t)((16 * sy) / area);
+                comp_score[k] = best;
+            }
+            ++k;
+            ++nc;
+        }
+        n_components[f] = nc;
+        comp_offsets[f + 1] = k;
+    }
+    free(queue);
+    return k;
 }

@@ -19,6 +19,7 @@ KDE_PINS = "tests/test_oracle_kde.py"
 HEAT_PINS = "tests/test_oracle_heatmap.py"
 ROI_PINS = "tests/test_oracle_roi.py"
 DRINK_PINS = "tests/test_oracle_drinkers.py"
+MASK_PINS = "tests/test_oracle_mask.py"
 
 MUTANTS = [
     # (name, old text, new text, which pin file must fail)
@@ -92,6 +93,20 @@ MUTANTS = [
      DRINK_PINS),
     ("drink_dy_from_x", "const int64_t wx = (int64_t)px - ax, wy = (int64_t)py - ay;",
      "const int64_t wx = (int64_t)px - ax, wy = (int64_t)py - ax;", DRINK_PINS),
+    ("mask_threshold_inclusive", "if (!(P[seed] > threshold) || L[seed] >= 0) continue;",
+     "if (!(P[seed] >= threshold) || L[seed] >= 0) continue;", MASK_PINS),
+    ("mask_4_as_8", "if (connectivity == 4 && dx * dy != 0) continue;", "", MASK_PINS),
+    ("mask_seeds_descending", "for (int64_t seed = 0; seed < px; ++seed) {",
+     "for (int64_t seed = px - 1; seed >= 0; --seed) {", MASK_PINS),
+    ("mask_box_width_exclusive", "comp_box[4 * k + 2] = x1 - x0 + 1;", "comp_box[4 * k + 2] = x1 - x0;", MASK_PINS),
+    ("mask_box_height_from_x", "comp_box[4 * k + 3] = y1 - y0 + 1;", "comp_box[4 * k + 3] = x1 - x0 + 1;",
+     MASK_PINS),
+    ("mask_centroid_y_from_x", "comp_centroid[2 * k + 1] = (double)sy / (double)area;",
+     "comp_centroid[2 * k + 1] = (double)sx / (double)area;", MASK_PINS),
+    ("mask_xy_rounded", "comp_xy[2 * k + 1] = (int32_t)((16 * sy) / area);",
+     "comp_xy[2 * k + 1] = (int32_t)((16 * sy + area / 2) / area);", MASK_PINS),
+    ("mask_score_of_seed", "if (P[c] > best) best = P[c];", "", MASK_PINS),
+    ("mask_offsets_per_frame", "comp_offsets[f + 1] = k;", "comp_offsets[f + 1] = nc;", MASK_PINS),
 ]
 
 
