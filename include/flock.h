@@ -258,6 +258,61 @@ flock_status drinker_proximity_frames(const int32_t *xy, const int32_t *offsets,
 /* Bytes of workspace drinker_proximity_frames needs for this batch. */
 size_t drinker_proximity_frames_workspace(int32_t n_frames, int32_t total);
 
+/*
+ * mask_components_frames - detection post-processing of a batch of
+ * segmentation outputs.
+ *
+ * Section 3.2 turns the segmentation network's output into detections with
+ * a connected-components-with-statistics routine (threshold, connected
+ * components, bounding boxes; Section 2.3 gives each box a confidence
+ * score).  Per frame f and pixel p = y * width + x:
+ *   foreground   prob[f][p] > threshold (NaN is background);
+ *   labels       connected foreground pixels under the 4-neighbourhood
+ *                (shared edge) or the 8-neighbourhood (shared edge or corner)
+ *                form a component, labelled by its first pixel in raster
+ *                order (smallest p); background gets -1;
+ *   components   listed frame after frame, in label order within a frame:
+ *                label, area (pixels), box (x, y, width, height), centroid
+ *                (mean x, mean y of the pixel indices, correctly rounded
+ *                quotient of exact integer sums), xy = floor(16 sum / area)
+ *                per axis (the centroid in the 1/16-px layout of
+ *                cluster_frames, with comp_offsets as its offsets), and score
+ *                (largest probability among the component's pixels).
+ *
+ * Arguments:
+ *   prob            device in, float[n_frames][height][width].
+ *   width, height   1 .. 32768 each; n_frames * width * height < 2^31.
+ *   threshold       finite and >= 0.
+ *   connectivity    4 or 8.
+ *   labels          device out, int32[n_frames][height][width], or NULL.
+ *   n_components    device out, int32[n_frames].
+ *   comp_offsets    device out, int32[n_frames + 1]: CSR offsets of the
+ *                   component list; comp_offsets[n_frames] is the count K.
+ *   capacity        rows of the component outputs; components with rank
+ *                   >= capacity are counted but not written.
+ *   comp_label, comp_area   device out, int32[capacity], or NULL.
+ *   comp_box        device out, int32[capacity][4], 16-byte aligned, or NULL.
+ *   comp_centroid   device out, double[capacity][2], 16-byte aligned, or NULL.
+ *   comp_xy         device out, int32[capacity][2], 8-byte aligned, or NULL.
+ *   comp_score      device out, float[capacity], or NULL.
+ *   workspace       as for cluster_frames, sized by
+ *                   mask_components_frames_workspace.
+ * Every output is deterministic: statistics are integer sums, minima and
+ * maxima, so their order of accumulation does not matter.
+ */
+flock_status mask_components_frames(const float *prob, int32_t n_frames, int32_t width, int32_t height,
+                                    float threshold, int32_t connectivity, int32_t *labels,
+                                    int32_t *n_components, int32_t *comp_offsets, int32_t capacity,
+                                    int32_t *comp_label, int32_t *comp_area, int32_t *comp_box,
+                                    double *comp_centroid, int32_t *comp_xy, float *comp_score,
+                                    void *workspace, size_t workspace_bytes, void *stream);
+
+/* Bytes of workspace mask_components_frames needs for this batch shape: 56
+ * bytes per possible piece of a component inside a 64 x 64 tile (a quarter
+ * of the pixels with 8 neighbours, half with 4), plus the tile seams and a
+ * bit per pixel. */
+size_t mask_components_frames_workspace(int32_t n_frames, int32_t width, int32_t height, int32_t connectivity);
+
 /* Text of the last error on this thread ("" if none); valid until the next
  * library call on this thread. */
 const char *flock_last_error(void);

@@ -63,6 +63,11 @@ def lib() -> ctypes.CDLL:
         L.drinker_proximity_frames.restype = i32
         L.drinker_proximity_frames_workspace.argtypes = [i32, i32]
         L.drinker_proximity_frames_workspace.restype = sz
+        L.mask_components_frames.argtypes = [p, i32, i32, i32, ctypes.c_float, i32, p, p, p, i32,
+                                             p, p, p, p, p, p, p, sz, p]
+        L.mask_components_frames.restype = i32
+        L.mask_components_frames_workspace.argtypes = [i32, i32, i32, i32]
+        L.mask_components_frames_workspace.restype = sz
         L.flock_last_error.argtypes = []
         L.flock_last_error.restype = ctypes.c_char_p
         L.flock_version.argtypes = []
@@ -252,6 +257,56 @@ def drinker_proximity_frames(xy: torch.Tensor, offsets: torch.Tensor, lines, thr
                                             ln.shape[0], int(threshold_q), _ptr(out["drinking"]),
                                             _ptr(out.get("line")), _ptr(out["counts"]), _ptr(ws), ws_bytes,
                                             _stream(stream))
+    _check(st)
+    return out
+
+
+def mask_capacity(n_frames: int, height: int, width: int, connectivity: int = 8) -> int:
+    """Most components a batch of this shape can hold (isolated pixels on
+    every other row and column with 8 neighbours, a checkerboard with 4)."""
+    if connectivity == 8:
+        return n_frames * ((height + 1) // 2) * ((width + 1) // 2)
+    return n_frames * ((height * width + 1) // 2)
+
+
+def mask_components_frames(prob: torch.Tensor, threshold: float, connectivity: int = 8, with_labels: bool = True,
+                           capacity: int | None = None, out=None, stream=None):
+    """Connected components of prob > threshold in float32 device masks
+    [F, H, W], with statistics (the detection post-processing).
+
+    Returns a dict of device tensors: labels int32[F, H, W] (first pixel of
+    the component in raster order, -1 background) or None, n_components
+    int32[F], offsets int32[F + 1] (offsets[F] = number of components K),
+    and per component, in rows 0 .. min(K, capacity) - 1: label int32[C],
+    area int32[C], box int32[C, 4] (x, y, width, height), centroid
+    float64[C, 2], xy int32[C, 2] (1/16 px), score float32[C].  capacity
+    defaults to the most components the shape can hold.
+    """
+    if not prob.is_cuda or prob.dtype != torch.float32 or prob.dim() != 3 or not prob.is_contiguous():
+        raise ValueError("prob must be a contiguous float32 device tensor [F, H, W]")
+    F, H, W = prob.shape
+    dev = prob.device
+    if capacity is None:
+        capacity = mask_capacity(F, H, W, connectivity)
+    C = int(capacity)
+    if out is None:
+        out = {"labels": torch.empty((F, H, W), dtype=torch.int32, device=dev) if with_labels else None,
+               "n_components": torch.empty(F, dtype=torch.int32, device=dev),
+               "offsets": torch.empty(F + 1, dtype=torch.int32, device=dev),
+               "label": torch.empty(C, dtype=torch.int32, device=dev),
+               "area": torch.empty(C, dtype=torch.int32, device=dev),
+               "box": torch.empty((C, 4), dtype=torch.int32, device=dev),
+               "centroid": torch.empty((C, 2), dtype=torch.float64, device=dev),
+               "xy": torch.empty((C, 2), dtype=torch.int32, device=dev),
+               "score": torch.empty(C, dtype=torch.float32, device=dev)}
+    ws_bytes = lib().mask_components_frames_workspace(F, W, H, int(connectivity))
+    ws = _workspace(ws_bytes, dev, stream)
+    with torch.cuda.device(dev):
+        st = lib().mask_components_frames(_ptr(prob), F, W, H, float(threshold), int(connectivity),
+                                          _ptr(out.get("labels")), _ptr(out["n_components"]), _ptr(out["offsets"]),
+                                          C, _ptr(out.get("label")), _ptr(out.get("area")), _ptr(out.get("box")),
+                                          _ptr(out.get("centroid")), _ptr(out.get("xy")), _ptr(out.get("score")),
+                                          _ptr(ws), ws_bytes, _stream(stream))
     _check(st)
     return out
 

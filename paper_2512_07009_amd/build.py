@@ -15,7 +15,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libflock.so")
-SOURCES = ["api.cpp", "cluster.hip", "cluster_big.hip", "density.hip", "heatmap.hip", "roi.hip"]
+SOURCES = ["api.cpp", "cluster.hip", "cluster_big.hip", "density.hip", "heatmap.hip", "roi.hip", "mask.hip"]
 ARCH = "gfx950"
 
 

@@ -559,4 +559,77 @@ flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid
     return FLOCK_OK;
 }
 
+size_t mask_components_frames_workspace(int32_t n_frames, int32_t width, int32_t height, int32_t connectivity) {
+    g_error.clear();
+    return flock::mask_workspace_bytes(n_frames, width, height, connectivity);
+}
+
+flock_status mask_components_frames(const float *prob, int32_t n_frames, int32_t width, int32_t height,
+                                    float threshold, int32_t connectivity, int32_t *labels,
+                                    int32_t *n_components, int32_t *comp_offsets, int32_t capacity,
+                                    int32_t *comp_label, int32_t *comp_area, int32_t *comp_box,
+                                    double *comp_centroid, int32_t *comp_xy, float *comp_score, void *workspace,
+                                    size_t workspace_bytes, void *stream) {
+    g_error.clear();
+    if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
+    if (width < 1 || height < 1 || width > 32768 || height > 32768)
+        return fail(FLOCK_EINVAL, "frame %d x %d outside 1..32768", width, height);
+    if (!std::isfinite(threshold) || !(threshold >= 0.0f))
+        return fail(FLOCK_EINVAL, "threshold must be finite and >= 0");
+    if (connectivity != 4 && connectivity != 8)
+        return fail(FLOCK_EINVAL, "connectivity = %d, expected 4 or 8", connectivity);
+    if (capacity < 0) return fail(FLOCK_EINVAL, "capacity = %d < 0", capacity);
+    if ((long long)n_frames * width * height > 0x7fffffffLL)
+        return fail(FLOCK_EUNSUPPORTED, "batch of %lld pixels above 2^31 - 1",
+                    (long long)n_frames * width * height);
+    if (n_frames == 0) return FLOCK_OK;
+    if (!prob || !n_components || !comp_offsets)
+        return fail(FLOCK_EINVAL, "prob, n_components and comp_offsets must be non-NULL");
+    if (!aligned(prob, 4) || !aligned(labels, 4) || !aligned(n_components, 4) || !aligned(comp_offsets, 4) ||
+        !aligned(comp_label, 4) || !aligned(comp_area, 4) || !aligned(comp_score, 4))
+        return fail(FLOCK_EINVAL, "prob, labels, n_components, comp_offsets, comp_label, comp_area and "
+                                  "comp_score must be 4-byte aligned");
+    if (!aligned(comp_box, 16) || !aligned(comp_centroid, 16) || !aligned(comp_xy, 8))
+        return fail(FLOCK_EINVAL, "comp_box and comp_centroid must be 16-byte aligned, comp_xy 8-byte aligned");
+
+    const DeviceInfo *dev = nullptr;
+    flock_status st = device_info(&dev);
+    if (st != FLOCK_OK) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const size_t need = flock::mask_workspace_bytes(n_frames, width, height, connectivity);
+    if (workspace && workspace_bytes < need)
+        return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
+    if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
+    void *ws = workspace;
+    hipError_t err = hipSuccess;
+    if (!ws) {
+        err = hipMallocAsync(&ws, need, s);
+        if (err != hipSuccess) return hip_fail(err, "workspace allocation");
+    }
+    flock::MaskArgs a{};
+    a.prob = prob;
+    a.n_frames = n_frames;
+    a.width = width;
+    a.height = height;
+    a.threshold = threshold;
+    a.connectivity = connectivity;
+    a.labels = labels;
+    a.n_components = n_components;
+    a.comp_offsets = comp_offsets;
+    a.capacity = capacity;
+    a.comp_label = comp_label;
+    a.comp_area = comp_area;
+    a.comp_box = comp_box;
+    a.comp_centroid = comp_centroid;
+    a.comp_xy = comp_xy;
+    a.comp_score = comp_score;
+    err = flock::launch_mask(a, ws, s);
+    if (!workspace) {
+        const hipError_t ferr = hipFreeAsync(ws, s);
+        if (err == hipSuccess) err = ferr;
+    }
+    if (err != hipSuccess) return hip_fail(err, "mask component kernels");
+    return FLOCK_OK;
+}
+
 }  // extern "C"

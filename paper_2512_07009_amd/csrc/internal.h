@@ -153,4 +153,27 @@ struct DrinkArgs {
 size_t drink_workspace_bytes(int32_t total);
 hipError_t launch_drinkers(const DrinkArgs &a, void *workspace, hipStream_t stream);
 
+// Detection post-processing (mask components with statistics)
+constexpr int kMaskTile = 64;  // tile side in pixels
+
+struct MaskArgs {
+    const float *prob;         // [n_frames][height][width]
+    int32_t n_frames, width, height;
+    float threshold;
+    int32_t connectivity;
+    int32_t tiles_x, tiles_y;  // set by launch_mask
+    int64_t n_tiles;
+    int64_t frame_slots, band_slots;
+    int32_t *labels;           // optional
+    int32_t *n_components;     // [n_frames]
+    int32_t *comp_offsets;     // [n_frames + 1]
+    int64_t capacity;
+    int32_t *comp_label, *comp_area, *comp_box;  // each optional
+    double *comp_centroid;
+    int32_t *comp_xy;
+    float *comp_score;
+};
+size_t mask_workspace_bytes(int32_t n_frames, int32_t width, int32_t height, int32_t connectivity);
+hipError_t launch_mask(MaskArgs a, void *workspace, hipStream_t stream);
+
 }  // namespace flock

@@ -238,3 +238,94 @@ def heat_grids(seed: int, n_frames: int, grid_h: int, grid_w: int, n_blobs: int 
             g += amp * np.maximum(0.0, 1.0 - np.hypot(gx - cx, gy - cy) / rad)
         out[f] = g.astype(np.float32)
     return out
+
+
+@dataclass(frozen=True)
+class MaskWorkload:
+    """One synthetic batch of segmentation outputs for the detection
+    post-processing: per-pixel bird probabilities, float32 [F, H, W]."""
+
+    name: str
+    seed: int
+    n_frames: int
+    width_px: int
+    height_px: int
+    n_birds: int
+    threshold: float
+    connectivity: int
+    recipe: str
+
+    def as_dict(self) -> dict:
+        return asdict(self)
+
+
+MASK_WORKLOADS: dict[str, MaskWorkload] = {
+    w.name: w
+    for w in [
+        MaskWorkload("masks8x2000_720p", 2001, 8, 1280, 720, 2000, 0.5, 8,
+                     "batch of 8 frames at 1280x720, 2000 elliptical birds per frame "
+                     "(6-component mixture + 10% uniform), speckle false positives"),
+        MaskWorkload("masks8x2000_1080p", 2002, 8, 1920, 1080, 2000, 0.5, 8,
+                     "batch of 8 frames at 1920x1080, 2000 elliptical birds per frame "
+                     "(6-component mixture + 10% uniform), speckle false positives"),
+    ]
+}
+
+
+def bird_masks(seed: int, n_frames: int, height_px: int, width_px: int, n_birds: int,
+               major_px: tuple = (7.0, 10.0), minor_px: tuple = (4.0, 6.0),
+               speckle_frac: float = 2e-4, empty_frac: float = 0.0) -> np.ndarray:
+    """Seeded probability maps float32[F, H, W] shaped like a segmentation
+    network's bird output: a faint background in [0, 0.1), one soft ellipse
+    per bird (random orientation, semi-axes drawn from major_px and minor_px,
+    value 1 at the centre falling below 0.5 a little outside the nominal
+    ellipse; overlapping birds keep the larger value), birds placed by a
+    6-component Gaussian mixture (std 80-200 px at 1920 px width, scaled with
+    the width) plus 10% uniform, and isolated speckle pixels in [0.5, 1)
+    (single-pixel false positives).  Frames drawn empty (background only)
+    with probability empty_frac."""
+    rng = np.random.default_rng(seed)
+    H, W = int(height_px), int(width_px)
+    out = np.empty((n_frames, H, W), np.float32)
+    scale = W / 1920.0
+    for f in range(n_frames):
+        g = rng.random((H, W), dtype=np.float32) * np.float32(0.1)
+        if rng.random() < empty_frac or n_birds <= 0:
+            out[f] = g
+            continue
+        n_mix = int(round(0.9 * n_birds))
+        x1, y1 = _mixture(rng, n_mix, W, H, 6, 80.0 * scale, 200.0 * scale)
+        x2, y2 = _uniform(rng, n_birds - n_mix, W, H)
+        xs, ys = np.concatenate([x1, x2]), np.concatenate([y1, y2])
+        maj = rng.uniform(*major_px, n_birds)
+        mnr = rng.uniform(*minor_px, n_birds)
+        th = rng.uniform(0.0, np.pi, n_birds)
+        for cx, cy, a, b, t in zip(xs, ys, maj, mnr, th):
+            r = int(np.ceil(1.1 * a)) + 1
+            xa, xb = max(0, int(cx) - r), min(W, int(cx) + r + 1)
+            ya, yb = max(0, int(cy) - r), min(H, int(cy) + r + 1)
+            if xa >= xb or ya >= yb:
+                continue
+            yy, xx = np.mgrid[ya:yb, xa:xb]
+            dx, dy = xx + 0.5 - cx, yy + 0.5 - cy
+            u = dx * np.cos(t) + dy * np.sin(t)
+            v = -dx * np.sin(t) + dy * np.cos(t)
+            p = np.clip(1.15 - 0.6 * ((u / a) ** 2 + (v / b) ** 2), 0.0, 1.0).astype(np.float32)
+            np.maximum(g[ya:yb, xa:xb], p, out=g[ya:yb, xa:xb])
+        k = int(rng.binomial(H * W, speckle_frac))
+        if k:
+            idx = rng.integers(0, H * W, k)
+            g.ravel()[idx] = rng.uniform(0.5, 1.0, k).astype(np.float32)
+        out[f] = g
+    return out
+
+
+def mask_batch(name: str, n_frames: int | None = None):
+    """(prob float32[F, H, W], MaskWorkload) for a named mask workload; the
+    first k frames are the same whatever n_frames asks for."""
+    wl = MASK_WORKLOADS[name]
+    F = wl.n_frames if n_frames is None else min(int(n_frames), wl.n_frames)
+    s = wl.width_px / 1280.0
+    prob = bird_masks(wl.seed, F, wl.height_px, wl.width_px, wl.n_birds,
+                      major_px=(7.0 * s, 10.0 * s), minor_px=(4.0 * s, 6.0 * s))
+    return prob, wl

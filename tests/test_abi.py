@@ -163,7 +163,41 @@ def test_drinkers_rejects_bad_arguments(kwargs, needle):
     assert needle in binding.lib().flock_last_error().decode()
 
 
+def _mask(n_frames=1, w=64, h=48, thr=0.5, conn=8, cap=16, prob=FAKE, labels=FAKE, ncomp=FAKE, offs=FAKE,
+          lab=FAKE, area=FAKE, box=FAKE, cen=FAKE, xy=FAKE, score=FAKE):
+    return binding.lib().mask_components_frames(prob, n_frames, w, h, thr, conn, labels, ncomp, offs, cap, lab, area,
+                                                box, cen, xy, score, None, 0, None)
+
+
+@pytest.mark.parametrize("kwargs,needle", [
+    (dict(n_frames=-1), "n_frames"),
+    (dict(w=0), "frame"),
+    (dict(h=32769), "frame"),
+    (dict(thr=-0.5), "threshold"),
+    (dict(thr=math.nan), "threshold"),
+    (dict(thr=math.inf), "threshold"),
+    (dict(conn=6), "connectivity"),
+    (dict(cap=-1), "capacity"),
+    (dict(prob=None), "non-NULL"),
+    (dict(offs=None), "non-NULL"),
+    (dict(ncomp=None), "non-NULL"),
+    (dict(prob=ctypes.c_void_p(0x100002)), "aligned"),
+    (dict(box=FAKE4), "16-byte"),
+    (dict(cen=FAKE4), "16-byte"),
+    (dict(xy=FAKE4), "8-byte"),
+])
+def test_mask_rejects_bad_arguments(kwargs, needle):
+    assert _mask(**kwargs) == binding.FLOCK_EINVAL
+    assert needle in binding.lib().flock_last_error().decode()
+
+
+def test_mask_rejects_batches_beyond_int32_pixels():
+    assert _mask(n_frames=1024, w=32768, h=32768) == binding.FLOCK_EUNSUPPORTED
+
+
 def test_empty_batches_are_noops_without_a_device():
+    assert _mask(n_frames=0, prob=None, labels=None, ncomp=None, offs=None, lab=None, area=None, box=None, cen=None,
+                 xy=None, score=None) == 0
     assert _drink(n_frames=0, total=0, xy=None, offsets=None, drinking=None, line=None, counts=None) == 0
     assert _roi(n_frames=0, total=0, xy=None, offsets=None, counts=None, oxy=None, ooff=None, oidx=None) == 0
     assert _heatmap(n_frames=0, dens=None, labels=None, ncomp=None, ent=None, deg=None, cells=None,
@@ -183,6 +217,10 @@ def test_workspace_queries():
     assert lib.roi_filter_frames_workspace(0, 0) == 0
     assert lib.drinker_proximity_frames_workspace(64, 128000) > 0
     assert lib.drinker_proximity_frames_workspace(0, 0) == 0
+    # 8 neighbours: a record and a key (56 bytes) per 2 x 2 block of pixels
+    assert lib.mask_components_frames_workspace(8, 1280, 720, 8) >= 56 * 8 * 640 * 360
+    assert lib.mask_components_frames_workspace(8, 1280, 720, 4) >= 56 * 8 * 1280 * 720 // 2
+    assert lib.mask_components_frames_workspace(0, 1280, 720, 8) == 0
 
 
 def test_eps_to_quanta():
