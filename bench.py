@@ -50,6 +50,7 @@ KERNEL_SOURCES = {
     "heatmap": "paper_2512_07009_amd/csrc/heatmap.hip",
     "roi": "paper_2512_07009_amd/csrc/roi.hip",
     "drinker": "paper_2512_07009_amd/csrc/roi.hip",
+    "mask": "paper_2512_07009_amd/csrc/mask.hip",
 }
 
 
@@ -106,6 +107,8 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--mask-workload", default="masks8x2000_720p",
+                    help="segmentation batch for the detection post-processing entry")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=2.0,
                     help="target wall seconds for the oracle sample (all host cores)")
@@ -307,6 +310,34 @@ def main():
     torch.cuda.synchronize(dev)
     t_drink = dev_ev[0].elapsed_time(dev_ev[1]) / K * 1e-3
 
+    # 6. detection post-processing (its own entry point, not part of `value`):
+    #    a batch of segmentation outputs, its own synthetic input
+    prob_np, mw = wl.mask_batch(args.mask_workload)
+    prob = torch.from_numpy(prob_np).to(dev)
+    MF, MH, MW = prob_np.shape
+    mcap = flock.mask_capacity(MF, MH, MW, mw.connectivity)
+    mout = {"labels": torch.empty((MF, MH, MW), dtype=torch.int32, device=dev),
+            "n_components": torch.empty(MF, dtype=torch.int32, device=dev),
+            "offsets": torch.empty(MF + 1, dtype=torch.int32, device=dev),
+            "label": torch.empty(mcap, dtype=torch.int32, device=dev),
+            "area": torch.empty(mcap, dtype=torch.int32, device=dev),
+            "box": torch.empty((mcap, 4), dtype=torch.int32, device=dev),
+            "centroid": torch.empty((mcap, 2), dtype=torch.float64, device=dev),
+            "xy": torch.empty((mcap, 2), dtype=torch.int32, device=dev),
+            "score": torch.empty(mcap, dtype=torch.float32, device=dev)}
+    for _ in range(3):
+        flock.mask_components_frames(prob, mw.threshold, mw.connectivity, capacity=mcap, out=mout, stream=stream)
+    mev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize(dev)
+    mev[0].record(stream)
+    for _ in range(K):
+        flock.mask_components_frames(prob, mw.threshold, mw.connectivity, capacity=mcap, out=mout, stream=stream)
+    mev[1].record(stream)
+    torch.cuda.synchronize(dev)
+    t_mask = mev[0].elapsed_time(mev[1]) / K * 1e-3
+    n_det = int(mout["offsets"][-1].item())
+    del prob, mout
+
     # algorithmic work per launch
     cluster_bytes = 13 * T + 8 * F + 4          # xy 8 + labels 4 + kind 1 per bird; offsets, n_clusters
     density_flops = 2.0 * w.grid_w * w.grid_h * T
@@ -336,6 +367,22 @@ def main():
           "threshold_px": dthr / 16, "in_value": False}
     dr["frac"] = dr["achieved"] / dr["peak"]
     dr["traffic"] = committed_traffic("drinker", w.name)
+    mpx = MF * MH * MW
+    # prob in and labels out per pixel; 52 B per component (label, area, box,
+    # centroid, 1/16-px centroid, score); counts and offsets per frame
+    mask_bytes = 8 * mpx + 52 * n_det + 8 * MF + 4
+    ma = {"bound": "hbm", "achieved": mask_bytes / t_mask / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+          "per_launch_us": t_mask * 1e6, "algorithmic_bytes": mask_bytes, "workload": mw.name,
+          "frames": MF, "frame_px": [MW, MH], "components": n_det, "threshold": mw.threshold,
+          "connectivity": mw.connectivity, "frames_per_s": MF / t_mask, "in_value": False}
+    ma["frac"] = ma["achieved"] / ma["peak"]
+    ma["traffic"] = committed_traffic("mask", mw.name)
+    if not args.no_cpu_baseline:
+        import oracle
+        t0 = time.perf_counter()
+        oracle.mask_components(prob_np, mw.threshold, mw.connectivity)
+        ma["oracle_frames_per_s"] = MF / (time.perf_counter() - t0)
+        ma["oracle_threads"] = 1
     dominant = ("cluster_frames", cl) if t_cluster >= t_density else ("density_frames", de)
     roof = {k: dominant[1][k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")}
     roof["kernel"] = dominant[0]
@@ -366,7 +413,7 @@ def main():
                                  "kernel durations: HIP events in the eager run of the same mode"),
         "roofline": roof,
         "kernels": {"cluster_frames": cl, "density_frames": de, "heatmap_frames": he, "roi_filter_frames": ro,
-                    "drinker_proximity_frames": dr},
+                    "drinker_proximity_frames": dr, "mask_components_frames": ma},
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")

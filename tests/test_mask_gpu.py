@@ -88,6 +88,21 @@ def test_serpentine_gpu(conn):
 
 
 @pytest.mark.parametrize("conn", [4, 8])
+def test_combs_merged_above_gpu(conn):
+    # teeth in the lower band of tiles joined by a bar in the upper band:
+    # every tooth is a piece of its tile whose component starts in the tile
+    # above (32 such pieces per tile, and 4 with sparser teeth)
+    H, W = 150, 200
+    dense = np.zeros((H, W), np.float32)
+    dense[63, :] = 1.0
+    dense[64:140, ::2] = 1.0
+    sparse = np.zeros((H, W), np.float32)
+    sparse[60:64, 5:190] = 1.0
+    sparse[64:150, ::16] = 1.0
+    check(np.stack([dense, sparse, dense[:, ::-1].copy()]), 0.5, conn, tag="combs")
+
+
+@pytest.mark.parametrize("conn", [4, 8])
 def test_full_and_empty_frames_gpu(conn):
     prob = np.zeros((4, 200, 333), np.float32)
     prob[1] = 1.0
