@@ -149,25 +149,27 @@ def main():
         `side` (or also on the first stream when not concurrent), with the join
         back on the first stream."""
         stream = launch_stream if launch_stream is not None else main_stream
-        ds = side if concurrent else stream
+        sd = side
+        lab_, kind_, ncl_, dens_ = labels, kind, ncl, dens
+        ds = sd if concurrent else stream
         if concurrent:
             fork = torch.cuda.Event()
             fork.record(stream)
-            side.wait_event(fork)
+            sd.wait_event(fork)
         if evs is not None:
             evs[0].record(stream)
-        flock.cluster_frames(dxy, doff, w.eps_px, w.min_pts, max_fp, out=(labels, kind, ncl),
+        flock.cluster_frames(dxy, doff, w.eps_px, w.min_pts, max_fp, out=(lab_, kind_, ncl_),
                              stream=stream)
         if evs is not None:
             evs[1].record(stream)
             evs[2].record(ds)
         flock.density_frames(dxy, doff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
-                             max_fp, out=dens, stream=ds)
+                             max_fp, out=dens_, stream=ds)
         if evs is not None:
             evs[3].record(ds)
         if concurrent:
             join = torch.cuda.Event()
-            join.record(side)
+            join.record(sd)
             stream.wait_event(join)
 
     def timed(concurrent, K):
@@ -192,6 +194,7 @@ def main():
         log(f"calibration copy: {nbytes} bytes read and written")
         del src, dst
 
+    log("warmup")
     for k in range(args.warmup):
         run_pair(k, True)
         run_pair(k, False)
@@ -199,6 +202,7 @@ def main():
     K = args.steps
 
     # 1. graph replays: the two-stream step and the one-stream step
+    log("graph replays, one batch at a time")
     ref = (labels.clone(), kind.clone(), ncl.clone(), dens.clone())
     graph_note = None
     walls = {}
@@ -239,6 +243,7 @@ def main():
             walls = {}
 
     # 2. eager steps with per-kernel events, two streams and one stream
+    log("eager steps with events")
     wall_eager, t_cluster, t_density = timed(True, K)
     wall_seq, t_cluster_seq, t_density_seq = timed(False, K)
     if not walls:
@@ -250,6 +255,7 @@ def main():
     ms_per_step = wall / K * 1e3
     value = F / (wall / K)
 
+    log("heatmap, roi, drinker and mask entries")
     # 3. heatmap analytics of the step's density grids (its own entry point,
     #    not part of `value`): hot cells at twice the frame-average density
     cells = w.grid_w * w.grid_h
