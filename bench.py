@@ -113,6 +113,8 @@ def main():
     ap.add_argument("--cpu-budget-s", type=float, default=2.0,
                     help="target wall seconds for the oracle sample (all host cores)")
     ap.add_argument("--no-graph", action="store_true", help="time `value` from eager launches")
+    ap.add_argument("--flush-mb", type=float, default=512,
+                    help="MiB written before each launch timed for the roofline (0: warm back-to-back launches only)")
     ap.add_argument("--calibrate-copy-mb", type=float, default=0,
                     help="also run one plain device copy of this many MiB (counter scaling)")
     args = ap.parse_args()
@@ -172,17 +174,51 @@ def main():
             join.record(sd)
             stream.wait_event(join)
 
-    def timed(concurrent, K):
+    # a buffer larger than L2 and the 256 MB memory-side cache together:
+    # writing it before a timed launch makes that launch read its inputs from HBM
+    flush = torch.empty(int(args.flush_mb) << 20, dtype=torch.uint8, device=dev) if args.flush_mb > 0 else None
+
+    def evict(k):
+        if flush is not None:
+            flush.fill_(k & 0xff)
+
+    def timed(concurrent, K, cold=False):
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
         torch.cuda.synchronize(dev)
         t0 = time.perf_counter()
         for k in range(K):
+            if cold:
+                evict(k)
             run_pair(k, concurrent, evs[k])
         torch.cuda.synchronize(dev)
         wall = time.perf_counter() - t0
         t_c = sum(e[0].elapsed_time(e[1]) for e in evs) / K * 1e-3   # s per launch
         t_d = sum(e[2].elapsed_time(e[3]) for e in evs) / K * 1e-3
         return wall, t_c, t_d
+
+    def per_launch(fn, K):
+        """Average duration of fn() on the main stream: back to back (warm
+        caches), and each launch after the flush (cold, inputs from HBM)."""
+        for _ in range(3):
+            fn()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize(dev)
+        e[0].record(stream)
+        for _ in range(K):
+            fn()
+        e[1].record(stream)
+        torch.cuda.synchronize(dev)
+        warm = e[0].elapsed_time(e[1]) / K * 1e-3
+        if flush is None:
+            return warm, warm
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
+        for k in range(K):
+            evict(k)
+            evs[k][0].record(stream)
+            fn()
+            evs[k][1].record(stream)
+        torch.cuda.synchronize(dev)
+        return sum(a.elapsed_time(b) for a, b in evs) / K * 1e-3, warm
 
     if args.calibrate_copy_mb > 0:
         # a plain device copy of known size, for scaling HBM byte counters
@@ -244,14 +280,20 @@ def main():
 
     # 2. eager steps with per-kernel events, two streams and one stream
     log("eager steps with events")
-    wall_eager, t_cluster, t_density = timed(True, K)
-    wall_seq, t_cluster_seq, t_density_seq = timed(False, K)
+    wall_eager, w_cluster, w_density = timed(True, K)
+    wall_seq, w_cluster_seq, w_density_seq = timed(False, K)
     if not walls:
         walls = {True: wall_eager, False: wall_seq}
     concurrent = walls[True] <= walls[False]
     wall = walls[concurrent]
     if not concurrent:
-        t_cluster, t_density = t_cluster_seq, t_density_seq
+        w_cluster, w_density = w_cluster_seq, w_density_seq
+    # the roofline's durations: the same mode, each step after the flush
+    if flush is not None:
+        log("eager steps with events after a cache flush")
+        _, t_cluster, t_density = timed(concurrent, K, cold=True)
+    else:
+        t_cluster, t_density = w_cluster, w_density
     ms_per_step = wall / K * 1e3
     value = F / (wall / K)
 
@@ -267,16 +309,7 @@ def main():
             "degree": torch.empty(F, dtype=torch.float64, device=dev),
             "comp_cells": torch.empty((F, w.grid_h, w.grid_w), dtype=torch.int32, device=dev),
             "comp_mass": torch.empty((F, w.grid_h, w.grid_w), dtype=torch.float64, device=dev)}
-    for _ in range(3):
-        flock.heatmap_frames(dens, area, heat_thr, 8, out=hout, stream=stream)
-    hev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize(dev)
-    hev[0].record(stream)
-    for _ in range(K):
-        flock.heatmap_frames(dens, area, heat_thr, 8, out=hout, stream=stream)
-    hev[1].record(stream)
-    torch.cuda.synchronize(dev)
-    t_heat = hev[0].elapsed_time(hev[1]) / K * 1e-3
+    t_heat, t_heat_warm = per_launch(lambda: flock.heatmap_frames(dens, area, heat_thr, 8, out=hout, stream=stream), K)
 
     # 4. region-of-interest filter and counts (its own entry point, not part of
     #    `value`): a strip along the left wall, a five-vertex polygon
@@ -286,16 +319,7 @@ def main():
             "xy": torch.empty((T, 2), dtype=torch.int32, device=dev),
             "offsets": torch.empty(F + 1, dtype=torch.int32, device=dev),
             "index": torch.empty(T, dtype=torch.int32, device=dev)}
-    for _ in range(3):
-        flock.roi_filter_frames(dxy, doff, roi_poly, out=rout, stream=stream)
-    rev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize(dev)
-    rev[0].record(stream)
-    for _ in range(K):
-        flock.roi_filter_frames(dxy, doff, roi_poly, out=rout, stream=stream)
-    rev[1].record(stream)
-    torch.cuda.synchronize(dev)
-    t_roi = rev[0].elapsed_time(rev[1]) / K * 1e-3
+    t_roi, t_roi_warm = per_launch(lambda: flock.roi_filter_frames(dxy, doff, roi_poly, out=rout, stream=stream), K)
     kept = int(rout["offsets"][-1].item())
 
     # 5. drinker-line proximity (its own entry point, not part of `value`): two
@@ -305,16 +329,8 @@ def main():
     dout = {"drinking": torch.empty(T, dtype=torch.uint8, device=dev),
             "line": torch.empty(T, dtype=torch.int32, device=dev),
             "counts": torch.empty(F, dtype=torch.int32, device=dev)}
-    for _ in range(3):
-        flock.drinker_proximity_frames(dxy, doff, dlines, dthr, out=dout, stream=stream)
-    dev_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize(dev)
-    dev_ev[0].record(stream)
-    for _ in range(K):
-        flock.drinker_proximity_frames(dxy, doff, dlines, dthr, out=dout, stream=stream)
-    dev_ev[1].record(stream)
-    torch.cuda.synchronize(dev)
-    t_drink = dev_ev[0].elapsed_time(dev_ev[1]) / K * 1e-3
+    t_drink, t_drink_warm = per_launch(
+        lambda: flock.drinker_proximity_frames(dxy, doff, dlines, dthr, out=dout, stream=stream), K)
 
     # 6. detection post-processing (its own entry point, not part of `value`):
     #    a batch of segmentation outputs, its own synthetic input
@@ -331,16 +347,8 @@ def main():
             "centroid": torch.empty((mcap, 2), dtype=torch.float64, device=dev),
             "xy": torch.empty((mcap, 2), dtype=torch.int32, device=dev),
             "score": torch.empty(mcap, dtype=torch.float32, device=dev)}
-    for _ in range(3):
-        flock.mask_components_frames(prob, mw.threshold, mw.connectivity, capacity=mcap, out=mout, stream=stream)
-    mev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    torch.cuda.synchronize(dev)
-    mev[0].record(stream)
-    for _ in range(K):
-        flock.mask_components_frames(prob, mw.threshold, mw.connectivity, capacity=mcap, out=mout, stream=stream)
-    mev[1].record(stream)
-    torch.cuda.synchronize(dev)
-    t_mask = mev[0].elapsed_time(mev[1]) / K * 1e-3
+    t_mask, t_mask_warm = per_launch(lambda: flock.mask_components_frames(prob, mw.threshold, mw.connectivity, capacity=mcap,
+                                                                   out=mout, stream=stream), K)
     n_det = int(mout["offsets"][-1].item())
     del prob, mout
 
@@ -348,28 +356,32 @@ def main():
     cluster_bytes = 13 * T + 8 * F + 4          # xy 8 + labels 4 + kind 1 per bird; offsets, n_clusters
     density_flops = 2.0 * w.grid_w * w.grid_h * T
     cl = {"bound": "hbm", "achieved": cluster_bytes / t_cluster / 1e9, "peak": HBM_PEAK_GBS,
-          "unit": "GB/s", "per_launch_us": t_cluster * 1e6, "algorithmic_bytes": cluster_bytes}
+          "unit": "GB/s", "per_launch_us": t_cluster * 1e6, "warm_per_launch_us": w_cluster * 1e6,
+          "algorithmic_bytes": cluster_bytes}
     cl["frac"] = cl["achieved"] / cl["peak"]
     cl["traffic"] = committed_traffic("cluster", w.name)
     de = {"bound": "mfma", "achieved": density_flops / t_density / 1e12, "peak": MFMA_F16_PEAK_TFLOPS,
-          "unit": "TFLOP/s", "per_launch_us": t_density * 1e6, "algorithmic_flops": density_flops}
+          "unit": "TFLOP/s", "per_launch_us": t_density * 1e6, "warm_per_launch_us": w_density * 1e6,
+          "algorithmic_flops": density_flops}
     de["frac"] = de["achieved"] / de["peak"]
     de["traffic"] = committed_traffic("density", w.name)
     heat_bytes = 20 * F * cells + 20 * F  # density 4 + labels 4 + cells 4 + mass 8 per cell; 20 B per frame
     he = {"bound": "hbm", "achieved": heat_bytes / t_heat / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-          "per_launch_us": t_heat * 1e6, "algorithmic_bytes": heat_bytes,
+          "per_launch_us": t_heat * 1e6, "warm_per_launch_us": t_heat_warm * 1e6, "algorithmic_bytes": heat_bytes,
           "threshold": heat_thr, "connectivity": 8, "in_value": False}
     he["frac"] = he["achieved"] / he["peak"]
     he["traffic"] = committed_traffic("heatmap", w.name)
     roi_bytes = 8 * T + 12 * kept + 12 * F + 8  # xy in; kept xy + index out; offsets in, counts + offsets out
     ro = {"bound": "hbm", "achieved": roi_bytes / t_roi / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-          "per_launch_us": t_roi * 1e6, "algorithmic_bytes": roi_bytes, "kept_birds": kept,
+          "per_launch_us": t_roi * 1e6, "warm_per_launch_us": t_roi_warm * 1e6, "algorithmic_bytes": roi_bytes,
+          "kept_birds": kept,
           "roi_vertices": len(roi_poly), "in_value": False}
     ro["frac"] = ro["achieved"] / ro["peak"]
     ro["traffic"] = committed_traffic("roi", w.name)
     drink_bytes = 13 * T + 8 * F + 4  # xy in, flag and line out per bird; offsets in, counts out
     dr = {"bound": "hbm", "achieved": drink_bytes / t_drink / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-          "per_launch_us": t_drink * 1e6, "algorithmic_bytes": drink_bytes, "lines": len(dlines),
+          "per_launch_us": t_drink * 1e6, "warm_per_launch_us": t_drink_warm * 1e6, "algorithmic_bytes": drink_bytes,
+          "lines": len(dlines),
           "threshold_px": dthr / 16, "in_value": False}
     dr["frac"] = dr["achieved"] / dr["peak"]
     dr["traffic"] = committed_traffic("drinker", w.name)
@@ -378,7 +390,8 @@ def main():
     # centroid, 1/16-px centroid, score); counts and offsets per frame
     mask_bytes = 8 * mpx + 52 * n_det + 8 * MF + 4
     ma = {"bound": "hbm", "achieved": mask_bytes / t_mask / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-          "per_launch_us": t_mask * 1e6, "algorithmic_bytes": mask_bytes, "workload": mw.name,
+          "per_launch_us": t_mask * 1e6, "warm_per_launch_us": t_mask_warm * 1e6, "algorithmic_bytes": mask_bytes,
+          "workload": mw.name,
           "frames": MF, "frame_px": [MW, MH], "components": n_det, "threshold": mw.threshold,
           "connectivity": mw.connectivity, "frames_per_s": MF / t_mask, "in_value": False}
     ma["frac"] = ma["achieved"] / ma["peak"]
@@ -416,7 +429,10 @@ def main():
         "eager_two_stream_frames_per_s": F / (wall_eager / K),
         "eager_one_stream_frames_per_s": F / (wall_seq / K),
         "timing": graph_note or ("value: HIP graph replay of the faster of the two-stream and one-stream steps; "
-                                 "kernel durations: HIP events in the eager run of the same mode"),
+                                 "kernel durations (per_launch_us, roofline): HIP events around each launch in "
+                                 "an eager run of the same mode, each launch after a write of flush_mb MiB that "
+                                 "evicts L2 and the memory-side cache (warm_per_launch_us: back to back)"),
+        "flush_mb": args.flush_mb,
         "roofline": roof,
         "kernels": {"cluster_frames": cl, "density_frames": de, "heatmap_frames": he, "roi_filter_frames": ro,
                     "drinker_proximity_frames": dr, "mask_components_frames": ma},
