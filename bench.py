@@ -97,8 +97,23 @@ def cpu_baseline(xy, off, w, budget_s: float):
     oracle.density_frames(sxy, soff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
                           n_threads=threads)
     dt = time.perf_counter() - t0
+    # the same oracle on one thread, on at most 8 frames
+    n1 = int(max(1, min(8, n)))
+    sxy1, soff1 = xy[: off[n1]], off[: n1 + 1]
+    t0 = time.perf_counter()
+    oracle.cluster_frames(sxy1, soff1, w.eps_q, w.min_pts, n_threads=1)
+    oracle.density_frames(sxy1, soff1, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px, n_threads=1)
+    dt1 = time.perf_counter() - t0
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {"value": n / dt, "unit": "frames/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {n} of {F} frames of {w.name} (clustering + density), {dt:.1f} s wall"}
+            "sample": f"first {n} of {F} frames of {w.name} (clustering + density), {dt:.1f} s wall",
+            "one_thread_value": n1 / dt1, "one_thread_sample": f"first {n1} frames, {dt1:.1f} s wall",
+            "cpu_model": model}
 
 
 def main():
