@@ -111,6 +111,17 @@ def test_full_and_empty_frames_gpu(conn):
     assert got["n_components"].tolist() == [0, 1, 0, 1]
 
 
+@pytest.mark.parametrize("shape", [(1, 1, 32768), (1, 32768, 1), (2000, 8, 8), (3, 2, 5000)],
+                         ids=["row32768", "col32768", "2000x8x8", "3x2x5000"])
+def test_extreme_shapes_gpu(shape):
+    # the widest and tallest frames the entry point takes, many tiny frames,
+    # and two-row strips (tiles of one partial band)
+    rng = np.random.default_rng(sum(shape))
+    prob = (rng.random(shape) < 0.45).astype(np.float32) * rng.uniform(0.51, 1.0, shape).astype(np.float32)
+    for conn in (4, 8):
+        check(prob, 0.5, conn, tag="extreme")
+
+
 def test_threshold_ties_nan_inf_gpu():
     rng = np.random.default_rng(5)
     prob = rng.choice(np.array([0.5, np.nextafter(np.float32(0.5), np.float32(1)), 0.25, np.nan, np.inf, 0.9],
