@@ -135,8 +135,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(frames shard across GPUs with no collective; see DESIGN.md)", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(frames would shard across GPUs by contiguous ranges, with no collective)", file=sys.stderr)
         sys.exit(2)
 
     import torch
