@@ -70,3 +70,63 @@ def test_graph_replays_match_eager(case):
         torch.cuda.synchronize()
         for got, want, what in zip((labels, kind, ncl, dens), ref, ("labels", "kind", "n_clusters", "density")):
             assert torch.equal(got, want), f"{name}: replay {rep} {what} differs from eager"
+
+
+def test_graph_replays_match_eager_analytics():
+    """heatmap_frames, roi_filter_frames, drinker_proximity_frames and
+    mask_components_frames captured in one graph, replayed several times with
+    eager work in between; every replay equals the eager outputs bit for bit."""
+    dev = torch.device("cuda")
+    xy, off, w = wl.generate("batch64x2000_1080p", n_frames=8)
+    F, T = len(off) - 1, xy.shape[0]
+    dxy, doff = torch.from_numpy(xy).to(dev), torch.from_numpy(off).to(dev)
+    grids = torch.from_numpy(wl.heat_grids(21, 6, 72, 128)).to(dev)
+    prob = torch.from_numpy(wl.bird_masks(22, 3, 200, 300, n_birds=150)).to(dev)
+    Wq, Hq = 16 * w.width_px, 16 * w.height_px
+    poly = [[0, 0], [Wq // 8, 0], [Wq // 6, Hq // 2], [Wq // 8, Hq], [0, Hq]]
+    lines = [[Wq // 10, Hq // 4, 9 * Wq // 10, Hq // 4], [Wq // 10, 3 * Hq // 4, 9 * Wq // 10, 3 * Hq // 4]]
+    cap = flock.mask_capacity(3, 200, 300, 8)
+    e = lambda *shape, dt=torch.int32: torch.empty(*shape, dtype=dt, device=dev)
+    hout = {"labels": e((6, 72, 128)), "n_components": e(6), "entropy": e(6, dt=torch.float64),
+            "degree": e(6, dt=torch.float64), "comp_cells": e((6, 72, 128)),
+            "comp_mass": e((6, 72, 128), dt=torch.float64)}
+    rout = {"counts": e(F), "xy": e((T, 2)), "offsets": e(F + 1), "index": e(T)}
+    dout = {"drinking": e(T, dt=torch.uint8), "line": e(T), "counts": e(F)}
+    mout = {"labels": e((3, 200, 300)), "n_components": e(3), "offsets": e(4), "label": e(cap), "area": e(cap),
+            "box": e((cap, 4)), "centroid": e((cap, 2), dt=torch.float64), "xy": e((cap, 2)),
+            "score": e(cap, dt=torch.float32)}
+    main = torch.cuda.Stream(dev)
+
+    def step():
+        flock.heatmap_frames(grids, 225.0, 2e-4, 8, out=hout, stream=main)
+        flock.roi_filter_frames(dxy, doff, poly, out=rout, stream=main)
+        flock.drinker_proximity_frames(dxy, doff, lines, 320, out=dout, stream=main)
+        flock.mask_components_frames(prob, 0.5, 8, capacity=cap, out=mout, stream=main)
+
+    outs = [t for d in (hout, rout, dout, mout) for t in d.values()]
+    with torch.cuda.stream(main):
+        step()
+    torch.cuda.synchronize()
+    # rows past the written counts of the capacity-sized outputs are not outputs
+    kept, ndet = int(rout["offsets"][-1]), int(mout["offsets"][-1])
+    valid = {id(rout["xy"]): kept, id(rout["index"]): kept}
+    for k in ("label", "area", "box", "centroid", "xy", "score"):
+        valid[id(mout[k])] = ndet
+    outs = [t[:valid[id(t)]] if id(t) in valid else t for t in outs]
+    ref = [t.clone() for t in outs]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=main):
+        step()
+    torch.cuda.synchronize()
+    other = torch.from_numpy(wl.bird_masks(23, 2, 90, 130, n_birds=40)).to(dev)
+    for rep in range(4):
+        for t in outs:
+            t.fill_(7)
+        # eager work of the program between replays
+        flock.mask_components_frames(other, 0.4, 4)
+        flock.heatmap_frames(grids[:2].contiguous(), 100.0, 1e-4, 4)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (got, want) in enumerate(zip(outs, ref)):
+            assert torch.equal(got, want), f"replay {rep}: output {i} differs from eager"
