@@ -28,8 +28,10 @@
 //      do not depend on their order); each root sets its first pixel's bit
 //      in a bitmap of the batch and counts itself in its block of 512 bits
 //      and its superblock of 64 blocks;
-//   4. mask_scan_kernel, one workgroup: each superblock's first rank, and
-//      per frame the rank of its first pixel (the component offsets);
+//   4. each superblock's first rank, and per frame the rank of its first
+//      pixel (the component offsets): in the finish kernel for batches of up
+//      to 2^26 pixels (every workgroup scans the superblock counts in LDS),
+//      else by mask_scan_kernel, one workgroup;
 //   5. mask_finish_kernel, one workgroup per tile: each root writes its
 //      component at its rank (the number of roots before its first pixel),
 //      and the pixels of the other pieces get their root's label (one wave
@@ -57,6 +59,7 @@ constexpr int kBitWords = kBitBlock / 32;
 constexpr int kSuper = 64;                      // blocks per superblock
 constexpr int kRelabel = 16;                    // relabelled pixels per lane per pass
 constexpr int kSuperBits = kBitBlock * kSuper;
+constexpr int kLocalSuper = 2048;               // superblocks the finish kernel scans itself (2^26 pixels)
 
 static_assert(kT == 64, "one lane per column of a tile");
 static_assert(kAccCap <= kMThreads, "one record per thread per pass");
@@ -485,9 +488,9 @@ __global__ __launch_bounds__(64) void mask_resolve_kernel(MaskArgs a, MaskWs w) 
 // wide and unconditional (the counts are padded to whole superblocks, the
 // bitmap to whole blocks plus one), so that they are all in flight at once;
 // the parts beyond b are masked off afterwards.
-__device__ __forceinline__ int32_t rank_before(const MaskWs &w, int64_t b) {
+__device__ __forceinline__ int32_t rank_before(const MaskWs &w, const int32_t *sbbase, int64_t b) {
     const int64_t sb = b / kSuperBits;
-    const int32_t base = w.sbbase[sb];
+    const int32_t base = sbbase[sb];
     if (b % kSuperBits == 0) return base;  // also b = total on a superblock edge
     const int64_t blk = b / kBitBlock;
     const int4 *cq = reinterpret_cast<const int4 *>(w.bcount) + sb * (kSuper / 4);
@@ -559,22 +562,55 @@ __global__ __launch_bounds__(1024) void mask_scan_kernel(MaskArgs a, MaskWs w) {
     __syncthreads();
     const int64_t WH = (int64_t)a.width * a.height;
     for (int f = tid; f <= a.n_frames; f += 1024) {
-        const int32_t r0 = rank_before(w, (int64_t)f * WH);
+        const int32_t r0 = rank_before(w, w.sbbase, (int64_t)f * WH);
         a.comp_offsets[f] = r0;
-        if (f < a.n_frames) a.n_components[f] = rank_before(w, (int64_t)(f + 1) * WH) - r0;
+        if (f < a.n_frames) a.n_components[f] = rank_before(w, w.sbbase, (int64_t)(f + 1) * WH) - r0;
     }
 }
 
 __global__ __launch_bounds__(kMThreads) void mask_finish_kernel(MaskArgs a, MaskWs w) {
     __shared__ int32_t s_list[kT * kT / 2];
+    __shared__ int32_t s_sbb[kLocalSuper + 1];
+    __shared__ int s_wtot[kMThreads / 64];
     __shared__ int32_t s_n;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const TileLoc t = tile_loc(a, blockIdx.x);
     const int np = w.tile_np[blockIdx.x];
-    const int64_t fbase = (int64_t)t.f * a.width * a.height;
+    const int64_t WH = (int64_t)a.width * a.height;
+    const int64_t fbase = (int64_t)t.f * WH;
     if (tid == 0) s_n = 0;
+    // the superblock bases: scanned here from the counts when they fit in
+    // LDS (no separate scan launch), else read from the scan kernel
+    const int32_t *sbbase = w.sbbase;
+    if (w.nsb <= kLocalSuper) {
+        constexpr int kPer = kLocalSuper / kMThreads;
+        int c[kPer], sum = 0;
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int i = tid * kPer + q;
+            c[q] = i < w.nsb ? w.sbcount[i] : 0;
+            sum += c[q];
+        }
+        int run = cl::block_exclusive_scan(sum, s_wtot);  // holds barriers
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            s_sbb[tid * kPer + q] = run;
+            run += c[q];
+        }
+        if (tid == kMThreads - 1) s_sbb[kLocalSuper] = run;
+        sbbase = s_sbb;
+    }
     __syncthreads();
+    if (w.nsb <= kLocalSuper) {
+        // frame offsets and counts: frame f's by workgroup f (there are at
+        // least as many tiles as frames)
+        for (int f = blockIdx.x; f <= a.n_frames && tid == 0; f += gridDim.x) {
+            const int32_t r0 = rank_before(w, sbbase, (int64_t)f * WH);
+            a.comp_offsets[f] = r0;
+            if (f < a.n_frames) a.n_components[f] = rank_before(w, sbbase, (int64_t)(f + 1) * WH) - r0;
+        }
+    }
     for (int p = tid; p < np; p += kMThreads) {
         const uint32_t s = (uint32_t)(t.base + p);
         const uint64_t k = w.gp[s];
@@ -586,7 +622,7 @@ __global__ __launch_bounds__(kMThreads) void mask_finish_kernel(MaskArgs a, Mask
             }
             continue;
         }
-        const int64_t rank = rank_before(w, (int64_t)(k >> 32));
+        const int64_t rank = rank_before(w, sbbase, (int64_t)(k >> 32));
         if (rank >= a.capacity) continue;
         const MaskRec R = w.rec[s];
         if (a.comp_label) a.comp_label[rank] = (int32_t)R.root;
@@ -727,7 +763,7 @@ hipError_t launch_mask(MaskArgs a, void *workspace, hipStream_t stream) {
         hipLaunchKernelGGL(mask_seam_kernel, dim3((unsigned)((nh + nv + 255) / 256)), dim3(256), 0, stream, a, w,
                            nh, nv);
     hipLaunchKernelGGL(mask_resolve_kernel, dim3(tiles), dim3(64), 0, stream, a, w);
-    hipLaunchKernelGGL(mask_scan_kernel, dim3(1), dim3(1024), 0, stream, a, w);
+    if (w.nsb > kLocalSuper) hipLaunchKernelGGL(mask_scan_kernel, dim3(1), dim3(1024), 0, stream, a, w);
     hipLaunchKernelGGL(mask_finish_kernel, dim3(tiles), dim3(kMThreads), 0, stream, a, w);
     return hipGetLastError();
 }

@@ -122,6 +122,13 @@ def test_extreme_shapes_gpu(shape):
         check(prob, 0.5, conn, tag="extreme")
 
 
+def test_batch_above_local_rank_limit_gpu():
+    # more than 2^26 pixels: the component ranks take the separate scan launch
+    rng = np.random.default_rng(44)
+    prob = rng.random((3, 4096, 6000), dtype=np.float32)
+    check(prob, 0.7, 8, tag="large batch")
+
+
 def test_threshold_ties_nan_inf_gpu():
     rng = np.random.default_rng(5)
     prob = rng.choice(np.array([0.5, np.nextafter(np.float32(0.5), np.float32(1)), 0.25, np.nan, np.inf, 0.9],
