@@ -459,6 +459,7 @@ __global__ __launch_bounds__(64) void mask_resolve_kernel(MaskArgs a, MaskWs w) 
     const int np = w.tile_np[blockIdx.x];
     for (int p = threadIdx.x; p < np; p += 64) {
         const uint32_t s = (uint32_t)(t.base + p);
+        const MaskRec R = w.rec[s];  // in flight during the root search
         const uint64_t own = ld64(w.gp + s);
         if ((uint32_t)own == s) {
             const uint64_t g = own >> 32;
@@ -469,7 +470,6 @@ __global__ __launch_bounds__(64) void mask_resolve_kernel(MaskArgs a, MaskWs w) 
         }
         const uint64_t rk = key_root_ro(w.gp, s);
         __hip_atomic_store(w.gp + s, rk, __ATOMIC_RELAXED, kAgent);  // step 5 reads the root here
-        const MaskRec R = w.rec[s];
         MaskRec *D = w.rec + (uint32_t)rk;
         // the root holds the component's first pixel, hence its top row
         atomicAdd(&D->area, R.area);
@@ -622,9 +622,9 @@ __global__ __launch_bounds__(kMThreads) void mask_finish_kernel(MaskArgs a, Mask
             }
             continue;
         }
+        const MaskRec R = w.rec[s];  // in flight with the rank's loads
         const int64_t rank = rank_before(w, sbbase, (int64_t)(k >> 32));
         if (rank >= a.capacity) continue;
-        const MaskRec R = w.rec[s];
         if (a.comp_label) a.comp_label[rank] = (int32_t)R.root;
         if (a.comp_area) a.comp_area[rank] = (int32_t)R.area;
         if (a.comp_box)
