@@ -278,18 +278,24 @@ def mask_components(prob, threshold: float, connectivity: int = 8):
     labels = np.zeros(p.shape, np.int32)
     ncomp = np.zeros(F, np.int32)
     offs = np.zeros(F + 1, np.int64)
-    cap = int(p.size)
-    lab = np.zeros(cap, np.int32)
-    area = np.zeros(cap, np.int32)
-    box = np.zeros((cap, 4), np.int32)
-    cen = np.zeros((cap, 2), np.float64)
-    qxy = np.zeros((cap, 2), np.int32)
-    score = np.zeros(cap, np.float32)
-    k = _load().oracle_mask_components(_ptr(p), F, w, h, float(threshold), int(connectivity), _ptr(labels),
-                                       _ptr(ncomp), _ptr(offs), cap, _ptr(lab), _ptr(area), _ptr(box), _ptr(cen),
-                                       _ptr(qxy), _ptr(score))
-    _check(int(k), "mask_components")
-    k = int(k)
+
+    def run(cap):
+        lab = np.zeros(cap, np.int32)
+        area = np.zeros(cap, np.int32)
+        box = np.zeros((cap, 4), np.int32)
+        cen = np.zeros((cap, 2), np.float64)
+        qxy = np.zeros((cap, 2), np.int32)
+        score = np.zeros(cap, np.float32)
+        k = _load().oracle_mask_components(_ptr(p), F, w, h, float(threshold), int(connectivity), _ptr(labels),
+                                           _ptr(ncomp), _ptr(offs), cap, _ptr(lab), _ptr(area), _ptr(box),
+                                           _ptr(cen), _ptr(qxy), _ptr(score))
+        _check(int(k), "mask_components")
+        return int(k), lab, area, box, cen, qxy, score
+
+    # small batches in one pass; large ones count first, then fill
+    k, lab, area, box, cen, qxy, score = run(int(p.size) if p.size <= (1 << 22) else 0)
+    if k > lab.shape[0]:
+        k, lab, area, box, cen, qxy, score = run(k)
     return {"labels": labels, "n_components": ncomp, "offsets": offs, "label": lab[:k].copy(),
             "area": area[:k].copy(), "box": box[:k].copy(), "centroid": cen[:k].copy(),
             "xy": qxy[:k].copy(), "score": score[:k].copy()}
