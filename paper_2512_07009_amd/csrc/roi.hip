@@ -42,8 +42,12 @@ constexpr int kRWaves = kRThreadsR / 64;
 // ex qy - ey qx below 2^51: exact in fp64 (two exact products, an exact
 // difference), one fp64 multiply per product where a 64-bit integer product
 // takes several instructions.
-__device__ __forceinline__ bool in_polygon(const RoiArgs &a, const int2 *poly, int px, int py) {
-    if (px < a.bx0 || px > a.bx1 || py < a.by0 || py > a.by1) return false;
+__device__ __forceinline__ bool in_box(const RoiArgs &a, int px, int py) {
+    return px >= a.bx0 && px <= a.bx1 && py >= a.by0 && py <= a.by1;
+}
+
+// The test for a point inside the bounding box.
+__device__ __forceinline__ bool in_polygon_boxed(const RoiArgs &a, const int2 *poly, int px, int py) {
     const int n = a.n_vertices;
     bool in = false;
     for (int i = 0; i < n; ++i) {
@@ -75,11 +79,19 @@ __device__ __forceinline__ void load_polygon(const RoiArgs &a, int2 *poly) {
 constexpr int kRBlock = kRoiBlock;             // birds per block
 constexpr int kRPer = kRBlock / kRThreadsR;    // birds per thread, consecutive chunks of 256
 
+// Flags of one block of birds.  The bounding-box test runs on every bird;
+// the birds inside the box (a small share for a region along a wall) are
+// queued in LDS and the edge tests run on the queue, so that whole waves
+// test in-box birds instead of every wave running the edge loop for the
+// few in-box lanes it holds.
 __global__ __launch_bounds__(kRThreadsR) void roi_flag_kernel(RoiArgs a, uint8_t *flag, int32_t *bcount) {
     __shared__ int2 poly[kRoiMaxVertices];
-    __shared__ int s_cnt[kRWaves];
-    load_polygon(a, poly);
-    const int tid = threadIdx.x;
+    __shared__ int2 s_pt[kRBlock];        // in-box birds: coordinates
+    __shared__ uint16_t s_at[kRBlock];    // and their index in the block
+    __shared__ int s_nq, s_in;
+    if (threadIdx.x == 0) s_nq = s_in = 0;
+    load_polygon(a, poly);  // holds a barrier
+    const int tid = threadIdx.x, lane = tid & 63;
     const long long i0 = (long long)blockIdx.x * kRBlock;
     const int2 *P = reinterpret_cast<const int2 *>(a.xy);
     // all loads first, so that their latencies overlap
@@ -89,29 +101,37 @@ __global__ __launch_bounds__(kRThreadsR) void roi_flag_kernel(RoiArgs a, uint8_t
         const long long i = i0 + k * kRThreadsR + tid;
         pts[k] = i < a.total ? P[i] : make_int2(INT_MIN, INT_MIN);
     }
-    // then every test, then every store (a store between two tests made the
-    // compiler wait for it before the next test's loads)
-    bool in[kRPer];
-    int cnt = 0;
-#pragma unroll
-    for (int k = 0; k < kRPer; ++k) {
-        in[k] = in_polygon(a, poly, pts[k].x, pts[k].y);  // a padding lane's point is outside every box
-        cnt += in[k];
-    }
+    // box test; birds outside are flagged 0 now, the others queued
 #pragma unroll
     for (int k = 0; k < kRPer; ++k) {
         const long long i = i0 + k * kRThreadsR + tid;
-        if (i < a.total) flag[i] = in[k];
+        const bool box = in_box(a, pts[k].x, pts[k].y);  // a padding lane's point is outside every box
+        const uint64_t m = __ballot(box);
+        int base = 0;
+        if (lane == 0 && m) base = atomicAdd(&s_nq, __popcll(m));
+        base = __shfl(base, 0, 64);
+        if (box) {
+            const int q = base + __popcll(m & ((1ull << lane) - 1));
+            s_pt[q] = pts[k];
+            s_at[q] = (uint16_t)(k * kRThreadsR + tid);
+        } else if (i < a.total) {
+            flag[i] = 0;
+        }
+    }
+    __syncthreads();
+    const int nq = s_nq;
+    int cnt = 0;
+    for (int q = tid; q < nq; q += kRThreadsR) {
+        const int2 pt = s_pt[q];
+        const bool in = in_polygon_boxed(a, poly, pt.x, pt.y);
+        flag[i0 + s_at[q]] = in;
+        cnt += in;
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
-    if ((tid & 63) == 0) s_cnt[tid >> 6] = cnt;
+    if (lane == 0 && cnt) atomicAdd(&s_in, cnt);
     __syncthreads();
-    if (tid == 0) {
-        int t = 0;
-        for (int w = 0; w < kRWaves; ++w) t += s_cnt[w];
-        bcount[blockIdx.x] = t;
-    }
+    if (tid == 0) bcount[blockIdx.x] = s_in;
 }
 
 // bbase[b] = bcount[0] + ... + bcount[b - 1]; bbase[nb] = all kept birds.
