@@ -289,11 +289,25 @@ __device__ __forceinline__ bool near_segment(int4 s, int px, int py, long long t
     return ch < lh || (ch == lh && cl < ll);
 }
 
+// Flags of one block of birds.  A bird within T of a segment lies in the
+// segment's bounding box widened by T on every side, so birds outside all
+// widened boxes (most of them, for lines across the frame) are not drinking;
+// the others are queued in LDS and tested exactly on the queue, so that whole
+// waves run the exact tests.
 __global__ __launch_bounds__(kRThreadsR) void drink_flag_kernel(DrinkArgs a, int32_t *bcount) {
     __shared__ int4 seg[kDrinkMaxLines];
-    __shared__ int s_cnt[kRWaves];
-    const int tid = threadIdx.x;
-    if (tid < a.n_lines) seg[tid] = make_int4(a.ax[tid], a.ay[tid], a.bx[tid], a.by[tid]);
+    __shared__ int4 box[kDrinkMaxLines];  // x0, y0, x1, y1 widened by T
+    __shared__ int2 s_pt[kRBlock];
+    __shared__ uint16_t s_at[kRBlock];
+    __shared__ int s_nq, s_in;
+    const int tid = threadIdx.x, lane = tid & 63;
+    if (tid == 0) s_nq = s_in = 0;
+    if (tid < a.n_lines) {
+        seg[tid] = make_int4(a.ax[tid], a.ay[tid], a.bx[tid], a.by[tid]);
+        const int t = a.threshold;  // |coordinates|, T <= 2^24: no overflow
+        box[tid] = make_int4(min(a.ax[tid], a.bx[tid]) - t, min(a.ay[tid], a.by[tid]) - t,
+                             max(a.ax[tid], a.bx[tid]) + t, max(a.ay[tid], a.by[tid]) + t);
+    }
     __syncthreads();
     const long long i0 = (long long)blockIdx.x * kRBlock;
     const int2 *P = reinterpret_cast<const int2 *>(a.xy);
@@ -304,32 +318,46 @@ __global__ __launch_bounds__(kRThreadsR) void drink_flag_kernel(DrinkArgs a, int
         const long long i = i0 + k * kRThreadsR + tid;
         pts[k] = i < a.total ? P[i] : make_int2(0, 0);
     }
-    int32_t hit[kRPer];
-    int cnt = 0;
 #pragma unroll
     for (int k = 0; k < kRPer; ++k) {
-        hit[k] = -1;
-        for (int l = 0; l < a.n_lines && hit[k] < 0; ++l)
-            if (near_segment(seg[l], pts[k].x, pts[k].y, t2)) hit[k] = l;
         const long long i = i0 + k * kRThreadsR + tid;
-        cnt += (i < a.total) & (hit[k] >= 0);
+        bool cand = false;
+        for (int l = 0; l < a.n_lines; ++l) {
+            const int4 b = box[l];
+            cand |= (pts[k].x > b.x) & (pts[k].x < b.z) & (pts[k].y > b.y) & (pts[k].y < b.w);
+        }
+        cand &= i < a.total;
+        const uint64_t m = __ballot(cand);
+        int base = 0;
+        if (lane == 0 && m) base = atomicAdd(&s_nq, __popcll(m));
+        base = __shfl(base, 0, 64);
+        if (cand) {
+            const int q = base + __popcll(m & ((1ull << lane) - 1));
+            s_pt[q] = pts[k];
+            s_at[q] = (uint16_t)(k * kRThreadsR + tid);
+        } else if (i < a.total) {
+            a.drinking[i] = 0;
+            if (a.line) a.line[i] = -1;
+        }
     }
-#pragma unroll
-    for (int k = 0; k < kRPer; ++k) {
-        const long long i = i0 + k * kRThreadsR + tid;
-        if (i >= a.total) continue;
-        a.drinking[i] = hit[k] >= 0;
-        if (a.line) a.line[i] = hit[k];
+    __syncthreads();
+    const int nq = s_nq;
+    int cnt = 0;
+    for (int q = tid; q < nq; q += kRThreadsR) {
+        const int2 pt = s_pt[q];
+        int32_t hit = -1;
+        for (int l = 0; l < a.n_lines && hit < 0; ++l)
+            if (near_segment(seg[l], pt.x, pt.y, t2)) hit = l;
+        const long long i = i0 + s_at[q];
+        a.drinking[i] = hit >= 0;
+        if (a.line) a.line[i] = hit;
+        cnt += hit >= 0;
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
-    if ((tid & 63) == 0) s_cnt[tid >> 6] = cnt;
+    if (lane == 0 && cnt) atomicAdd(&s_in, cnt);
     __syncthreads();
-    if (tid == 0) {
-        int t = 0;
-        for (int w = 0; w < kRWaves; ++w) t += s_cnt[w];
-        bcount[blockIdx.x] = t;
-    }
+    if (tid == 0) bcount[blockIdx.x] = s_in;
 }
 
 }  // namespace
