@@ -222,7 +222,8 @@ flock_status roi_filter_frames(const int32_t *xy, const int32_t *offsets, int32_
                                size_t workspace_bytes, void *stream);
 
 /* Bytes of workspace roi_filter_frames needs for this batch (a flag per bird,
- * plus a count and a base per block of 2048 birds). */
+ * a count and a base per block of 2048 birds, and 12 bytes per bird, rounded
+ * up to whole blocks, where each block stages its kept birds). */
 size_t roi_filter_frames_workspace(int32_t n_frames, int32_t total);
 
 /*

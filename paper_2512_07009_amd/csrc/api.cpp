@@ -334,7 +334,7 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
 
 size_t roi_filter_frames_workspace(int32_t n_frames, int32_t total) {
     g_error.clear();
-    return n_frames > 0 ? flock::roi_workspace_bytes(total) : 0;  // flags, block counts and bases
+    return n_frames > 0 ? flock::roi_workspace_bytes(total) : 0;  // flags, block counts and bases, staging
 }
 
 flock_status roi_filter_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,

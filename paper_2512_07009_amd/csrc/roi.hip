@@ -12,9 +12,10 @@
 //   1. roi_flag_kernel: the inside test per bird (polygon in LDS), a flag
 //      byte per bird and a count per block;
 //   2. roi_scan_kernel, one workgroup: each block's first output position;
-//   3. roi_write_kernel: ballots and wave totals give each kept bird its rank
-//      in its block; coordinates and input index go to base + rank, so kept
-//      birds keep their input order;
+//   3. roi_write_kernel: each block's kept birds, which the flag kernel
+//      staged in input order (ballots and wave totals give each its rank in
+//      the block), are copied to the block's base + rank, so kept birds keep
+//      their input order;
 //   4. frame_counts_kernel, one wave per frame boundary: the output position
 //      of the boundary bird (its block's base plus the flags before it in the
 //      block) gives out_offsets, and neighbouring boundaries give counts.
@@ -83,15 +84,20 @@ constexpr int kRPer = kRBlock / kRThreadsR;    // birds per thread, consecutive 
 // the birds inside the box (a small share for a region along a wall) are
 // queued in LDS and the edge tests run on the queue, so that whole waves
 // test in-box birds instead of every wave running the edge loop for the
-// few in-box lanes it holds.
-__global__ __launch_bounds__(kRThreadsR) void roi_flag_kernel(RoiArgs a, uint8_t *flag, int32_t *bcount) {
+// few in-box lanes it holds.  The kept birds then go, in input order, to the
+// block's staging area (coordinates and input index), for the write kernel
+// to copy to their final places without reading every bird again.
+__global__ __launch_bounds__(kRThreadsR) void roi_flag_kernel(RoiArgs a, uint8_t *flag, int32_t *bcount,
+                                                             int2 *stage_xy, int32_t *stage_idx) {
     __shared__ int2 poly[kRoiMaxVertices];
     __shared__ int2 s_pt[kRBlock];        // in-box birds: coordinates
     __shared__ uint16_t s_at[kRBlock];    // and their index in the block
-    __shared__ int s_nq, s_in;
-    if (threadIdx.x == 0) s_nq = s_in = 0;
+    __shared__ uint8_t s_f[kRBlock];      // every bird's flag
+    __shared__ int s_tot[kRPer][kRWaves];
+    __shared__ int s_nq;
+    if (threadIdx.x == 0) s_nq = 0;
     load_polygon(a, poly);  // holds a barrier
-    const int tid = threadIdx.x, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const long long i0 = (long long)blockIdx.x * kRBlock;
     const int2 *P = reinterpret_cast<const int2 *>(a.xy);
     // all loads first, so that their latencies overlap
@@ -101,10 +107,9 @@ __global__ __launch_bounds__(kRThreadsR) void roi_flag_kernel(RoiArgs a, uint8_t
         const long long i = i0 + k * kRThreadsR + tid;
         pts[k] = i < a.total ? P[i] : make_int2(INT_MIN, INT_MIN);
     }
-    // box test; birds outside are flagged 0 now, the others queued
+    // box test; birds outside are out, the others queued
 #pragma unroll
     for (int k = 0; k < kRPer; ++k) {
-        const long long i = i0 + k * kRThreadsR + tid;
         const bool box = in_box(a, pts[k].x, pts[k].y);  // a padding lane's point is outside every box
         const uint64_t m = __ballot(box);
         int base = 0;
@@ -114,24 +119,47 @@ __global__ __launch_bounds__(kRThreadsR) void roi_flag_kernel(RoiArgs a, uint8_t
             const int q = base + __popcll(m & ((1ull << lane) - 1));
             s_pt[q] = pts[k];
             s_at[q] = (uint16_t)(k * kRThreadsR + tid);
-        } else if (i < a.total) {
-            flag[i] = 0;
+        } else {
+            s_f[k * kRThreadsR + tid] = 0;
         }
     }
     __syncthreads();
     const int nq = s_nq;
-    int cnt = 0;
     for (int q = tid; q < nq; q += kRThreadsR) {
         const int2 pt = s_pt[q];
-        const bool in = in_polygon_boxed(a, poly, pt.x, pt.y);
-        flag[i0 + s_at[q]] = in;
-        cnt += in;
+        s_f[s_at[q]] = in_polygon_boxed(a, poly, pt.x, pt.y);
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
-    if (lane == 0 && cnt) atomicAdd(&s_in, cnt);
     __syncthreads();
-    if (tid == 0) bcount[blockIdx.x] = s_in;
+    // flags out, and the kept birds' ranks in the block (input order)
+    bool in[kRPer];
+    uint64_t m[kRPer];
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) {
+        const long long i = i0 + k * kRThreadsR + tid;
+        in[k] = s_f[k * kRThreadsR + tid] != 0;
+        if (i < a.total) flag[i] = in[k];
+        m[k] = __ballot(in[k]);
+        if (lane == 0) s_tot[k][wave] = __popcll(m[k]);
+    }
+    __syncthreads();
+    int at = 0;
+    const long long sbase = (long long)blockIdx.x * kRBlock;
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) {
+        int before = 0, chunk = 0;
+#pragma unroll
+        for (int w = 0; w < kRWaves; ++w) {
+            before += w < wave ? s_tot[k][w] : 0;
+            chunk += s_tot[k][w];
+        }
+        if (in[k]) {
+            const long long r = sbase + at + before + __popcll(m[k] & ((1ull << lane) - 1ull));
+            stage_xy[r] = pts[k];
+            stage_idx[r] = (int32_t)(i0 + k * kRThreadsR + tid);
+        }
+        at += chunk;
+    }
+    if (tid == 0) bcount[blockIdx.x] = at;
 }
 
 // bbase[b] = bcount[0] + ... + bcount[b - 1]; bbase[nb] = all kept birds.
@@ -159,46 +187,16 @@ __global__ __launch_bounds__(1024) void roi_scan_kernel(const int32_t *bcount, i
     if (tid == 1023) bbase[nb] = run;  // the last thread's chunk ends at nb
 }
 
-__global__ __launch_bounds__(kRThreadsR) void roi_write_kernel(RoiArgs a, const uint8_t *flag,
-                                                              const int32_t *bbase) {
-    __shared__ int s_tot[kRPer][kRWaves];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const long long i0 = (long long)blockIdx.x * kRBlock;
-    const int2 *P = reinterpret_cast<const int2 *>(a.xy);
+// Each block's kept birds, staged in input order by the flag kernel, go to
+// base + rank.
+__global__ __launch_bounds__(kRThreadsR) void roi_write_kernel(RoiArgs a, const int32_t *bbase,
+                                                              const int2 *stage_xy, const int32_t *stage_idx) {
+    const int32_t base = bbase[blockIdx.x], n = bbase[blockIdx.x + 1] - base;
+    const long long sbase = (long long)blockIdx.x * kRBlock;
     int2 *O = reinterpret_cast<int2 *>(a.out_xy);
-    // every chunk's flags and ballots first, one barrier for all wave totals
-    bool in[kRPer];
-    uint64_t m[kRPer];
-#pragma unroll
-    for (int k = 0; k < kRPer; ++k) {
-        const long long i = i0 + k * kRThreadsR + tid;
-        in[k] = i < a.total && flag[i];
-    }
-#pragma unroll
-    for (int k = 0; k < kRPer; ++k) {
-        m[k] = __ballot(in[k]);
-        if (lane == 0) s_tot[k][wave] = __popcll(m[k]);
-    }
-    __syncthreads();
-    // the kept birds' coordinates are loaded before any store
-    int2 pt[kRPer];
-#pragma unroll
-    for (int k = 0; k < kRPer; ++k) pt[k] = in[k] ? P[i0 + k * kRThreadsR + tid] : make_int2(0, 0);
-    int32_t at = bbase[blockIdx.x];
-#pragma unroll
-    for (int k = 0; k < kRPer; ++k) {
-        int before = 0, chunk = 0;
-#pragma unroll
-        for (int w = 0; w < kRWaves; ++w) {
-            before += w < wave ? s_tot[k][w] : 0;
-            chunk += s_tot[k][w];
-        }
-        if (in[k]) {
-            const int32_t r = at + before + __popcll(m[k] & ((1ull << lane) - 1ull));
-            O[r] = pt[k];
-            if (a.out_index) a.out_index[r] = (int32_t)(i0 + k * kRThreadsR + tid);
-        }
-        at += chunk;
+    for (int t = threadIdx.x; t < n; t += kRThreadsR) {
+        O[base + t] = stage_xy[sbase + t];
+        if (a.out_index) a.out_index[base + t] = stage_idx[sbase + t];
     }
 }
 
@@ -362,10 +360,13 @@ __global__ __launch_bounds__(kRThreadsR) void drink_flag_kernel(DrinkArgs a, int
 
 }  // namespace
 
+// Workspace: a flag per bird; a count and a base per block; per block a
+// staging area of kRBlock coordinates and kRBlock input indices.
 size_t roi_workspace_bytes(int32_t total) {
     if (total <= 0) return 256;
     const size_t nb = ((size_t)total + kRBlock - 1) / kRBlock;
-    return (((size_t)total + 255) & ~(size_t)255) + (((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255);
+    return (((size_t)total + 255) & ~(size_t)255) + (((2 * nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255) +
+           nb * kRBlock * (sizeof(int2) + sizeof(int32_t));
 }
 
 hipError_t launch_roi(const RoiArgs &a, void *workspace, hipStream_t stream) {
@@ -373,9 +374,16 @@ hipError_t launch_roi(const RoiArgs &a, void *workspace, hipStream_t stream) {
     uint8_t *flag = static_cast<uint8_t *>(workspace);
     int32_t *bcount = reinterpret_cast<int32_t *>(flag + (a.total > 0 ? (((size_t)a.total + 255) & ~(size_t)255) : 0));
     int32_t *bbase = bcount + nb;
-    if (nb > 0) hipLaunchKernelGGL(roi_flag_kernel, dim3((unsigned)nb), dim3(kRThreadsR), 0, stream, a, flag, bcount);
+    char *stage = reinterpret_cast<char *>(bcount) + (((2 * (size_t)nb + 1) * sizeof(int32_t) + 255) & ~(size_t)255);
+    int2 *stage_xy = reinterpret_cast<int2 *>(stage);
+    int32_t *stage_idx = reinterpret_cast<int32_t *>(stage + (size_t)nb * kRBlock * sizeof(int2));
+    if (nb > 0)
+        hipLaunchKernelGGL(roi_flag_kernel, dim3((unsigned)nb), dim3(kRThreadsR), 0, stream, a, flag, bcount, stage_xy,
+                           stage_idx);
     hipLaunchKernelGGL(roi_scan_kernel, dim3(1), dim3(1024), 0, stream, bcount, bbase, nb);
-    if (nb > 0) hipLaunchKernelGGL(roi_write_kernel, dim3((unsigned)nb), dim3(kRThreadsR), 0, stream, a, flag, bbase);
+    if (nb > 0)
+        hipLaunchKernelGGL(roi_write_kernel, dim3((unsigned)nb), dim3(kRThreadsR), 0, stream, a, bbase, stage_xy,
+                           stage_idx);
     const FrameCounts fc{flag, bbase, a.offsets, a.n_frames, a.total, a.counts, a.out_offsets};
     const long long waves = (long long)a.n_frames + 1;
     hipLaunchKernelGGL(frame_counts_kernel, dim3((unsigned)((waves * 64 + 255) / 256)), dim3(256), 0, stream, fc);
