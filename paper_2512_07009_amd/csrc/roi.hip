@@ -316,15 +316,19 @@ __global__ __launch_bounds__(kRThreadsR) void drink_flag_kernel(DrinkArgs a, int
         const long long i = i0 + k * kRThreadsR + tid;
         pts[k] = i < a.total ? P[i] : make_int2(0, 0);
     }
+    bool cands[kRPer];
+#pragma unroll
+    for (int k = 0; k < kRPer; ++k) cands[k] = false;
+    for (int l = 0; l < a.n_lines; ++l) {  // each box read once, for all of the thread's birds
+        const int4 b = box[l];
+#pragma unroll
+        for (int k = 0; k < kRPer; ++k)
+            cands[k] |= (pts[k].x > b.x) & (pts[k].x < b.z) & (pts[k].y > b.y) & (pts[k].y < b.w);
+    }
 #pragma unroll
     for (int k = 0; k < kRPer; ++k) {
         const long long i = i0 + k * kRThreadsR + tid;
-        bool cand = false;
-        for (int l = 0; l < a.n_lines; ++l) {
-            const int4 b = box[l];
-            cand |= (pts[k].x > b.x) & (pts[k].x < b.z) & (pts[k].y > b.y) & (pts[k].y < b.w);
-        }
-        cand &= i < a.total;
+        const bool cand = cands[k] & (i < a.total);
         const uint64_t m = __ballot(cand);
         int base = 0;
         if (lane == 0 && m) base = atomicAdd(&s_nq, __popcll(m));
