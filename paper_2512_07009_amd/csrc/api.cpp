@@ -523,7 +523,7 @@ flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid
     // (FLOCK_HEATMAP_PATH=tiled takes the tiled kernels for every grid)
     const char *hp = std::getenv("FLOCK_HEATMAP_PATH");
     const bool tiled = hp && std::strcmp(hp, "tiled") == 0;
-    const bool resident = !tiled && flock::heatmap_frame_lds_bytes(grid_w, grid_h) + 1024 <= dev->lds_per_block;
+    const bool resident = !tiled && flock::heatmap_frame_lds_bytes(grid_w, grid_h) + 4096 <= dev->lds_per_block;
     const size_t need = resident ? flock::heatmap_frame_workspace_bytes(n_frames)
                                  : flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h);
     if (workspace && workspace_bytes < need)

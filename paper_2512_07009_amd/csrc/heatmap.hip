@@ -71,6 +71,39 @@ __device__ __forceinline__ uint32_t wave_max_u(uint32_t v) {
     return v;
 }
 
+// Natural log of a positive float in fp64, from a table of bucket centres:
+// v = m 2^e exactly (m in [1, 2)), c is the centre of m's bucket of width
+// 1/kLnBuckets, and ln v = e ln 2 + ln c + ln(1 + r) with r = m / c - 1,
+// |r| <= 2^-8, formed as fma(m, 1/c, -1); ln(1 + r) is its Taylor series
+// through r^7 (truncation below 2^-67).  The absolute error is a few 1e-16
+// (ln 2 and the table entries are rounded to fp64; |e| <= 149), about the
+// library routine's, at a fraction of its instructions.
+constexpr int kLnBuckets = 128;
+struct LnTable {
+    double ln_c[kLnBuckets], inv_c[kLnBuckets];
+};
+
+// Filled by threads 0 .. kLnBuckets - 1; the caller syncs before use.
+__device__ __forceinline__ void ln_table_init(LnTable &t) {
+    const int k = threadIdx.x;
+    if (k < kLnBuckets) {
+        const double c = 1.0 + ((double)k + 0.5) / kLnBuckets;
+        t.ln_c[k] = log(c);
+        t.inv_c[k] = 1.0 / c;
+    }
+}
+
+__device__ __forceinline__ double ln_pos(float vf, const LnTable &t) {
+    const uint64_t b = (uint64_t)__double_as_longlong((double)vf);
+    const int e = (int)(b >> 52) - 1023;
+    const int k = (int)((b >> 45) & (kLnBuckets - 1));
+    const double m = __longlong_as_double((long long)((b & 0x000fffffffffffffull) | 0x3ff0000000000000ull));
+    const double r = fma(m, t.inv_c[k], -1.0);
+    const double p =
+        r * (1.0 + r * (-0.5 + r * (1.0 / 3.0 + r * (-0.25 + r * (0.2 + r * (-1.0 / 6.0 + r * (1.0 / 7.0)))))));
+    return fma((double)e, 0.69314718055994530942, t.ln_c[k] + p);
+}
+
 struct TileGeom {
     int f, x0, y0, w, h;
 };
@@ -92,6 +125,9 @@ __global__ __launch_bounds__(kHThreads) void heat_tile_kernel(HeatArgs a, TilePa
     __shared__ uint8_t hotm[kHT * kHT];
     __shared__ double s_red[3][kHThreads / 64];
     __shared__ uint32_t s_max[kHThreads / 64];
+    __shared__ LnTable lnt;
+    ln_table_init(lnt);
+    __syncthreads();
     const TileGeom t = tile_of(a, blockIdx.x);
     const int tid = threadIdx.x, lx = tid % kHT, ly0 = tid / kHT;
     const size_t cells = (size_t)a.grid_w * a.grid_h;
@@ -112,7 +148,7 @@ __global__ __launch_bounds__(kHThreads) void heat_tile_kernel(HeatArgs a, TilePa
         hotm[l] = hot[k];
         if (v[k] > 0.0f) {
             s += (double)v[k];
-            e += (double)v[k] * log((double)v[k]);
+            e += (double)v[k] * ln_pos(v[k], lnt);
             mb = max(mb, __float_as_uint(v[k]));
         }
         if (hot[k]) hs += (double)v[k];
@@ -361,6 +397,9 @@ __global__ __launch_bounds__(kFThreads) void heat_frame_kernel(HeatArgs a, int32
     __shared__ double s_red[3][kFWaves];
     __shared__ uint32_t s_max[kFWaves];
     __shared__ int s_shift, s_ncomp;
+    __shared__ LnTable lnt;
+    ln_table_init(lnt);
+    __syncthreads();
     const int f = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int gw = a.grid_w, gh = a.grid_h;
     const int cells = gw * gh;
@@ -379,7 +418,7 @@ __global__ __launch_bounds__(kFThreads) void heat_frame_kernel(HeatArgs a, int32
         P[c] = hot ? c : -1;
         if (v > 0.0f) {
             s += (double)v;
-            e += (double)v * log((double)v);
+            e += (double)v * ln_pos(v, lnt);
             mb = max(mb, __float_as_uint(v));
         }
         if (hot) hs += (double)v;
