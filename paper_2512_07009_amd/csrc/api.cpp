@@ -486,7 +486,9 @@ flock_status drinker_proximity_frames(const int32_t *xy, const int32_t *offsets,
 
 size_t heatmap_frames_workspace(int32_t n_frames, int32_t grid_w, int32_t grid_h) {
     g_error.clear();
-    return flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h);
+    // enough for either path (which one runs depends on the device's LDS)
+    return std::max(flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h),
+                    flock::heatmap_frame_workspace_bytes(n_frames, grid_w, grid_h));
 }
 
 flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid_w, int32_t grid_h,
@@ -524,7 +526,7 @@ flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid
     const char *hp = std::getenv("FLOCK_HEATMAP_PATH");
     const bool tiled = hp && std::strcmp(hp, "tiled") == 0;
     const bool resident = !tiled && flock::heatmap_frame_lds_bytes(grid_w, grid_h) + 4096 <= dev->lds_per_block;
-    const size_t need = resident ? flock::heatmap_frame_workspace_bytes(n_frames)
+    const size_t need = resident ? flock::heatmap_frame_workspace_bytes(n_frames, grid_w, grid_h)
                                  : flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h);
     if (workspace && workspace_bytes < need)
         return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);

@@ -359,6 +359,22 @@ __global__ __launch_bounds__(256) void heat_mass_kernel(HeatArgs a, const int32_
     a.comp_mass[i] = ldexp((double)q, -shift[f]) * a.cell_area;
 }
 
+// The same for the frame-resident path, over each frame's list of label
+// cells only (one workgroup per frame).
+__global__ __launch_bounds__(256) void heat_root_mass_kernel(HeatArgs a, const int32_t *shift,
+                                                             const int32_t *roots) {
+    const int f = blockIdx.x;
+    const size_t cells = (size_t)a.grid_w * a.grid_h;
+    const int n = a.n_components[f];
+    const int sh = shift[f];
+    unsigned long long *CMu = reinterpret_cast<unsigned long long *>(a.comp_mass) + (size_t)f * cells;
+    double *CM = a.comp_mass + (size_t)f * cells;
+    for (int t = threadIdx.x; t < n; t += 256) {
+        const int32_t c = roots[(size_t)f * cells + t];
+        CM[c] = ldexp((double)CMu[c], -sh) * a.cell_area;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Frame-resident path: one workgroup per frame, the whole grid's forest in LDS
 // ---------------------------------------------------------------------------
@@ -388,11 +404,12 @@ __device__ __forceinline__ unsigned long long wave_incl_scan_u64(unsigned long l
 //      and for the 8-neighbourhood a diagonal pair only where no edge-sharing
 //      path through c's row neighbour or the cell below exists;
 //   D. labels by read-only walks; per wave, runs of lanes with equal roots
-//      add their cells and fixed-point mass with one global atomic each.
-// heat_mass_kernel then converts the label cells' mass (after the kernel
+//      add their cells and fixed-point mass with one global atomic each;
+//      each root cell appends its index to the frame's list in the workspace.
+// heat_root_mass_kernel then converts the listed cells' mass (after the kernel
 // boundary every atomic is complete; a device-scope fence inside the kernel
 // would instead write back the L2 once per workgroup).
-__global__ __launch_bounds__(kFThreads) void heat_frame_kernel(HeatArgs a, int32_t *shift) {
+__global__ __launch_bounds__(kFThreads) void heat_frame_kernel(HeatArgs a, int32_t *shift, int32_t *roots) {
     extern __shared__ int32_t P[];
     __shared__ double s_red[3][kFWaves];
     __shared__ uint32_t s_max[kFWaves];
@@ -495,7 +512,7 @@ __global__ __launch_bounds__(kFThreads) void heat_frame_kernel(HeatArgs a, int32
         if (r >= 0) {
             L[c] = r;
             q = (unsigned long long)llrint(ldexp((double)D[c], sh));
-            if (r == c) atomicAdd(&s_ncomp, 1);
+            if (r == c) roots[(size_t)f * cells + atomicAdd(&s_ncomp, 1)] = c;  // for heat_root_mass_kernel
         } else if (in) {
             L[c] = -1;
         }
@@ -527,18 +544,21 @@ size_t heatmap_workspace_bytes(int32_t n_frames, int32_t grid_w, int32_t grid_h)
 
 size_t heatmap_frame_lds_bytes(int32_t grid_w, int32_t grid_h) { return (size_t)grid_w * grid_h * sizeof(int32_t); }
 
-size_t heatmap_frame_workspace_bytes(int32_t n_frames) {
-    return n_frames > 0 ? (((size_t)n_frames * sizeof(int32_t) + 255) & ~(size_t)255) : 0;
+// A shift per frame, then each frame's label cells (at most one per cell).
+size_t heatmap_frame_workspace_bytes(int32_t n_frames, int32_t grid_w, int32_t grid_h) {
+    if (n_frames <= 0 || grid_w < 1 || grid_h < 1) return 0;
+    return (((size_t)n_frames * sizeof(int32_t) + 255) & ~(size_t)255) +
+           (size_t)n_frames * grid_w * grid_h * sizeof(int32_t);
 }
 
 hipError_t launch_heatmap(HeatArgs a, void *workspace, bool resident, hipStream_t stream) {
     if (resident) {
         int32_t *shift = static_cast<int32_t *>(workspace);
-        const long long cells = (long long)a.grid_w * a.grid_h * a.n_frames;
+        int32_t *roots = reinterpret_cast<int32_t *>(static_cast<unsigned char *>(workspace) +
+                                                     (((size_t)a.n_frames * sizeof(int32_t) + 255) & ~(size_t)255));
         hipLaunchKernelGGL(heat_frame_kernel, dim3((unsigned)a.n_frames), dim3(kFThreads),
-                           heatmap_frame_lds_bytes(a.grid_w, a.grid_h), stream, a, shift);
-        hipLaunchKernelGGL(heat_mass_kernel, dim3((unsigned)((cells + 255) / 256)), dim3(256), 0, stream, a,
-                           shift);
+                           heatmap_frame_lds_bytes(a.grid_w, a.grid_h), stream, a, shift, roots);
+        hipLaunchKernelGGL(heat_root_mass_kernel, dim3((unsigned)a.n_frames), dim3(256), 0, stream, a, shift, roots);
         return hipGetLastError();
     }
     a.tiles_x = (a.grid_w + kHT - 1) / kHT;

@@ -103,7 +103,7 @@ size_t heatmap_workspace_bytes(int32_t n_frames, int32_t grid_w, int32_t grid_h)
 // Dynamic LDS of the frame-resident kernel (one workgroup per frame), and
 // its workspace (the per-frame fixed-point scales).
 size_t heatmap_frame_lds_bytes(int32_t grid_w, int32_t grid_h);
-size_t heatmap_frame_workspace_bytes(int32_t n_frames);
+size_t heatmap_frame_workspace_bytes(int32_t n_frames, int32_t grid_w, int32_t grid_h);
 // resident: one workgroup per frame with the grid in LDS (needs
 // heatmap_frame_lds_bytes within the device's limit); else the tiled kernels,
 // which use the workspace.
