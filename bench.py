@@ -413,10 +413,29 @@ def main():
     ma["traffic"] = committed_traffic("mask", mw.name)
     if not args.no_cpu_baseline:
         import oracle
+        log("timing the CPU oracle beside the heatmap, roi, drinker and mask entries")
         t0 = time.perf_counter()
         oracle.mask_components(prob_np, mw.threshold, mw.connectivity)
         ma["oracle_frames_per_s"] = MF / (time.perf_counter() - t0)
         ma["oracle_threads"] = 1
+        # bounded samples: the first frames, up to 4M grid cells / 2M birds
+        nh = int(max(1, min(F, (1 << 22) // cells)))
+        dens_np = dens[:nh].float().cpu().numpy()
+        t0 = time.perf_counter()
+        oracle.heatmap_frames(dens_np, area, heat_thr, 8)
+        he["oracle_frames_per_s"] = nh / (time.perf_counter() - t0)
+        he["oracle_threads"] = oracle.default_threads()
+        he["oracle_sample_frames"] = nh
+        nb = int(max(1, np.searchsorted(off, 1 << 21, side="right") - 1))
+        sxy, soff = xy[: off[nb]], off[: nb + 1]
+        t0 = time.perf_counter()
+        oracle.roi_filter(sxy, soff, roi_poly)
+        ro["oracle_frames_per_s"] = nb / (time.perf_counter() - t0)
+        t0 = time.perf_counter()
+        oracle.drinkers(sxy, soff, dlines, dthr)
+        dr["oracle_frames_per_s"] = nb / (time.perf_counter() - t0)
+        ro["oracle_threads"] = dr["oracle_threads"] = 1
+        ro["oracle_sample_frames"] = dr["oracle_sample_frames"] = nb
     dominant = ("cluster_frames", cl) if t_cluster >= t_density else ("density_frames", de)
     roof = {k: dominant[1][k] for k in ("bound", "achieved", "peak", "unit", "frac", "traffic")}
     roof["kernel"] = dominant[0]
