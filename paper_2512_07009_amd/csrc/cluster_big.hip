@@ -376,11 +376,20 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
         const int32_t ddx = min(max(max(rx0 - va.x, va.x - rx1), 0), r.e1);
         const int32_t ddy = min(max(max(ry0 - va.y, va.y - ry1), 0), r.e1);
         if (__mul24(ddx, ddx) + __mul24(ddy, ddy) > r.e2) continue;
-        for (int32_t qb = b0; qb < b1; ++qb) {
-            if (core[qb] && within(va, S[qb], r)) {
-                uf_unite<kAgent>(parent, na, nb);
-                return;
-            }
+        // four independent loads in flight per step: the scan of a large
+        // cell pair is bound by their latency, not by the tests
+        int32_t qb = b0;
+        bool hit = false;
+        for (; qb + 4 <= b1 && !hit; qb += 4) {
+            const int2 s0 = S[qb], s1 = S[qb + 1], s2 = S[qb + 2], s3 = S[qb + 3];
+            const uint8_t c0 = core[qb], c1 = core[qb + 1], c2 = core[qb + 2], c3 = core[qb + 3];
+            hit = (c0 && within(va, s0, r)) | (c1 && within(va, s1, r)) | (c2 && within(va, s2, r)) |
+                  (c3 && within(va, s3, r));
+        }
+        for (; qb < b1 && !hit; ++qb) hit = core[qb] && within(va, S[qb], r);
+        if (hit) {
+            uf_unite<kAgent>(parent, na, nb);
+            return;
         }
     }
 }
