@@ -40,6 +40,8 @@ using namespace cl;
 
 constexpr int kBlock = 256;
 constexpr int kScanThreads = 1024;
+constexpr int kPrepThreads = 1024;
+constexpr int kUnroll = 8;  // independent loads per thread and step in prep and scan
 constexpr int kRec = 16;  // int32 fields per frame record
 
 enum RecField {
@@ -138,7 +140,7 @@ __device__ __forceinline__ void cell_xy(int2 p, const BigGrid &g, int32_t *cx, i
 
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kBlock) void big_prep(ClusterArgs a, BigWs w) {
+__global__ __launch_bounds__(kPrepThreads) void big_prep(ClusterArgs a, BigWs w) {
     __shared__ int s_bbox[4];
     const int f = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
     int32_t *rec = w.rec + (size_t)f * kRec;
@@ -158,12 +160,20 @@ __global__ __launch_bounds__(kBlock) void big_prep(ClusterArgs a, BigWs w) {
     __syncthreads();
     const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
     int xmn = INT_MAX, ymn = INT_MAX, xmx = INT_MIN, ymx = INT_MIN;
-    for (int32_t i = tid; i < n; i += kBlock) {
-        const int2 p = P[i];
-        xmn = min(xmn, p.x);
-        ymn = min(ymn, p.y);
-        xmx = max(xmx, p.x);
-        ymx = max(ymx, p.y);
+    for (int32_t i0 = tid; i0 < n; i0 += kPrepThreads * kUnroll) {
+        int2 pv[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int32_t i = i0 + u * kPrepThreads;
+            pv[u] = i < n ? P[i] : P[i0];
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            xmn = min(xmn, pv[u].x);
+            ymn = min(ymn, pv[u].y);
+            xmx = max(xmx, pv[u].x);
+            ymx = max(ymx, pv[u].y);
+        }
     }
     xmn = wave_min(xmn);
     ymn = wave_min(ymn);
@@ -216,7 +226,7 @@ __global__ __launch_bounds__(kBlock) void big_prep(ClusterArgs a, BigWs w) {
         if (a.n_clusters) a.n_clusters[f] = 0;
     }
     const int64_t base = cell_base(a.offsets, f);
-    for (int32_t c = tid; c <= ncell; c += kBlock) {
+    for (int32_t c = tid; c <= ncell; c += kPrepThreads) {
         w.cstart[base + c] = 0;
         w.cnode[base + c] = INT_MAX;
     }
@@ -235,24 +245,50 @@ __global__ __launch_bounds__(kBlock) void big_hist(ClusterArgs a, BigWs w) {
     w.rank[i] = atomicAdd(&w.cstart[cell_base(a.offsets, f) + (int64_t)cy * g.ncx + cx], 1);
 }
 
+// Exclusive scan of a frame's cell counts, in tiles of kScanThreads * kUnroll
+// cells: coalesced loads into LDS, kUnroll consecutive cells per thread, a
+// workgroup scan plus the carry of the earlier tiles, coalesced stores.
 __global__ __launch_bounds__(kScanThreads) void big_scan(ClusterArgs a, BigWs w) {
+    constexpr int kTileCells = kScanThreads * kUnroll;
     __shared__ int s_wave[kScanThreads / 64];
+    __shared__ int s_tile[kTileCells];
+    __shared__ int s_carry;
     const int f = blockIdx.x, tid = threadIdx.x;
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig]) return;
     const int32_t ncell = rec[kNcell];
     int32_t *cs = w.cstart + cell_base(a.offsets, f);
-    const int32_t chunk = (ncell + kScanThreads - 1) / kScanThreads;
-    const int32_t c0 = min(tid * chunk, ncell), c1 = min(c0 + chunk, ncell);
-    int sum = 0;
-    for (int32_t c = c0; c < c1; ++c) sum += cs[c];
-    int run = block_exclusive_scan(sum, s_wave);
-    for (int32_t c = c0; c < c1; ++c) {
-        const int v = cs[c];
-        cs[c] = run;
-        run += v;
+    int carry = 0;
+    for (int32_t t0 = 0; t0 < ncell; t0 += kTileCells) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int32_t c = t0 + u * kScanThreads + tid;
+            s_tile[u * kScanThreads + tid] = c < ncell ? cs[c] : 0;
+        }
+        __syncthreads();
+        int v[kUnroll], sum = 0;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            v[u] = s_tile[tid * kUnroll + u];
+            sum += v[u];
+        }
+        int run = carry + block_exclusive_scan(sum, s_wave);  // ends with a barrier
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            s_tile[tid * kUnroll + u] = run;
+            run += v[u];
+        }
+        if (tid == kScanThreads - 1) s_carry = run;
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int32_t c = t0 + u * kScanThreads + tid;
+            if (c < ncell) cs[c] = s_tile[u * kScanThreads + tid];
+        }
+        carry = s_carry;
+        __syncthreads();  // s_tile and s_carry are rewritten by the next tile
     }
-    if (tid == kScanThreads - 1) cs[ncell] = run;
+    if (tid == 0) cs[ncell] = carry;
 }
 
 __global__ __launch_bounds__(kBlock) void big_scatter(ClusterArgs a, BigWs w) {
@@ -512,7 +548,7 @@ hipError_t launch_cluster_big(const ClusterArgs &a, void *workspace, hipStream_t
     const BigWs w = carve(workspace, a.n_frames, a.total);
     const int64_t cells = 2 * (int64_t)a.total + 2 * (int64_t)a.n_frames;
     const unsigned pts = blocks_for(a.total);
-    hipLaunchKernelGGL(big_prep, dim3(a.n_frames), dim3(kBlock), 0, stream, a, w);
+    hipLaunchKernelGGL(big_prep, dim3(a.n_frames), dim3(kPrepThreads), 0, stream, a, w);
     if (a.total > 0) {
         hipLaunchKernelGGL(big_hist, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_scan, dim3(a.n_frames), dim3(kScanThreads), 0, stream, a, w);
