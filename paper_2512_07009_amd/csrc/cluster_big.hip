@@ -332,8 +332,14 @@ __global__ __launch_bounds__(kBlock) void big_core(ClusterArgs a, BigWs w) {
             const int dxm = g.dx[dy < 0 ? -dy : dy];
             const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
             const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
-            for (int32_t q = cs[ry * g.ncx + rx0]; q < q1 && cnt < a.min_pts; ++q)
-                cnt += within(v, S[q], r) ? 1 : 0;
+            int32_t q = cs[ry * g.ncx + rx0];
+            // four loads in flight per step (the count may pass min_pts)
+            for (; q + 4 <= q1 && cnt < a.min_pts; q += 4) {
+                const int2 s0 = S[q], s1 = S[q + 1], s2 = S[q + 2], s3 = S[q + 3];
+                cnt += (within(v, s0, r) ? 1 : 0) + (within(v, s1, r) ? 1 : 0) + (within(v, s2, r) ? 1 : 0) +
+                       (within(v, s3, r) ? 1 : 0);
+            }
+            for (; q < q1 && cnt < a.min_pts; ++q) cnt += within(v, S[q], r) ? 1 : 0;
         }
     }
     const bool core = cnt >= a.min_pts;
