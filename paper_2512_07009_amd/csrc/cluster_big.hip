@@ -518,16 +518,26 @@ __global__ __launch_bounds__(kBlock) void big_border(ClusterArgs a, BigWs w) {
         const int dxm = g.dx[dy < 0 ? -dy : dy];
         const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
         const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
-        for (int32_t q = cs[ry * g.ncx + rx0]; q < q1; ++q) {
-            if (!core[q]) continue;
-            const int2 qq = S[q];
-            const int32_t d2 = sq_dist_clamped(v, qq, r);
-            if (d2 > r.e2) continue;
-            const bool take = core_before(d2, qq.y, qq.x, best_d2, by, bx);
-            best = take ? q : best;
-            best_d2 = take ? d2 : best_d2;
-            by = take ? qq.y : by;
-            bx = take ? qq.x : bx;
+        // four candidates loaded per step (indices past the span repeat its
+        // last point and are masked), then tested in order
+        for (int32_t q = cs[ry * g.ncx + rx0]; q < q1; q += 4) {
+            int2 qv[4];
+            bool cv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int32_t qi = min(q + u, q1 - 1);
+                qv[u] = S[qi];
+                cv[u] = (q + u < q1) & (core[qi] != 0);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int32_t d2 = sq_dist_clamped(v, qv[u], r);
+                const bool take = cv[u] & (d2 <= r.e2) & core_before(d2, qv[u].y, qv[u].x, best_d2, by, bx);
+                best = take ? q + u : best;
+                best_d2 = take ? d2 : best_d2;
+                by = take ? qv[u].y : by;
+                bx = take ? qv[u].x : bx;
+            }
         }
     }
     const int32_t o = w.ssid[p];
