@@ -141,6 +141,30 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
 size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h);
 
 /*
+ * density_frames_noalloc - density_frames for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid allocation.
+ *
+ * Arguments, result and accuracy are those of density_frames (the same plan
+ * and kernels, so the same bits), without the workspace: a launch split into
+ * bird slices keeps its partial grids in a static scratch array of the
+ * library, 16 MiB per device (n_frames * slices * grid_w * grid_h * 4 bytes;
+ * density_frames_workspace() gives that size for a batch shape).  The call
+ * allocates nothing and makes no host-device copy or synchronisation
+ * (FLOCK_VALIDATE is ignored here).
+ * Errors: FLOCK_ENOMEM, with nothing enqueued, when the batch needs more
+ * partial-grid bytes than the scratch holds; otherwise as density_frames.
+ * Every call on one device shares that device's scratch: calls that overlap
+ * in time on one device (concurrent streams, or threads) race and must be
+ * serialised by the caller.  Every byte a call reads from the scratch it has
+ * written first, so nothing needs clearing between calls.
+ */
+flock_status density_frames_noalloc(const int32_t *xy, const int32_t *offsets, int32_t n_frames,
+                                    int32_t total, int32_t max_frame_points, int32_t width_px,
+                                    int32_t height_px, int32_t grid_w, int32_t grid_h, float sigma_px,
+                                    float *density, void *stream);
+
+/*
  * heatmap_frames - heatmap analytics of every frame's density grid.
  *
  * The clustering module of Section 2.3 thresholds the density heatmaps and

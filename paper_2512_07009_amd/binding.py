@@ -48,6 +48,8 @@ def lib() -> ctypes.CDLL:
         L.density_frames.restype = i32
         L.cluster_frames_workspace.argtypes = [i32, i32, i32]
         L.cluster_frames_workspace.restype = sz
+        L.density_frames_noalloc.argtypes = [p, p, i32, i32, i32, i32, i32, i32, i32, ctypes.c_float, p, p]
+        L.density_frames_noalloc.restype = i32
         L.density_frames_workspace.argtypes = [i32, i32, i32, i32]
         L.density_frames_workspace.restype = sz
         L.heatmap_frames.argtypes = [p, i32, i32, i32, ctypes.c_double, ctypes.c_float, i32,

@@ -19,15 +19,13 @@
 
 namespace {
 
-thread_local std::string g_error;
+thread_local char g_error[512];
 
 flock_status fail(flock_status st, const char *fmt, ...) {
-    char buf[512];
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
+    vsnprintf(g_error, sizeof g_error, fmt, ap);
     va_end(ap);
-    g_error = buf;
     return st;
 }
 
@@ -170,7 +168,7 @@ ClusterPlan plan_cluster(int32_t max_frame_points, size_t lds_limit) {
 
 extern "C" {
 
-const char *flock_last_error(void) { return g_error.c_str(); }
+const char *flock_last_error(void) { return g_error; }
 
 const char *flock_version(void) { return "flock 0.1.0 gfx950"; }
 
@@ -179,7 +177,7 @@ size_t cluster_frames_workspace(int32_t n_frames, int32_t total, int32_t max_fra
     const DeviceInfo *dev = nullptr;
     size_t lds = 160 * 1024;
     if (device_info(&dev) == FLOCK_OK) lds = dev->lds_per_block;
-    g_error.clear();
+    g_error[0] = '\0';
     const ClusterPlan plan = plan_cluster(max_frame_points, lds);
     const bool big = max_frame_points == 0 || max_frame_points > plan.cap_points;
     return big ? flock::cluster_big_workspace(n_frames, total) : 0;
@@ -189,7 +187,7 @@ size_t density_frames_workspace(int32_t n_frames, int32_t total, int32_t grid_w,
     const DeviceInfo *dev = nullptr;
     int n_cus = 256;
     if (device_info(&dev) == FLOCK_OK) n_cus = dev->n_cus;
-    g_error.clear();
+    g_error[0] = '\0';
     return flock::density_workspace_bytes(n_frames, total, grid_w, grid_h, n_cus);
 }
 
@@ -197,7 +195,7 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
                             int32_t max_frame_points, int32_t eps_q, int32_t min_pts, int32_t *labels,
                             uint8_t *kind, int32_t *n_clusters, void *workspace, size_t workspace_bytes,
                             void *stream) {
-    g_error.clear();
+    g_error[0] = '\0';
     if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
     if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
     if (max_frame_points < 0) return fail(FLOCK_EINVAL, "max_frame_points = %d < 0", max_frame_points);
@@ -267,12 +265,18 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     return FLOCK_OK;
 }
 
-flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
-                            int32_t max_frame_points, int32_t width_px, int32_t height_px,
-                            int32_t grid_w, int32_t grid_h,
-                            float sigma_px, float *density, void *workspace, size_t workspace_bytes,
-                            void *stream) {
-    g_error.clear();
+}  // extern "C"
+
+namespace {
+
+// density_frames and density_frames_noalloc: the same checks, plan and
+// kernels; they differ only in where a split launch keeps its partial grids
+// (the caller's workspace or a library allocation, or the static scratch).
+flock_status density_run(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
+                         int32_t max_frame_points, int32_t width_px, int32_t height_px, int32_t grid_w,
+                         int32_t grid_h, float sigma_px, float *density, void *workspace,
+                         size_t workspace_bytes, bool noalloc, void *stream) {
+    g_error[0] = '\0';
     if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
     if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
     if (max_frame_points < 0) return fail(FLOCK_EINVAL, "max_frame_points = %d < 0", max_frame_points);
@@ -293,7 +297,9 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     flock_status st = device_info(&dev);
     if (st != FLOCK_OK) return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (validate_requested()) {
+    // the debug check copies to the host and synchronises: never on the
+    // allocation-free entry point, which may run under graph capture
+    if (!noalloc && validate_requested()) {
         st = validate_batch(xy, offsets, n_frames, total, s);
         if (st != FLOCK_OK) return st;
     }
@@ -314,17 +320,30 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     if (plan.blocks > 0x7fffffffLL) return fail(FLOCK_EUNSUPPORTED, "batch too large for one launch");
     // a split launch keeps partial grids in the workspace
     const size_t need = plan.split > 1 ? (size_t)n_frames * plan.split * (size_t)grid_w * grid_h * sizeof(float) : 0;
-    if (workspace && workspace_bytes < need)
-        return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
-    if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
     void *ws = workspace;
     hipError_t err = hipSuccess;
-    if (need > 0 && !ws) {
-        err = hipMallocAsync(&ws, need, s);
-        if (err != hipSuccess) return hip_fail(err, "workspace allocation");
+    if (noalloc) {
+        if (need > flock::kDensityScratchBytes)
+            return fail(FLOCK_ENOMEM,
+                        "this batch needs %zu bytes of partial grids, beyond the %zu bytes of static scratch "
+                        "of the allocation-free entry point (density_frames with a workspace takes it)",
+                        need, flock::kDensityScratchBytes);
+        ws = nullptr;
+        if (need > 0) {
+            err = flock::density_static_scratch(&ws);
+            if (err != hipSuccess || !ws) return hip_fail(err, "static scratch address");
+        }
+    } else {
+        if (workspace && workspace_bytes < need)
+            return fail(FLOCK_ENOMEM, "workspace of %zu bytes < %zu needed", workspace_bytes, need);
+        if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
+        if (need > 0 && !ws) {
+            err = hipMallocAsync(&ws, need, s);
+            if (err != hipSuccess) return hip_fail(err, "workspace allocation");
+        }
     }
     err = flock::launch_density(a, plan, static_cast<float *>(ws), s);
-    if (need > 0 && !workspace) {
+    if (!noalloc && need > 0 && !workspace) {
         const hipError_t ferr = hipFreeAsync(ws, s);
         if (err == hipSuccess) err = ferr;
     }
@@ -332,8 +351,29 @@ flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     return FLOCK_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+flock_status density_frames(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
+                            int32_t max_frame_points, int32_t width_px, int32_t height_px,
+                            int32_t grid_w, int32_t grid_h,
+                            float sigma_px, float *density, void *workspace, size_t workspace_bytes,
+                            void *stream) {
+    return density_run(xy, offsets, n_frames, total, max_frame_points, width_px, height_px, grid_w, grid_h,
+                       sigma_px, density, workspace, workspace_bytes, false, stream);
+}
+
+flock_status density_frames_noalloc(const int32_t *xy, const int32_t *offsets, int32_t n_frames, int32_t total,
+                                    int32_t max_frame_points, int32_t width_px, int32_t height_px,
+                                    int32_t grid_w, int32_t grid_h, float sigma_px, float *density,
+                                    void *stream) {
+    return density_run(xy, offsets, n_frames, total, max_frame_points, width_px, height_px, grid_w, grid_h,
+                       sigma_px, density, nullptr, 0, true, stream);
+}
+
 size_t roi_filter_frames_workspace(int32_t n_frames, int32_t total) {
-    g_error.clear();
+    g_error[0] = '\0';
     return n_frames > 0 ? flock::roi_workspace_bytes(total) : 0;  // flags, block counts and bases, staging
 }
 
@@ -341,7 +381,7 @@ flock_status roi_filter_frames(const int32_t *xy, const int32_t *offsets, int32_
                                const int32_t *roi_xy, int32_t n_vertices, int32_t *counts, int32_t *out_xy,
                                int32_t *out_offsets, int32_t *out_index, void *workspace,
                                size_t workspace_bytes, void *stream) {
-    g_error.clear();
+    g_error[0] = '\0';
     if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
     if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
     if (n_vertices < 3 || n_vertices > flock::kRoiMaxVertices)
@@ -406,7 +446,7 @@ flock_status roi_filter_frames(const int32_t *xy, const int32_t *offsets, int32_
 }
 
 size_t drinker_proximity_frames_workspace(int32_t n_frames, int32_t total) {
-    g_error.clear();
+    g_error[0] = '\0';
     return n_frames > 0 ? flock::drink_workspace_bytes(total) : 0;  // block counts and bases
 }
 
@@ -414,7 +454,7 @@ flock_status drinker_proximity_frames(const int32_t *xy, const int32_t *offsets,
                                       const int32_t *lines, int32_t n_lines, int32_t threshold_q,
                                       uint8_t *drinking, int32_t *line, int32_t *counts, void *workspace,
                                       size_t workspace_bytes, void *stream) {
-    g_error.clear();
+    g_error[0] = '\0';
     if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
     if (total < 0) return fail(FLOCK_EINVAL, "total = %d < 0", total);
     if (n_lines < 1 || n_lines > flock::kDrinkMaxLines)
@@ -485,7 +525,7 @@ flock_status drinker_proximity_frames(const int32_t *xy, const int32_t *offsets,
 }
 
 size_t heatmap_frames_workspace(int32_t n_frames, int32_t grid_w, int32_t grid_h) {
-    g_error.clear();
+    g_error[0] = '\0';
     // enough for either path (which one runs depends on the device's LDS)
     return std::max(flock::heatmap_workspace_bytes(n_frames, grid_w, grid_h),
                     flock::heatmap_frame_workspace_bytes(n_frames, grid_w, grid_h));
@@ -495,7 +535,7 @@ flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid
                             double cell_area_px2, float threshold, int32_t connectivity, int32_t *labels,
                             int32_t *n_components, double *entropy, double *degree, int32_t *comp_cells,
                             double *comp_mass, void *workspace, size_t workspace_bytes, void *stream) {
-    g_error.clear();
+    g_error[0] = '\0';
     if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
     if (grid_w < 1 || grid_h < 1 || grid_w > 4096 || grid_h > 4096)
         return fail(FLOCK_EINVAL, "grid %d x %d outside 1..4096", grid_w, grid_h);
@@ -562,7 +602,7 @@ flock_status heatmap_frames(const float *density, int32_t n_frames, int32_t grid
 }
 
 size_t mask_components_frames_workspace(int32_t n_frames, int32_t width, int32_t height, int32_t connectivity) {
-    g_error.clear();
+    g_error[0] = '\0';
     return flock::mask_workspace_bytes(n_frames, width, height, connectivity);
 }
 
@@ -572,7 +612,7 @@ flock_status mask_components_frames(const float *prob, int32_t n_frames, int32_t
                                     int32_t *comp_label, int32_t *comp_area, int32_t *comp_box,
                                     double *comp_centroid, int32_t *comp_xy, float *comp_score, void *workspace,
                                     size_t workspace_bytes, void *stream) {
-    g_error.clear();
+    g_error[0] = '\0';
     if (n_frames < 0) return fail(FLOCK_EINVAL, "n_frames = %d < 0", n_frames);
     if (width < 1 || height < 1 || width > 32768 || height > 32768)
         return fail(FLOCK_EINVAL, "frame %d x %d outside 1..32768", width, height);

@@ -48,6 +48,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <algorithm>
+#include <mutex>
 
 #include "internal.h"
 
@@ -685,7 +686,33 @@ void gather_split(int32_t n_frames, int32_t total, long long regions, int n_cus,
     *split = (int)sp;
 }
 
+// Scratch of the allocation-free entry point (density_frames_noalloc): the
+// partial grids of split launches, in a file-scope device array instead of a
+// workspace.  Each device holds its own copy for the life of the process.
+// In host code `scratch` names a host-side stand-in, never the device memory:
+// its device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[kDensityScratchBytes];
+
+constexpr int kScratchDevices = 64;
+std::once_flag g_scratch_once[kScratchDevices];
+void *g_scratch_ptr[kScratchDevices];
+hipError_t g_scratch_err[kScratchDevices];
+
 }  // namespace
+
+hipError_t density_static_scratch(void **ptr) {
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+    std::call_once(g_scratch_once[dev], [dev] {
+        void *p = nullptr;
+        g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? p : nullptr;
+    });
+    *ptr = g_scratch_ptr[dev];
+    return g_scratch_err[dev];
+}
 
 size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h, int n_cus) {
     if (n_frames <= 0 || grid_w < 1 || grid_h < 1) return 0;

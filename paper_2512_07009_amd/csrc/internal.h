@@ -79,6 +79,11 @@ DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit);
 // batch shape and grid only, and bounds every plan for that shape.
 size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h, int n_cus);
 hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, float *partial, hipStream_t stream);
+// The allocation-free entry point's scratch: a file-scope device array of
+// kDensityScratchBytes per device (the partial grids of split launches).
+// Returns its address on the current device (looked up once per device).
+constexpr size_t kDensityScratchBytes = (size_t)16 << 20;
+hipError_t density_static_scratch(void **ptr);
 
 // ----------------------------------------------------------------------------
 // Heatmap analytics

@@ -81,6 +81,25 @@ def test_density_rejects_bad_arguments(kwargs, needle):
     assert needle in binding.lib().flock_last_error().decode()
 
 
+def _density_noalloc(n_frames=1, total=4, max_fp=0, w=1920, h=1080, gx=128, gy=72, sigma=30.0, xy=FAKE,
+                     offsets=FAKE, out=FAKE):
+    return binding.lib().density_frames_noalloc(xy, offsets, n_frames, total, max_fp, w, h, gx, gy, sigma,
+                                                out, None)
+
+
+@pytest.mark.parametrize("kwargs,needle", [
+    (dict(n_frames=-1), "n_frames"),
+    (dict(gy=5000), "grid"),
+    (dict(sigma=math.nan), "sigma"),
+    (dict(out=None), "non-NULL"),
+    (dict(xy=FAKE4), "aligned"),
+])
+def test_density_noalloc_rejects_bad_arguments(kwargs, needle):
+    assert _density_noalloc(**kwargs) == binding.FLOCK_EINVAL
+    assert needle in binding.lib().flock_last_error().decode()
+    assert _density_noalloc(n_frames=0, total=0, xy=None, offsets=None, out=None) == 0
+
+
 def _heatmap(n_frames=1, gw=128, gh=72, area=225.0, thr=1e-4, conn=8, dens=FAKE, labels=FAKE, ncomp=FAKE,
              ent=FAKE, deg=FAKE, cells=FAKE, mass=FAKE):
     return binding.lib().heatmap_frames(dens, n_frames, gw, gh, area, thr, conn, labels, ncomp, ent, deg,

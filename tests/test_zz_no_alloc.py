@@ -1,0 +1,77 @@
+"""The allocation-free density entry point (density_frames_noalloc) against
+density_frames, through the C ABI: two calls in a row on one device (the
+second with a smaller batch, so the static scratch holds the first call's
+partial grids when the second starts), then a batch whose partial grids do
+not fit the scratch, which is refused with nothing enqueued."""
+
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2512_07009_amd as flock
+from paper_2512_07009_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+DENSITY_RTOL_OF_MAX = 1e-3
+
+
+def _args(dxy, doff, F, T, max_fp, w, h, gx, gy, sigma, out):
+    return (ctypes.c_void_p(dxy.data_ptr()), ctypes.c_void_p(doff.data_ptr()), F, T, max_fp, w, h, gx, gy,
+            ctypes.c_float(sigma), ctypes.c_void_p(out.data_ptr()))
+
+
+def _frames(seed, counts, w, h):
+    rng = np.random.default_rng(seed)
+    return wl.pack([np.stack([rng.integers(0, 16 * w, n), rng.integers(0, 16 * h, n)], 1).astype(np.int32)
+                    for n in counts])
+
+
+# (seed, birds per frame, frame px, grid, sigma): a one-frame 4K house batch
+# split into bird slices, then a smaller 1080p batch, also split
+CASES = [(41, [30000], 3840, 2160, 512, 288, 20.0), (42, [4000, 2500], 1920, 1080, 128, 72, 30.0)]
+
+
+def test_noalloc_matches_density_frames_gpu():
+    lib = flock.lib()
+    print("density_frames_noalloc: two calls, large batch then small", flush=True)
+    for seed, counts, w, h, gx, gy, sigma in CASES:
+        xy, off = _frames(seed, counts, w, h)
+        F, T = len(counts), xy.shape[0]
+        assert lib.density_frames_workspace(F, T, gx, gy) > 0, "the case must use the scratch"
+        dxy = torch.from_numpy(xy).cuda()
+        doff = torch.from_numpy(off).cuda()
+        want = torch.full((F, gy, gx), -1.0, dtype=torch.float32, device="cuda")
+        got = torch.full((F, gy, gx), -2.0, dtype=torch.float32, device="cuda")
+        max_fp = int(max(counts))
+        st = lib.density_frames(*_args(dxy, doff, F, T, max_fp, w, h, gx, gy, sigma, want), None, 0, None)
+        assert st == 0, lib.flock_last_error().decode()
+        st = lib.density_frames_noalloc(*_args(dxy, doff, F, T, max_fp, w, h, gx, gy, sigma, got), None)
+        assert st == 0, lib.flock_last_error().decode()
+        torch.cuda.synchronize()
+        a, b = want.cpu().numpy(), got.cpu().numpy()
+        for f in range(F):
+            m = float(a[f].max())
+            assert m > 0
+            assert np.abs(b[f].astype(np.float64) - a[f]).max() <= DENSITY_RTOL_OF_MAX * m, f"frame {f}"
+        # the same plan and kernels: the same bits
+        assert np.array_equal(a, b), f"{counts} birds on {gx}x{gy}: differs from density_frames"
+        print(f"  {F} frames x {counts} birds on {gx}x{gy}: identical", flush=True)
+
+
+def test_noalloc_refuses_beyond_scratch_gpu(monkeypatch):
+    """64 slices of a 512 x 288 grid need 37.7 MB of partial grids: refused."""
+    monkeypatch.setenv("FLOCK_DENSITY_SPLIT", "64")
+    lib = flock.lib()
+    xy, off = _frames(43, [20000], 3840, 2160)
+    dxy = torch.from_numpy(xy).cuda()
+    doff = torch.from_numpy(off).cuda()
+    out = torch.full((1, 288, 512), -3.0, dtype=torch.float32, device="cuda")
+    st = lib.density_frames_noalloc(*_args(dxy, doff, 1, xy.shape[0], 20000, 3840, 2160, 512, 288, 20.0, out),
+                                    None)
+    assert st == flock.binding.FLOCK_ENOMEM
+    assert "static scratch" in lib.flock_last_error().decode()
+    torch.cuda.synchronize()
+    assert (out == -3.0).all().item(), "a refused call must leave the output untouched"
