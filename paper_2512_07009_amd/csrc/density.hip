@@ -240,8 +240,9 @@ constexpr int kGWaves = 8;                 // waves per workgroup (two per SIMD)
 constexpr int kGThreads = 64 * kGWaves;
 constexpr int kGStep = 32;                 // birds per MFMA k-step (16 x 16 x 32)
 constexpr int kGRedTiles = 8;              // 16 x 16 tiles per round of the cross-wave sum
+constexpr int kGRing = 128;                // staged birds per wave (one k-step left over + one round)
 constexpr int kGMaxTableBytes = 96 * 1024; // both factor tables
-constexpr int kGMinWaveBirds = 192;        // birds per wave, at least, when a launch splits frames
+constexpr int kGMinWaveBirds = 48;         // kept birds per wave, at least, when a launch splits frames
 constexpr int32_t kGFar = 1 << 28;         // bird term that clamps every row to a zero entry
 
 typedef float float4v __attribute__((ext_vector_type(4)));
@@ -348,12 +349,19 @@ __device__ __forceinline__ void contract_y(float4v (&acc)[TM][TN], const half8 (
     }
 }
 
-// One workgroup of four waves.  A work item is (frame, output region of
-// 16 TM rows x 16 TN columns, slice of the frame's birds); `waves` waves share
-// an item, each taking a contiguous part of the slice, and their tiles are
-// added in a fixed order at the end (deterministic).  Every wave stages its
-// own birds (lane = bird) and needs no barrier until that final sum.  With
-// split > 1 the slices' grids go to `partial` for a second kernel to add.
+// A work item is (frame, output region of 16 TM rows x 16 TN columns, slice
+// of the frame's birds); `waves` waves of a workgroup share an item, each
+// taking a contiguous part of the slice, and their tiles are added in a fixed
+// order at the end (deterministic).  With split > 1 the slices' grids go to
+// `partial` for a second kernel to add.
+//
+// Only birds whose window of cells (G - j .. G + j on both axes) meets the
+// region contribute to it: every other bird's factors there are table zeros.
+// Each wave reads its birds 64 at a time (one per lane), keeps the ones that
+// meet the region, in input order, in a ring of staged birds in LDS (ballot
+// ranks), and runs a k-step whenever 32 are staged; the last step is padded
+// with birds whose factors are all zero.  No barrier is needed until the
+// final sum.
 template <int TM, int TN, int PW>
 __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) void density_gather_kernel(DensityArgs a, GatherGeom gg, int regions_y,
                                                                    int regions_x, int split, int waves,
@@ -362,7 +370,6 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-
 
     // this wave's item and its part of the item's birds
     const int per_wg = kGWaves / waves;
@@ -390,10 +397,15 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
     const int32_t p1 = k0 + (int32_t)((int64_t)(k1 - k0) * (part + 1) / waves);
     const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
 
-    GBird *stage = reinterpret_cast<GBird *>(lds + gg.table_bytes) + wave * 2 * kGStep;
+    GBird *ring = reinterpret_cast<GBird *>(lds + gg.table_bytes) + wave * kGRing;
     const float inv_cy = 1.0f / (float)gg.ay.c, inv_cx = 1.0f / (float)gg.ax.c;
     const int r16 = lane & 15, grp = lane >> 4;
     const int32_t yoff = 4 * (row0 + r16), xoff = 4 * (col0 + r16);
+    // a bird in cell G meets rows [row0, row0 + 16 TM) when
+    // row0 - j <= G <= row0 + 16 TM - 1 + j, i.e. when its staged
+    // g = 4 (j + 17 - G) lies in [4 (17 - 16 TM + 1 - row0), 4 (2 j + 17 - row0)]
+    const int32_t gy_lo = 4 * (18 - 16 * TM - row0), gy_hi = 4 * (2 * gg.ay.j + 17 - row0);
+    const int32_t gx_lo = 4 * (18 - 16 * TN - col0), gx_hi = 4 * (2 * gg.ax.j + 17 - col0);
 
     float4v acc[TM][TN];
 #pragma unroll
@@ -401,48 +413,9 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
 #pragma unroll
         for (int t = 0; t < TN; ++t) acc[m][t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
 
-    // Software pipeline over k-steps of 32 birds: while the matrix cores run
-    // step s, the wave stages the birds of step s + 1 (lane = bird and axis,
-    // coordinates fetched two steps ahead) and gathers that step's x
-    // operands, so both kinds of work are in flight in one instruction stream.
-    const int32_t nsteps = (p1 - p0 + kGStep - 1) / kGStep;
-    const int sbird = lane & (kGStep - 1);
-    const bool sx = lane >= kGStep;  // lanes 0-31 stage the y axis, 32-63 the x axis
-    const GatherAxis &sax = sx ? gg.ax : gg.ay;
-    const float sinv = sx ? inv_cx : inv_cy;
-    auto coord = [&](int32_t t) -> int32_t {
-        const int32_t k = p0 + t * kGStep + sbird;
-        return k < p1 ? (sx ? P[k].x : P[k].y) : INT_MIN;
-    };
-    auto put = [&](int32_t t, int32_t q) {
-        int32_t rb = sax.tab, g = kGFar;  // beyond the slice: factors 0
-        if (q != INT_MIN) stage_axis<PW>(q, sax, sinv, &rb, &g);
-        reinterpret_cast<int2 *>(stage + (t & 1) * kGStep + sbird)[sx] = make_int2(rb, g);
-        // a wave's LDS accesses stay in program order; the fences keep the
-        // compiler from moving them
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    };
-    auto x_operands = [&](int32_t t, half8 (&bx)[TN]) {
-        const GBird *sb = stage + (t & 1) * kGStep + 8 * grp;  // this lane's eight birds of step t
-        int32_t rbx[8], vx[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int2 q = reinterpret_cast<const int2 *>(sb + e)[1];
-            rbx[e] = q.x;
-            vx[e] = q.y + xoff;
-        }
-        operands_x<TN, PW>(bx, rbx, vx, lds);
-    };
-
-    // the first coordinates are in flight while the tables are built
-    int32_t q0 = 0, qa = 0, qb = 0;
-    if (nsteps > 0) {
-        q0 = coord(0);
-        qa = coord(1);
-        qb = coord(2);
-    }
+    // the first round's coordinates are in flight while the tables are built
+    int2 qn = make_int2(0, 0);
+    if (p0 + lane < p1) qn = P[p0 + lane];
     // the factor tables (exact: every distance is a multiple of 1/32 px), one
     // row per thread: its PW factors in registers, then its pairs
     auto build = [&](const GatherAxis &t) {
@@ -473,16 +446,58 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
     build(gg.ay);
     if (gg.ax.tab != gg.ay.tab) build(gg.ax);
     __syncthreads();  // tables written
-    if (nsteps > 0) put(0, q0);
-    half8 bx[TN];
-    if (nsteps > 0) x_operands(0, bx);
-    for (int32_t st = 0; st < nsteps; ++st) {
-        put(st + 1, qa);  // harmless past the last step: every factor 0
-        qa = qb;
-        qb = coord(st + 3);
-        half8 bxn[TN];
-        x_operands(st + 1, bxn);
-        const GBird *sb = stage + (st & 1) * kGStep + 8 * grp;
+
+    // a wave's LDS accesses stay in program order; the fences keep the
+    // compiler from moving them across the ring's writes and reads
+    auto wave_sync = [] {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+    const uint64_t below = (1ull << lane) - 1ull;
+    int32_t head = 0, tail = 0;  // ring positions, taken modulo kGRing
+    int32_t next = p0;           // first bird of the next round
+    // stage rounds of 64 birds until a k-step's worth meets the region (or
+    // the birds run out); the last, partial step is filled with birds whose
+    // factors are all zero
+    auto fill = [&] {
+        while (tail - head < kGStep && next < p1) {
+            const int2 q = qn;
+            const bool have = next + lane < p1;
+            next += 64;
+            if (next + lane < p1) qn = P[next + lane];  // the following round in flight
+            GBird gb{gg.ay.tab, kGFar, gg.ax.tab, kGFar};
+            bool keep = false;
+            if (have) {
+                stage_axis<PW>(q.y, gg.ay, inv_cy, &gb.rb_y, &gb.g_y);
+                stage_axis<PW>(q.x, gg.ax, inv_cx, &gb.rb_x, &gb.g_x);
+                keep = (gb.g_y >= gy_lo) & (gb.g_y <= gy_hi) & (gb.g_x >= gx_lo) & (gb.g_x <= gx_hi);
+            }
+            const uint64_t m = __ballot(keep);
+            if (keep) ring[(tail + __popcll(m & below)) & (kGRing - 1)] = gb;
+            tail += __popcll(m);
+        }
+        if (tail > head && tail - head < kGStep) {
+            if (lane < kGStep && head + lane >= tail)
+                ring[(head + lane) & (kGRing - 1)] = GBird{gg.ay.tab, kGFar, gg.ax.tab, kGFar};
+            tail = head + kGStep;
+        }
+        wave_sync();
+    };
+    fill();
+    while (tail > head) {  // wave-uniform
+        const GBird *sb = ring + (head & (kGRing - 1)) + 8 * grp;  // this lane's eight birds of the step
+        half8 bx[TN];
+        {
+            int32_t rbx[8], vx[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int2 q = reinterpret_cast<const int2 *>(sb + e)[1];
+                rbx[e] = q.x;
+                vx[e] = q.y + xoff;
+            }
+            operands_x<TN, PW>(bx, rbx, vx, lds);
+        }
         int32_t rby[8], vy[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -491,8 +506,9 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
             vy[e] = q.y + yoff;
         }
         contract_y<TM, TN, PW>(acc, bx, rby, vy, lds);
-#pragma unroll
-        for (int n = 0; n < TN; ++n) bx[n] = bxn[n];
+        head += kGStep;
+        wave_sync();  // the step's reads are done before the ring is written again
+        fill();
     }
 
     const size_t cells = (size_t)a.grid_h * a.grid_w;
@@ -569,10 +585,11 @@ struct Shape {
 // most 12 tiles per region)
 constexpr Shape kShapes[] = {{1, 1}, {1, 2}, {2, 1}, {2, 2}, {1, 4}, {3, 2},
                              {2, 4}, {3, 4}, {4, 2}, {5, 2}, {4, 1}, {5, 1}};
-// instantiated region shapes of the gather path (tiles of 16 x 16; at most 40
-// tiles per region)
+// instantiated region shapes of the gather path (tiles of 16 x 16; at most 36
+// tiles per region, so that the accumulators and operands fit the registers
+// of two waves per SIMD without spilling)
 constexpr Shape kGShapes[] = {{1, 1}, {2, 2}, {1, 4}, {4, 1}, {2, 4}, {4, 2}, {3, 4},
-                              {4, 4}, {5, 4}, {5, 8}, {9, 2}, {9, 4}, {3, 8}, {4, 8}};
+                              {4, 4}, {5, 4}, {9, 2}, {9, 4}, {3, 8}, {4, 8}};
 
 Geometry make_geometry(const DensityArgs &a) {
     Geometry g;
@@ -617,7 +634,7 @@ bool make_gather_geom(const DensityArgs &a, GatherGeom *gg) {
     gg->ay.tab = 0;
     gg->ax.tab = shared ? 0 : (int32_t)ty;
     gg->table_bytes = (int)(ty + tx);
-    const int stage = kGWaves * 2 * kGStep * (int)sizeof(GBird);
+    const int stage = kGWaves * kGRing * (int)sizeof(GBird);
     gg->lds_bytes = std::max(gg->table_bytes + stage, kGWaves * kGRedTiles * 256 * 4);
     const double s = (double)a.sigma_px;
     gg->neg_k = (float)(-1.4426950408889634 / (2.0 * s * s));
@@ -630,17 +647,34 @@ long long shape_regions(const Shape &sh, int tile, int grid_w, int grid_h) {
            ((grid_w + (long long)tile * sh.rn - 1) / ((long long)tile * sh.rn));
 }
 
-// Gather-path region shape: least padded area, then fewest regions.
-Shape gather_shape(int grid_w, int grid_h) {
+// Share of a frame's birds whose window of 2 j + 1 cells meets one region
+// of `rows` grid rows, `nreg` regions along the axis: about 1 + 2 j / rows
+// regions per bird, at most all of them.
+double meet_share(int j, int rows, long long nreg) {
+    return std::min((double)nreg, 1.0 + 2.0 * j / rows) / (double)nreg;
+}
+
+long long axis_regions(int grid_n, int rows) { return (grid_n + rows - 1) / rows; }
+
+// Modelled SIMD cycles of one 32-bird k-step on a region: per lane a pair
+// read (read, clamp, address, pack: about 112 cycles for its eight birds)
+// for every two tile rows of each axis, and one 16-cycle MFMA per tile.
+double step_cycles(const Shape &sh) { return 112.0 * ((sh.rm + 1) / 2 + (sh.rn + 1) / 2) + 16.0 * sh.rm * sh.rn; }
+
+// Gather-path region shape of least modelled cost per frame: each bird's
+// k-step share on every region its window meets, the test that keeps or
+// drops every bird on every region (about 3 cycles a bird), and a fixed cost
+// per region (tables, the final sum and the stores).
+Shape gather_shape(int jy, int jx, int grid_w, int grid_h, double birds) {
     Shape best = kGShapes[0];
-    long long best_area = -1, best_regions = 0;
+    double best_cost = 1e300;
     for (const Shape &sh : kGShapes) {
-        const long long r = shape_regions(sh, 16, grid_w, grid_h);
-        const long long area = r * sh.rm * sh.rn;
-        if (best_area < 0 || area < best_area || (area == best_area && r < best_regions)) {
+        const long long ry = axis_regions(grid_h, 16 * sh.rm), rx = axis_regions(grid_w, 16 * sh.rn);
+        const double meets = ry * meet_share(jy, 16 * sh.rm, ry) * rx * meet_share(jx, 16 * sh.rn, rx);
+        const double cost = birds / kGStep * meets * step_cycles(sh) + (3.2 * birds + 4000.0) * (double)(ry * rx);
+        if (cost < best_cost * 0.999) {
             best = sh;
-            best_area = area;
-            best_regions = r;
+            best_cost = cost;
         }
     }
     return best;
@@ -652,27 +686,21 @@ int env_int(const char *name) {
 }
 
 // Waves per work item and slices per (frame, region) of a gather launch.  A
-// compute unit holds kGWaves waves (two per SIMD); with w waves per item an
-// item takes about 1/w of one wave's time, and the launch runs in
-// ceil(items * w / resident) rounds, so w minimises rounds / w (ties to fewer
-// waves, which add fewer tiles at the end).  FLOCK_DENSITY_WAVES / FLOCK_DENSITY_SPLIT
-// override (for tuning and tests).
-void gather_split(int32_t n_frames, int32_t total, long long regions, int n_cus, int *waves, int *split) {
+// compute unit holds kGWaves waves (two per SIMD).  Items are spread over
+// as few waves as fill the chip (the smallest power of two w, at most
+// kGWaves, with items * w >= resident waves): more waves per item only add
+// fixed costs (a table build per workgroup, the final sum across waves).
+// `birds` is the birds an item keeps (those whose window meets its region),
+// on average.  FLOCK_DENSITY_WAVES / FLOCK_DENSITY_SPLIT override (for
+// tuning and tests).
+void gather_split(int32_t n_frames, double birds, long long regions, int n_cus, int *waves, int *split) {
     const long long items = (long long)n_frames * regions;
     const long long resident = (long long)kGWaves * std::max(n_cus, 1);
     int w = 1;
-    double best = 1e300;
-    for (int c = 1; c <= kGWaves; c *= 2) {
-        const double cost = (double)((items * c + resident - 1) / resident) / c;
-        if (cost < best * 0.999) {
-            best = cost;
-            w = c;
-        }
-    }
+    while (w < kGWaves && items * w < resident) w *= 2;
     // slices only while one launch would leave most of the chip idle (the
     // partial grids cost traffic), up to one round of waves, with at least
-    // kGMinWaveBirds birds per wave
-    const double birds = n_frames > 0 ? (double)total / n_frames : 0.0;
+    // kGMinWaveBirds kept birds per wave
     long long sp = 1;
     if (2 * items * w < resident) {
         sp = resident / (items * w);
@@ -716,11 +744,18 @@ hipError_t density_static_scratch(void **ptr) {
 
 size_t density_workspace_bytes(int32_t n_frames, int32_t total, int32_t grid_w, int32_t grid_h, int n_cus) {
     if (n_frames <= 0 || grid_w < 1 || grid_h < 1) return 0;
-    const Shape sh = gather_shape(grid_w, grid_h);
-    int waves = 1, split = 1;
-    gather_split(n_frames, total, shape_regions(sh, 16, grid_w, grid_h), n_cus, &waves, &split);
-    if (split <= 1) return 0;
-    return (size_t)n_frames * split * (size_t)grid_w * grid_h * sizeof(float);
+    // the shape depends on the frame extent and sigma, which the query does
+    // not know: bound the split over every shape, with every bird kept (a
+    // split only shrinks when an item keeps fewer birds)
+    const double birds = (double)total / n_frames;
+    int most = 1;
+    for (const Shape &sh : kGShapes) {
+        int waves = 1, split = 1;
+        gather_split(n_frames, birds, shape_regions(sh, 16, grid_w, grid_h), n_cus, &waves, &split);
+        most = std::max(most, split);
+    }
+    if (most <= 1) return 0;
+    return (size_t)n_frames * most * (size_t)grid_w * grid_h * sizeof(float);
 }
 
 // Gather path whenever its tables apply; otherwise the recurrence path, whose
@@ -738,14 +773,17 @@ DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit) {
     const bool force_recur = path && std::strcmp(path, "recur") == 0;
     GatherGeom gg;
     if (!force_recur && make_gather_geom(a, &gg) && (size_t)gg.lds_bytes <= lds_limit) {
-        const Shape sh = gather_shape(a.grid_w, a.grid_h);
+        const double birds = a.n_frames > 0 ? (double)a.total / a.n_frames : 0.0;
+        const Shape sh = gather_shape(gg.ay.j, gg.ax.j, a.grid_w, a.grid_h, birds);
         DensityPlan p{};
         p.gather = 1;
         p.rm = sh.rm;
         p.rn = sh.rn;
         p.regions_y = (a.grid_h + 16 * sh.rm - 1) / (16 * sh.rm);
         p.regions_x = (a.grid_w + 16 * sh.rn - 1) / (16 * sh.rn);
-        gather_split(a.n_frames, a.total, (long long)p.regions_y * p.regions_x, n_cus, &p.waves, &p.split);
+        const double kept = birds * meet_share(gg.ay.j, 16 * sh.rm, p.regions_y) *
+                            meet_share(gg.ax.j, 16 * sh.rn, p.regions_x);
+        gather_split(a.n_frames, kept, (long long)p.regions_y * p.regions_x, n_cus, &p.waves, &p.split);
         const long long items = (long long)a.n_frames * p.regions_y * p.regions_x * p.split;
         const int per_wg = kGWaves / p.waves;
         p.blocks = (items + per_wg - 1) / per_wg;
@@ -816,7 +854,7 @@ hipError_t launch_density(const DensityArgs &a, const DensityPlan &p, float *par
     }
 #define FLOCK_GSHAPE(TM, TN) FLOCK_GSHAPE_PW(TM, TN, 32) FLOCK_GSHAPE_PW(TM, TN, 64)
         FLOCK_GSHAPE(1, 1) FLOCK_GSHAPE(2, 2) FLOCK_GSHAPE(1, 4) FLOCK_GSHAPE(4, 1) FLOCK_GSHAPE(2, 4)
-        FLOCK_GSHAPE(4, 2) FLOCK_GSHAPE(3, 4) FLOCK_GSHAPE(4, 4) FLOCK_GSHAPE(5, 4) FLOCK_GSHAPE(5, 8)
+        FLOCK_GSHAPE(4, 2) FLOCK_GSHAPE(3, 4) FLOCK_GSHAPE(4, 4) FLOCK_GSHAPE(5, 4)
         FLOCK_GSHAPE(9, 2) FLOCK_GSHAPE(9, 4) FLOCK_GSHAPE(3, 8) FLOCK_GSHAPE(4, 8)
 #undef FLOCK_GSHAPE
 #undef FLOCK_GSHAPE_PW

@@ -333,8 +333,11 @@ def test_density_bird_slices_gpu(split, monkeypatch):
     assert not got[2].any()
 
 
-def test_density_workspace_gpu():
+def test_density_workspace_gpu(monkeypatch):
+    """A launch split into three bird slices: a workspace one byte short is
+    refused; the caller's workspace and the library's own give the grid."""
     import ctypes
+    monkeypatch.setenv("FLOCK_DENSITY_SPLIT", "3")
     rng = np.random.default_rng(5)
     xy, off = wl.pack([np.stack([rng.integers(0, 16 * 1920, 4000), rng.integers(0, 16 * 1080, 4000)],
                                 1).astype(np.int32)])

@@ -30,8 +30,9 @@ def _frames(seed, counts, w, h):
 
 
 # (seed, birds per frame, frame px, grid, sigma): a one-frame 4K house batch
-# split into bird slices, then a smaller 1080p batch, also split
-CASES = [(41, [30000], 3840, 2160, 512, 288, 20.0), (42, [4000, 2500], 1920, 1080, 128, 72, 30.0)]
+# split into bird slices, then a smaller one-frame 4K batch on a coarser
+# grid, also split
+CASES = [(41, [30000], 3840, 2160, 512, 288, 20.0), (42, [12000], 3840, 2160, 256, 144, 45.0)]
 
 
 def test_noalloc_matches_density_frames_gpu():
@@ -40,12 +41,17 @@ def test_noalloc_matches_density_frames_gpu():
     for seed, counts, w, h, gx, gy, sigma in CASES:
         xy, off = _frames(seed, counts, w, h)
         F, T = len(counts), xy.shape[0]
-        assert lib.density_frames_workspace(F, T, gx, gy) > 0, "the case must use the scratch"
         dxy = torch.from_numpy(xy).cuda()
         doff = torch.from_numpy(off).cuda()
         want = torch.full((F, gy, gx), -1.0, dtype=torch.float32, device="cuda")
         got = torch.full((F, gy, gx), -2.0, dtype=torch.float32, device="cuda")
         max_fp = int(max(counts))
+        # the plan splits the frame into bird slices (a one-byte workspace is
+        # refused), so the allocation-free call keeps partial grids in its scratch
+        one = torch.empty(256, dtype=torch.uint8, device="cuda")
+        st = lib.density_frames(*_args(dxy, doff, F, T, max_fp, w, h, gx, gy, sigma, want),
+                                ctypes.c_void_p(one.data_ptr()), 1, None)
+        assert st == flock.binding.FLOCK_ENOMEM, "the case must use the scratch"
         st = lib.density_frames(*_args(dxy, doff, F, T, max_fp, w, h, gx, gy, sigma, want), None, 0, None)
         assert st == 0, lib.flock_last_error().decode()
         st = lib.density_frames_noalloc(*_args(dxy, doff, F, T, max_fp, w, h, gx, gy, sigma, got), None)
