@@ -168,6 +168,7 @@ __device__ __forceinline__ void cluster_frame_inplace(const ClusterArgs &a, int 
 // ---------------------------------------------------------------------------
 
 constexpr uint16_t kNone = 0xffff;
+constexpr uint8_t kIsolated = 3;  // kind marker of a non-core point with no neighbour but itself (noise)
 constexpr int kMaxOffsets = 16;
 // Neighbour cells lie within +-reach cells, and reach <= 2 for every eps:
 // reach = 1 + (E - 1) / side with side >= max(1, floor(E / sqrt 2)) > (E - 1) / 2.
@@ -953,29 +954,27 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         if (tid == kThreads - 1) cell[g.ncell] = (uint32_t)run | 0xffff0000u;
     }
     __syncthreads();
+    // scatter into sorted order; 4a. on the way, a cell holding >= min_pts
+    // points is all core, and the other points go to the work list
 #pragma unroll
     for (int k = 0; k < kPtsPerThread; ++k) {
         const int32_t i = tid + k * kThreads;
-        if (i >= n) break;
-        int32_t cx, cy;
-        const int32_t pos = cstart(cell_id(pv[k], g, &cx, &cy)) + prank[k];
-        pxy[pos] = pv[k];
-        sid[pos] = (uint16_t)i;
-    }
-    __syncthreads();
-
-    // 4a. a cell holding >= min_pts points is all core; list the other points
-    for (int32_t p0 = tid - lane; p0 < n; p0 += kThreads) {
-        const int32_t p = p0 + lane;
+        if (tid - lane + k * kThreads >= n) break;  // wave-uniform
         bool need = false;
-        if (p < n) {
+        int32_t pos = 0;
+        if (i < n) {
             int32_t cx, cy;
-            const int32_t c = cell_id(pxy[p], g, &cx, &cy);
-            const bool dense = g.dense_ok && cstart(c + 1) - cstart(c) >= a.min_pts;
-            score[p] = dense ? 1 : 0;
+            const int32_t c = cell_id(pv[k], g, &cx, &cy);
+            const int32_t c0 = cstart(c);
+            pos = c0 + prank[k];
+            pxy[pos] = pv[k];
+            sid[pos] = (uint16_t)i;
+            const bool dense = g.dense_ok && cstart(c + 1) - c0 >= a.min_pts;
+            score[pos] = dense ? 1 : 0;
+            kindo[i] = 0;
             need = !dense;
         }
-        wave_append(need, (uint16_t)p, list, &s_nlist);
+        wave_append(need, (uint16_t)pos, list, &s_nlist);
     }
     __syncthreads();
     // 4b. count the listed points' neighbours, nearest rows first, stopping
@@ -1007,6 +1006,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
             for (int k = 0; k < 5; ++k)
                 if (cnt < a.min_pts) cnt += count_span(pxy, q0[k], q1[k], v, r, a.min_pts - cnt);
             if (cnt >= a.min_pts) score[p] = 1;
+            else if (cnt == 1) kindo[sid[p]] = kIsolated;  // no neighbour but itself: noise, no border search
         }
     }
     __syncthreads();
@@ -1015,8 +1015,8 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     for (int32_t p = tid; p < n; p += kThreads) {
         parent[p] = p;
         const bool core = score[p];
-        kindo[sid[p]] = core ? 2 : 0;
         if (core) {
+            kindo[sid[p]] = 2;
             int32_t cx, cy;
             const int32_t c = cell_id(pxy[p], g, &cx, &cy);
             atomicMin(&cell[c], (cell[c] & 0xffffu) | ((uint32_t)sid[p] << 16));
@@ -1184,7 +1184,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     // 8. border points: nearest core, ties by smaller (y, x)
     for (int32_t p0 = tid - lane; p0 < n; p0 += kThreads) {
         const int32_t p = p0 + lane;
-        wave_append(p < n && !score[p], (uint16_t)p, list, &s_nlist);
+        wave_append(p < n && !score[p] && kindo[sid[p]] != kIsolated, (uint16_t)p, list, &s_nlist);
     }
     __syncthreads();
     {
@@ -1248,8 +1248,9 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
 
     // 9. outputs in original order (coalesced)
     for (int32_t i = tid; i < n; i += kThreads) {
-        a.labels[b + i] = parent[i];
-        a.kind[b + i] = kindo[i];
+        const uint8_t k = kindo[i];
+        a.labels[b + i] = k == kIsolated ? -1 : parent[i];
+        a.kind[b + i] = k == kIsolated ? 0 : k;
     }
     if (tid == 0 && a.n_clusters) a.n_clusters[f] = s_red;
 }

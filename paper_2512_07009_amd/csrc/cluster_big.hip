@@ -86,7 +86,10 @@ __device__ __forceinline__ bool frame_ok(const ClusterArgs &a, int f, int32_t *b
     return !(*b < 0 || *e < *b || *e > a.total);
 }
 
-// Frame holding global point index i: the last f with offsets[f] <= i.
+// Frame holding global point index i: the last f with offsets[f] <= i, or -1
+// when i lies past that frame's end (points beyond offsets[n_frames], or
+// under a frame whose offsets decrease): such points belong to no frame and
+// are never read.
 __device__ __forceinline__ int frame_of_point(const int32_t *offsets, int n_frames, int32_t i) {
     int lo = 0, hi = n_frames - 1;
     while (lo < hi) {
@@ -94,7 +97,7 @@ __device__ __forceinline__ int frame_of_point(const int32_t *offsets, int n_fram
         if (offsets[mid] <= i) lo = mid;
         else hi = mid - 1;
     }
-    return lo;
+    return (i >= offsets[lo] && i < offsets[lo + 1]) ? lo : -1;
 }
 
 // Frame owning cell-table entry c: the last f with 2 offsets[f] + 2 f <= c.
@@ -133,9 +136,8 @@ __device__ __forceinline__ BigGrid load_grid(const int32_t *rec) {
 }
 
 __device__ __forceinline__ void cell_xy(int2 p, const BigGrid &g, int32_t *cx, int32_t *cy) {
-    const uint32_t ux = (uint32_t)(p.x - g.x0), uy = (uint32_t)(p.y - g.y0);
-    *cx = min((int32_t)(ux / (uint32_t)g.side), g.ncx - 1);
-    *cy = min((int32_t)(uy / (uint32_t)g.side), g.ncy - 1);
+    *cx = cell_coord_clamped(p.x, g.x0, g.side, g.ncx);
+    *cy = cell_coord_clamped(p.y, g.y0, g.side, g.ncy);
 }
 
 // ---------------------------------------------------------------------------
@@ -236,6 +238,7 @@ __global__ __launch_bounds__(kBlock) void big_hist(ClusterArgs a, BigWs w) {
     const int32_t i = blockIdx.x * kBlock + threadIdx.x;
     if (i >= a.total) return;
     const int f = frame_of_point(a.offsets, a.n_frames, i);
+    if (f < 0) return;
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig]) return;
     const BigGrid g = load_grid(rec);
@@ -295,6 +298,7 @@ __global__ __launch_bounds__(kBlock) void big_scatter(ClusterArgs a, BigWs w) {
     const int32_t i = blockIdx.x * kBlock + threadIdx.x;
     if (i >= a.total) return;
     const int f = frame_of_point(a.offsets, a.n_frames, i);
+    if (f < 0) return;
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig]) return;
     const BigGrid g = load_grid(rec);
@@ -311,6 +315,7 @@ __global__ __launch_bounds__(kBlock) void big_core(ClusterArgs a, BigWs w) {
     const int32_t p = blockIdx.x * kBlock + threadIdx.x;
     if (p >= a.total) return;
     const int f = frame_of_point(a.offsets, a.n_frames, p);
+    if (f < 0) return;
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig]) return;
     const BigGrid g = load_grid(rec);
@@ -353,6 +358,7 @@ __global__ __launch_bounds__(kBlock) void big_nodes(ClusterArgs a, BigWs w) {
     const int32_t p = blockIdx.x * kBlock + threadIdx.x;
     if (p >= a.total || !w.score[p]) return;
     const int f = frame_of_point(a.offsets, a.n_frames, p);
+    if (f < 0) return;
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig] || !rec[kDense]) return;
     const BigGrid g = load_grid(rec);
@@ -441,6 +447,7 @@ __global__ __launch_bounds__(kBlock) void big_union_points(ClusterArgs a, BigWs 
     const int32_t p = blockIdx.x * kBlock + threadIdx.x;
     if (p >= a.total || !w.score[p]) return;
     const int f = frame_of_point(a.offsets, a.n_frames, p);
+    if (f < 0) return;
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig] || rec[kDense]) return;
     const BigGrid g = load_grid(rec);
@@ -476,8 +483,8 @@ __global__ __launch_bounds__(kBlock) void big_flatten(ClusterArgs a, BigWs w) {
     int f = 0;
     if (p < a.total && w.score[p]) {
         f = frame_of_point(a.offsets, a.n_frames, p);
-        const int32_t *rec = w.rec + (size_t)f * kRec;
-        if (rec[kBig]) {
+        if (f >= 0 && w.rec[(size_t)f * kRec + kBig]) {
+            const int32_t *rec = w.rec + (size_t)f * kRec;
             const BigGrid g = load_grid(rec);
             const int32_t b = a.offsets[f];
             const int32_t o = w.ssid[p];
@@ -499,6 +506,7 @@ __global__ __launch_bounds__(kBlock) void big_border(ClusterArgs a, BigWs w) {
     const int32_t p = blockIdx.x * kBlock + threadIdx.x;
     if (p >= a.total || w.score[p]) return;
     const int f = frame_of_point(a.offsets, a.n_frames, p);
+    if (f < 0) return;
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig]) return;
     const BigGrid g = load_grid(rec);

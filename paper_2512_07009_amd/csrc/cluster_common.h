@@ -136,6 +136,17 @@ __device__ inline int block_exclusive_scan(int v, int *wave_tot) {
     return base + inc - v;
 }
 
+// Cell coordinate of v on an axis whose grid starts at v0 with cells of
+// `side` quanta and `ncoord` cells: floor((v - v0) / side), clamped into
+// [0, ncoord - 1].  The difference is taken in unsigned arithmetic, so a
+// value below v0 (which a frame's own points never are) lands in the last
+// cell instead of a negative index.
+__host__ __device__ __forceinline__ int32_t cell_coord_clamped(int32_t v, int32_t v0, int32_t side, int32_t ncoord) {
+    const uint32_t q = ((uint32_t)v - (uint32_t)v0) / (uint32_t)side;
+    const uint32_t last = (uint32_t)(ncoord - 1);
+    return (int32_t)(q < last ? q : last);
+}
+
 // Smallest per-axis distance between points of two cells |d| cells apart.
 __device__ __forceinline__ int64_t cell_gap(int32_t d, int32_t side) {
     d = d < 0 ? -d : d;
