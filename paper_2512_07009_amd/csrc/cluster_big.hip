@@ -41,7 +41,8 @@ using namespace cl;
 constexpr int kBlock = 256;
 constexpr int kScanThreads = 1024;
 constexpr int kPrepThreads = 1024;
-constexpr int kUnroll = 8;  // independent loads per thread and step in prep and scan
+constexpr int kUnroll = 8;       // independent loads per thread and step in the bounding box
+constexpr int kScanUnroll = 32;  // cells per thread in a scan tile (32768 cells, 132 KiB of LDS)
 constexpr int kRec = 16;  // int32 fields per frame record
 
 enum RecField {
@@ -248,14 +249,19 @@ __global__ __launch_bounds__(kBlock) void big_hist(ClusterArgs a, BigWs w) {
     w.rank[i] = atomicAdd(&w.cstart[cell_base(a.offsets, f) + (int64_t)cy * g.ncx + cx], 1);
 }
 
-// Exclusive scan of a frame's cell counts, in tiles of kScanThreads * kUnroll
-// cells: coalesced loads into LDS, kUnroll consecutive cells per thread, a
-// workgroup scan plus the carry of the earlier tiles, coalesced stores.
+// Exclusive scan of a frame's cell counts, in tiles of kScanThreads *
+// kScanUnroll cells: coalesced loads into LDS, kScanUnroll consecutive cells
+// per thread, a workgroup scan plus the carry of the earlier tiles, coalesced
+// stores.
 __global__ __launch_bounds__(kScanThreads) void big_scan(ClusterArgs a, BigWs w) {
-    constexpr int kTileCells = kScanThreads * kUnroll;
+    constexpr int kTileCells = kScanThreads * kScanUnroll;
+    // cell c of a tile sits at (c / 32) * 33 + c % 32: both the coalesced
+    // passes (consecutive c per lane) and the per-thread runs (32 consecutive
+    // c per lane) then touch 64 different banks per wave
     __shared__ int s_wave[kScanThreads / 64];
-    __shared__ int s_tile[kTileCells];
+    __shared__ int s_tile[kTileCells / 32 * 33];
     __shared__ int s_carry;
+    auto at = [](int c) { return (c >> 5) * 33 + (c & 31); };
     const int f = blockIdx.x, tid = threadIdx.x;
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig]) return;
@@ -264,29 +270,29 @@ __global__ __launch_bounds__(kScanThreads) void big_scan(ClusterArgs a, BigWs w)
     int carry = 0;
     for (int32_t t0 = 0; t0 < ncell; t0 += kTileCells) {
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < kScanUnroll; ++u) {
             const int32_t c = t0 + u * kScanThreads + tid;
-            s_tile[u * kScanThreads + tid] = c < ncell ? cs[c] : 0;
+            s_tile[at(u * kScanThreads + tid)] = c < ncell ? cs[c] : 0;
         }
         __syncthreads();
-        int v[kUnroll], sum = 0;
+        int v[kScanUnroll], sum = 0;
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            v[u] = s_tile[tid * kUnroll + u];
+        for (int u = 0; u < kScanUnroll; ++u) {
+            v[u] = s_tile[at(tid * kScanUnroll + u)];
             sum += v[u];
         }
         int run = carry + block_exclusive_scan(sum, s_wave);  // ends with a barrier
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            s_tile[tid * kUnroll + u] = run;
+        for (int u = 0; u < kScanUnroll; ++u) {
+            s_tile[at(tid * kScanUnroll + u)] = run;
             run += v[u];
         }
         if (tid == kScanThreads - 1) s_carry = run;
         __syncthreads();
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < kScanUnroll; ++u) {
             const int32_t c = t0 + u * kScanThreads + tid;
-            if (c < ncell) cs[c] = s_tile[u * kScanThreads + tid];
+            if (c < ncell) cs[c] = s_tile[at(u * kScanThreads + tid)];
         }
         carry = s_carry;
         __syncthreads();  // s_tile and s_carry are rewritten by the next tile
@@ -385,8 +391,10 @@ __device__ __forceinline__ bool forward_offset(const BigGrid &g, int k, int *odx
 constexpr int kMaxForward = 12;
 
 // Cell-pair unions for frames with the eps-diagonal grid: the cores of a
-// cell are one node (its smallest core index).
-__global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w, int64_t n_items) {
+// cell are one node (its smallest core index).  Two launches: the adjacent
+// cells (far = 0), then the farther ones (far = 1), whose pairs mostly join
+// nodes that the first launch has already connected and skip their tests.
+__global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w, int64_t n_items, int far) {
     const int64_t item = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (item >= n_items) return;
     const int64_t c = item / kMaxForward;
@@ -402,6 +410,7 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
     if (na == INT_MAX) return;
     int odx, ody;
     if (!forward_offset(g, k, &odx, &ody)) return;
+    if ((odx >= -1 && odx <= 1 && ody <= 1) == (far != 0)) return;  // the other launch's pair
     const int32_t ay = ca / g.ncx, ax = ca - ay * g.ncx;
     const int32_t bx = ax + odx, by = ay + ody;
     if (bx < 0 || bx >= g.ncx || by >= g.ncy) return;
@@ -580,7 +589,8 @@ hipError_t launch_cluster_big(const ClusterArgs &a, void *workspace, hipStream_t
         hipLaunchKernelGGL(big_core, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_nodes, dim3(pts), dim3(kBlock), 0, stream, a, w);
         const int64_t items = cells * kMaxForward;
-        hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items);
+        hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items, 0);
+        hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items, 1);
         hipLaunchKernelGGL(big_union_points, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_flatten, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_border, dim3(pts), dim3(kBlock), 0, stream, a, w);
