@@ -31,6 +31,12 @@
  *  Thread safety: calls on different streams may run concurrently; the only
  *  global state is a per-thread error string and a once-initialised cache of
  *  device properties.
+ *  Graph capture: a call enqueues only kernel launches when it is given the
+ *  workspace its *_workspace() query asks for (or when that query returns 0),
+ *  so it can be captured into a HIP graph.  With a NULL workspace where one
+ *  is needed the library allocates and frees its scratch stream-ordered
+ *  (hipMallocAsync / hipFreeAsync), which a capture records as memory nodes;
+ *  pass a workspace (or use density_frames_noalloc) under capture.
  */
 #ifndef FLOCK_H
 #define FLOCK_H

@@ -97,15 +97,15 @@ def _stream(stream):
 
 
 def _workspace(nbytes: int, dev, stream):
-    """Scratch for one call.  torch's caching allocator ties a block to the
-    stream it was allocated on, so the block is also recorded on the stream
-    the kernels run on: it is not handed out again before they finish."""
+    """Scratch for one call, allocated on the stream the kernels run on.
+    torch's caching allocator hands a freed block out again only to work
+    ordered after it on that stream, so the block is not reused before the
+    kernels finish, with no cross-stream bookkeeping (and none under graph
+    capture, where the block comes from the graph's own pool)."""
     if not nbytes:
         return None
-    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
-    if stream is not None:
-        ws.record_stream(stream)
-    return ws
+    with torch.cuda.device(dev), torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream(dev)):
+        return torch.empty(nbytes, dtype=torch.uint8, device=dev)
 
 
 def _batch(xy: torch.Tensor, offsets: torch.Tensor):
