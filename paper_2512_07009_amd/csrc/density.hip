@@ -9,10 +9,13 @@
 // contraction over the birds of the frame, run on the matrix cores with fp16
 // factors and fp32 accumulation.
 //
-// A factor below 2^-25 rounds to +0 in fp16, and exp(-t^2/2) < 2^-25 for
-// |t| > 5.9, so a bird has nonzero factors only in the rows within 6 s of it
-// (its window); every other factor is +0 in either evaluation, and the
-// contraction stays dense over all (row, column, bird) triples.
+// Factors are stored as fp16 values of 2^8 f (kLift; the largest, 256, is
+// far from fp16's limit) and the 2^-16 of the product goes into the output
+// scale, so fp16's subnormal range starts at f = 2^-22 (5.5 s from the bird)
+// instead of 2^-14 (4.4 s).  A bird has nonzero factors only in the rows
+// within about 6 s of it (its window: the tables hold the cells up to
+// ceil(6 s / cell) + 1 away, exact zeros beyond); the contraction stays
+// dense over all (row, column, bird) triples.
 //
 // Two ways to make the operands:
 //
@@ -36,11 +39,15 @@
 // thread) and restarted every kRestart rows; when h > 2 s every factor is an
 // exact exponential.
 //
-// Accuracy: each fp16 factor carries a relative rounding error <= 2^-11 (plus
-// at most a few fp32 ulps before the conversion), so each term of the sum is
-// within about 2^-10 of exact; all terms are positive, so the same relative
-// bound holds for every output, which is <= the frame's maximum.  Every sum
-// is taken in a fixed order, so results are deterministic.
+// Accuracy: a normal fp16 factor (f >= 2^-22) carries a relative rounding
+// error <= 2^-11 (plus a few fp32 ulps before the conversion); a subnormal
+// one an absolute error <= 2^-25 of 2^8 f, i.e. 2^-33 of f.  A term is a
+// product of two factors <= 1, so its error is <= about 2^-10 of the term plus
+// 2^-32 absolute; all terms are positive, so an output's error is <= 2^-10 of
+// the output plus N 2^-32 c for N birds (c = 1 / (2 pi s^2)), against an
+// output <= the frame's maximum.  The window's cut contributes < 2^-25 per
+// factor.  Every sum is taken in a fixed order, so results are
+// deterministic.
 
 #include <climits>
 #include <cmath>
@@ -64,6 +71,7 @@ constexpr int kRChunk = 128;         // birds per LDS chunk: one (bird, axis) wi
 constexpr int kRPitch = kRChunk + 8; // halves per LDS row (16-byte skew between rows)
 constexpr int kRestart = 16;         // rows between exact restarts of the recurrence
 constexpr float kCutSigmas = 6.0f;
+constexpr float kLift = 256.0f;      // factors are stored as fp16(kLift f)
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float16v __attribute__((ext_vector_type(16)));
@@ -73,7 +81,7 @@ struct Geometry {
     float inv_hx, inv_hy;
     float neg_k;           // -log2(e) / (2 s^2): exp(-d^2/(2s^2)) = exp2(d^2 * neg_k)
     float cut;             // window half-width, px
-    float scale;           // 1 / (2 pi s^2)
+    float scale;           // 1 / (2 pi s^2 kLift^2)
     int recur_x, recur_y;  // recurrence usable along the axis (h <= 2 s)
 };
 
@@ -86,11 +94,10 @@ struct RecurLayout {
     static constexpr int kBytes = kFactorBytes > kRedBytes ? kFactorBytes : kRedBytes;
 };
 
-// Write one bird's factors for rows [row0, row0 + nrows) of one axis into a
-// column of buf (row-major, kRPitch halves per row); rows outside the window
-// are left as they are (cleared).  A row just outside the computed window has
-// a factor below 2^-25 (its fp16 value is +0), so float rounding of the
-// bounds cannot change the tile.
+// Write one bird's factors (times kLift) for rows [row0, row0 + nrows) of one
+// axis into a column of buf (row-major, kRPitch halves per row); rows outside
+// the window (6 s) are left as they are (cleared): their factors are below
+// exp(-18) = 1.5e-8 of the peak.
 __device__ __forceinline__ void fill_window(_Float16 *col, float pos, float h, float inv_h, int grid_n,
                                             int row0, int nrows, float neg_k, float cut, bool recur) {
     int lo = max((int)ceilf((pos - cut) * inv_h - 0.5f), row0);
@@ -98,7 +105,7 @@ __device__ __forceinline__ void fill_window(_Float16 *col, float pos, float h, f
     if (!recur) {
         for (int row = lo; row <= hi; ++row) {
             const float d = ((float)row + 0.5f) * h - pos;
-            col[(row - row0) * kRPitch] = (_Float16)__builtin_amdgcn_exp2f(d * d * neg_k);
+            col[(row - row0) * kRPitch] = (_Float16)(kLift * __builtin_amdgcn_exp2f(d * d * neg_k));
         }
         return;
     }
@@ -108,9 +115,9 @@ __device__ __forceinline__ void fill_window(_Float16 *col, float pos, float h, f
     for (int base = lo, top = hi; base <= mid; base += kRestart, top -= kRestart) {
         const float da = ((float)base + 0.5f) * h - pos;
         const float db = ((float)top + 0.5f) * h - pos;
-        float fa = __builtin_amdgcn_exp2f(da * da * neg_k);
+        float fa = kLift * __builtin_amdgcn_exp2f(da * da * neg_k);
         float ra = __builtin_amdgcn_exp2f((2.0f * da + h) * h * neg_k);
-        float fb = __builtin_amdgcn_exp2f(db * db * neg_k);
+        float fb = kLift * __builtin_amdgcn_exp2f(db * db * neg_k);
         float rb = __builtin_amdgcn_exp2f((h - 2.0f * db) * h * neg_k);  // ratio going down
         const int steps = min(kRestart, mid - base + 1);
         for (int i = 0; i < steps; ++i) {
@@ -262,7 +269,7 @@ struct GatherGeom {
     GatherAxis ay, ax;
     int pw;           // 32 or 64
     float neg_k;      // -log2(e) / (2 s^2), px^-2
-    float scale;      // 1 / (2 pi s^2)
+    float scale;      // 1 / (2 pi s^2 kLift^2)
     int table_bytes;  // the tables (one when both axes agree), 16-byte aligned
     int lds_bytes;
 };
@@ -426,7 +433,7 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
                 float f = 0.0f;
                 if (i >= 1 && i <= 2 * t.j + 1) {
                     const float d = (((float)(i - 1 - t.j) + 0.5f) * (float)t.c - (float)r) * 0.0625f;
-                    f = __builtin_amdgcn_exp2f(d * d * gg.neg_k);
+                    f = kLift * __builtin_amdgcn_exp2f(d * d * gg.neg_k);
                 }
                 v[i] = __builtin_bit_cast(uint16_t, (_Float16)f);
             }
@@ -601,7 +608,7 @@ Geometry make_geometry(const DensityArgs &a) {
     g.inv_hy = (float)(1.0 / hy);
     g.neg_k = (float)(-1.4426950408889634 / (2.0 * s * s));
     g.cut = (float)(kCutSigmas * s);
-    g.scale = (float)(1.0 / (2.0 * 3.14159265358979323846 * s * s));
+    g.scale = (float)(1.0 / (2.0 * 3.14159265358979323846 * s * s) / ((double)kLift * kLift));
     g.recur_x = hx <= 2.0 * s;
     g.recur_y = hy <= 2.0 * s;
     return g;
@@ -638,7 +645,7 @@ bool make_gather_geom(const DensityArgs &a, GatherGeom *gg) {
     gg->lds_bytes = std::max(gg->table_bytes + stage, kGWaves * kGRedTiles * 256 * 4);
     const double s = (double)a.sigma_px;
     gg->neg_k = (float)(-1.4426950408889634 / (2.0 * s * s));
-    gg->scale = (float)(1.0 / (2.0 * 3.14159265358979323846 * s * s));
+    gg->scale = (float)(1.0 / (2.0 * 3.14159265358979323846 * s * s) / ((double)kLift * kLift));
     return true;
 }
 
