@@ -10,13 +10,18 @@ Inputs are resident in device memory before any timed region.
 Timed regions (each bracketed by device synchronisation):
   1. K steps replayed from HIP graphs captured from the step (graphs of up
      to 10 steps; host launch cost out of the loop), once with the two calls
-     on two streams and once on one stream.  One replay of each is checked
-     against the eager outputs first.  `value` is the faster of the two
-     (`config.streams` says which): on large batches the two kernels compete
-     for compute units and one stream wins.
-  2. per-kernel durations for the roofline: the same K steps issued eagerly
-     in the same mode, with HIP events recorded on the stream each kernel
-     runs on.
+     on two streams and once on one stream.  Step k reads and writes copy
+     k mod R of the batch (inputs and outputs), with R copies together larger
+     than twice the 256 MB memory-side cache (at most 1000 copies), so each
+     step finds its data in HBM, not in a cache.  Every copy's outputs are
+     checked against the eager outputs first.  `value` is the faster of the
+     two modes (`config.streams` says which): on large batches the two
+     kernels compete for compute units and one stream wins.
+  2. the same replays on one copy of the batch (`warm_value`: inputs and
+     outputs stay in L2 and the memory-side cache where they fit).
+  3. per-kernel durations for the roofline: K steps issued eagerly on one
+     stream (each kernel alone on the GPU), each after a write of flush_mb
+     MiB that evicts the caches, with HIP events recorded on that stream.
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -77,42 +82,53 @@ def committed_traffic(kernel: str, workload: str):
     return float(m_bytes.group(1))
 
 
-def cpu_baseline(xy, off, w, budget_s: float):
-    """The CPU oracle on the host cores: whole frames, as many as fit ~budget_s."""
+def cpu_baseline(xy, off, w, budget_s: float, one_thread_s: float):
+    """The CPU oracle on the host cores: whole frames, as many as fit about
+    budget_s; then on one thread, the whole batch if it fits one_thread_s,
+    else the first 8 frames."""
     import oracle
     threads = oracle.default_threads()
     F = len(off) - 1
-    # probe one frame, then size the sample
-    t0 = time.perf_counter()
-    sx, so = xy[off[0]:off[1]], np.array([0, off[1] - off[0]], np.int32)
-    oracle.cluster_frames(sx, so, w.eps_q, w.min_pts, n_threads=threads)
-    oracle.density_frames(sx, so, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
-                          n_threads=threads)
-    per_frame = max(time.perf_counter() - t0, 1e-6)
-    # frames run concurrently across threads for clustering; density threads over rows
+
+    def run(n, n_threads):
+        sxy, soff = xy[: off[n]], off[: n + 1]
+        t0 = time.perf_counter()
+        oracle.cluster_frames(sxy, soff, w.eps_q, w.min_pts, n_threads=n_threads)
+        oracle.density_frames(sxy, soff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
+                              n_threads=n_threads)
+        return time.perf_counter() - t0
+
+    def rate(n, n_threads, probe):
+        """Frames/s over the first n frames (the probe is that run when n is
+        1); a batch that runs in under a second is repeated until about 1 s."""
+        dt = probe if n == 1 else run(n, n_threads)
+        reps = 1
+        while dt < 1.0:
+            dt += run(n, n_threads)
+            reps += 1
+        return reps * n / dt, reps, dt
+
+    # probe one frame, then size the sample (clustering threads over frames,
+    # density over grid rows)
+    per_frame = max(run(1, threads), 1e-6)
     n = int(max(1, min(F, budget_s / per_frame)))
-    sxy, soff = xy[: off[n]], off[: n + 1]
-    t0 = time.perf_counter()
-    oracle.cluster_frames(sxy, soff, w.eps_q, w.min_pts, n_threads=threads)
-    oracle.density_frames(sxy, soff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
-                          n_threads=threads)
-    dt = time.perf_counter() - t0
-    # the same oracle on one thread, on at most 8 frames
-    n1 = int(max(1, min(8, n)))
-    sxy1, soff1 = xy[: off[n1]], off[: n1 + 1]
-    t0 = time.perf_counter()
-    oracle.cluster_frames(sxy1, soff1, w.eps_q, w.min_pts, n_threads=1)
-    oracle.density_frames(sxy1, soff1, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px, n_threads=1)
-    dt1 = time.perf_counter() - t0
+    v, reps, dt = rate(n, threads, per_frame)
+    per_frame1 = max(run(1, 1), 1e-6)
+    n1 = F if per_frame1 * F <= one_thread_s else int(min(F, 8))
+    v1, reps1, dt1 = rate(n1, 1, per_frame1)
+
+    def what(k, r, t):
+        return (f"all {F} frames" if k == F else f"first {k} of {F} frames") + \
+            (f" x{r}" if r > 1 else "") + f", {t:.1f} s wall"
     model = ""
     try:
         with open("/proc/cpuinfo") as fh:
             model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
     except OSError:
         pass
-    return {"value": n / dt, "unit": "frames/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {n} of {F} frames of {w.name} (clustering + density), {dt:.1f} s wall",
-            "one_thread_value": n1 / dt1, "one_thread_sample": f"first {n1} frames, {dt1:.1f} s wall",
+    return {"value": v, "unit": "frames/s", "cores": threads, "kind": "oracle",
+            "sample": f"{w.name} (clustering + density): " + what(n, reps, dt),
+            "one_thread_value": v1, "one_thread_sample": what(n1, reps1, dt1),
             "cpu_model": model}
 
 
@@ -125,9 +141,16 @@ def main():
     ap.add_argument("--mask-workload", default="masks8x2000_720p",
                     help="segmentation batch for the detection post-processing entry")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget-s", type=float, default=2.0,
+    ap.add_argument("--cpu-budget-s", type=float, default=10.0,
                     help="target wall seconds for the oracle sample (all host cores)")
+    ap.add_argument("--cpu-one-thread-s", type=float, default=30.0,
+                    help="the one-thread oracle leg takes the whole batch if it fits this many seconds, "
+                         "else the first 8 frames")
+    ap.add_argument("--rotate-mb", type=float, default=512,
+                    help="MiB of batch copies that `value` rotates over (0: one copy, warm caches)")
     ap.add_argument("--no-graph", action="store_true", help="time `value` from eager launches")
+    ap.add_argument("--streams", choices=("auto", "1", "2"), default="auto",
+                    help="step modes timed for `value`: both (the faster is reported), one stream, or two")
     ap.add_argument("--flush-mb", type=float, default=512,
                     help="MiB written before each launch timed for the roofline (0: warm back-to-back launches only)")
     ap.add_argument("--calibrate-copy-mb", type=float, default=0,
@@ -157,17 +180,27 @@ def main():
     ncl = torch.empty(F, dtype=torch.int32, device=dev)
     dens = torch.empty((F, w.grid_h, w.grid_w), dtype=torch.float32, device=dev)
     stream = main_stream = torch.cuda.current_stream(dev)
+    cells = w.grid_w * w.grid_h
     log(f"workload {w.name}: {F} frames, {T} birds, max {max_fp}/frame; {flock.version()}")
 
     side = torch.cuda.Stream(dev)  # default priority
 
-    def run_pair(k, concurrent, evs=None, launch_stream=None):
+    def buffers(src_xy, src_off):
+        return {"xy": src_xy, "off": src_off,
+                "labels": torch.empty(T, dtype=torch.int32, device=dev),
+                "kind": torch.empty(T, dtype=torch.uint8, device=dev),
+                "ncl": torch.empty(F, dtype=torch.int32, device=dev),
+                "dens": torch.empty((F, w.grid_h, w.grid_w), dtype=torch.float32, device=dev)}
+
+    home = {"xy": dxy, "off": doff, "labels": labels, "kind": kind, "ncl": ncl, "dens": dens}
+
+    def run_pair(k, concurrent, evs=None, launch_stream=None, buf=None):
         """cluster_frames on `stream` (or `launch_stream`), density_frames on
         `side` (or also on the first stream when not concurrent), with the join
-        back on the first stream."""
+        back on the first stream; on the batch copy `buf` (default: the first)."""
         stream = launch_stream if launch_stream is not None else main_stream
+        b = buf if buf is not None else home
         sd = side
-        lab_, kind_, ncl_, dens_ = labels, kind, ncl, dens
         ds = sd if concurrent else stream
         if concurrent:
             fork = torch.cuda.Event()
@@ -175,13 +208,13 @@ def main():
             sd.wait_event(fork)
         if evs is not None:
             evs[0].record(stream)
-        flock.cluster_frames(dxy, doff, w.eps_px, w.min_pts, max_fp, out=(lab_, kind_, ncl_),
+        flock.cluster_frames(b["xy"], b["off"], w.eps_px, w.min_pts, max_fp, out=(b["labels"], b["kind"], b["ncl"]),
                              stream=stream)
         if evs is not None:
             evs[1].record(stream)
             evs[2].record(ds)
-        flock.density_frames(dxy, doff, w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
-                             max_fp, out=dens_, stream=ds)
+        flock.density_frames(b["xy"], b["off"], w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
+                             max_fp, out=b["dens"], stream=ds)
         if evs is not None:
             evs[3].record(ds)
         if concurrent:
@@ -252,70 +285,95 @@ def main():
     torch.cuda.synchronize(dev)
     K = args.steps
 
-    # 1. graph replays: the two-stream step and the one-stream step
-    log("graph replays, one batch at a time")
+    # 1-2. graph replays: the two-stream step and the one-stream step, over
+    #      rotated copies of the batch and on one copy
     ref = (labels.clone(), kind.clone(), ncl.clone(), dens.clone())
+    gsteps = min(K, 10)
+    step_bytes = xy.nbytes + off.nbytes + 5 * T + 4 * F + 4 * F * cells
+    n_copies = 1
+    if args.rotate_mb > 0:
+        n_copies = min(1000, max(2, -(-int(args.rotate_mb * (1 << 20)) // step_bytes)))
+        n_copies = -(-n_copies // gsteps) * gsteps
+    copies = [home] + [buffers(dxy.clone(), doff.clone()) for _ in range(n_copies - 1)]
+    rotation = {"copies": n_copies, "bytes_per_copy": step_bytes, "total_mb": n_copies * step_bytes / 2**20}
+    log(f"graph replays over {n_copies} copies of the batch ({rotation['total_mb']:.0f} MiB), then on one copy")
+
+    def same_as_ref(b):
+        return (torch.equal(b["labels"], ref[0]) and torch.equal(b["kind"], ref[1]) and torch.equal(b["ncl"], ref[2])
+                and torch.equal(b["dens"], ref[3]))
+
+    def replay_wall(concurrent, bufs):
+        """Capture graphs of `gsteps` steps cycling over `bufs`, check one pass
+        over every copy against the eager outputs, then time K steps."""
+        cap = torch.cuda.Stream(dev)
+        cap.wait_stream(main_stream)
+        groups = [bufs[i:i + gsteps] for i in range(0, len(bufs), gsteps)] if len(bufs) > 1 else [bufs * gsteps]
+        graphs = []
+        for grp in groups:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=cap):
+                for k, b in enumerate(grp):
+                    run_pair(k, concurrent, launch_stream=cap, buf=b)
+            graphs.append(g)
+        rem = None
+        if K % gsteps:
+            grp = groups[(K // gsteps) % len(groups)][:K % gsteps]
+            rem = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(rem, stream=cap):
+                for k, b in enumerate(grp):
+                    run_pair(k, concurrent, launch_stream=cap, buf=b)
+        torch.cuda.synchronize(dev)
+        for b in bufs:
+            b["labels"].fill_(-7)
+            b["dens"].fill_(-1.0)
+        for g in graphs:
+            g.replay()
+        torch.cuda.synchronize(dev)
+        if not all(same_as_ref(b) for b in bufs):
+            raise RuntimeError("graph replay differs from the eager outputs")
+        plan = [graphs[i % len(graphs)] for i in range(K // gsteps)] + ([rem] if rem is not None else [])
+        torch.cuda.synchronize(dev)
+        t0 = time.perf_counter()
+        for g in plan:
+            g.replay()
+        torch.cuda.synchronize(dev)
+        return time.perf_counter() - t0
+
     graph_note = None
-    walls = {}
+    modes = {"auto": (True, False), "1": (False,), "2": (True,)}[args.streams]
+    walls, warm_walls = {}, {}
     if not args.no_graph:
         try:
-            cap = torch.cuda.Stream(dev)
-            cap.wait_stream(stream)
-            gsteps = min(K, 10)
-            for concurrent in (True, False):
-                graphs = []
-                for n_in in sorted({gsteps, K % gsteps} - {0}, reverse=True):
-                    g = torch.cuda.CUDAGraph()
-                    with torch.cuda.graph(g, stream=cap):
-                        for k in range(n_in):
-                            run_pair(k, concurrent, launch_stream=cap)
-                    graphs.append(g)
-                torch.cuda.synchronize(dev)
-                labels.fill_(-7)
-                dens.fill_(-1.0)
-                graphs[0].replay()
-                torch.cuda.synchronize(dev)
-                same = (torch.equal(labels, ref[0]) and torch.equal(kind, ref[1]) and torch.equal(ncl, ref[2])
-                        and torch.equal(dens, ref[3]))
-                if not same:
-                    raise RuntimeError("graph replay differs from the eager outputs")
-                plan = [graphs[0]] * (K // gsteps) + ([graphs[-1]] if K % gsteps else [])
-                for g in plan[:3]:
-                    g.replay()
-                torch.cuda.synchronize(dev)
-                t0 = time.perf_counter()
-                for g in plan:
-                    g.replay()
-                torch.cuda.synchronize(dev)
-                walls[concurrent] = time.perf_counter() - t0
+            for concurrent in modes:
+                walls[concurrent] = replay_wall(concurrent, copies)
+                warm_walls[concurrent] = replay_wall(concurrent, [home]) if n_copies > 1 else walls[concurrent]
         except RuntimeError as ex:
-            graph_note = f"graph replay unavailable ({ex}); value timed eagerly"
+            graph_note = f"graph replay unavailable ({ex}); value timed eagerly on one copy"
             log(graph_note)
-            walls = {}
+            walls, warm_walls = {}, {}
 
-    # 2. eager steps with per-kernel events, two streams and one stream
+    # 3. eager steps with per-kernel events in each mode; the roofline's
+    #    durations come from one-stream steps (each kernel alone on the GPU),
+    #    each step after the flush
     log("eager steps with events")
-    wall_eager, w_cluster, w_density = timed(True, K)
-    wall_seq, w_cluster_seq, w_density_seq = timed(False, K)
+    eager = {c: timed(c, K) for c in modes}
     if not walls:
-        walls = {True: wall_eager, False: wall_seq}
-    concurrent = walls[True] <= walls[False]
+        walls = warm_walls = {c: eager[c][0] for c in modes}
+    concurrent = min(modes, key=lambda c: walls[c])
     wall = walls[concurrent]
-    if not concurrent:
-        w_cluster, w_density = w_cluster_seq, w_density_seq
-    # the roofline's durations: the same mode, each step after the flush
+    warm_wall = min(warm_walls.values())
+    _, w_cluster, w_density = eager[False] if False in modes else timed(False, K)
     if flush is not None:
-        log("eager steps with events after a cache flush")
-        _, t_cluster, t_density = timed(concurrent, K, cold=True)
+        log("one-stream eager steps with events after a cache flush")
+        _, t_cluster, t_density = timed(False, K, cold=True)
     else:
         t_cluster, t_density = w_cluster, w_density
     ms_per_step = wall / K * 1e3
     value = F / (wall / K)
 
     log("heatmap, roi, drinker and mask entries")
-    # 3. heatmap analytics of the step's density grids (its own entry point,
+    # 4. heatmap analytics of the step's density grids (its own entry point,
     #    not part of `value`): hot cells at twice the frame-average density
-    cells = w.grid_w * w.grid_h
     area = (w.width_px / w.grid_w) * (w.height_px / w.grid_h)
     heat_thr = 2.0 * T / (F * w.width_px * w.height_px)
     hout = {"labels": torch.empty((F, w.grid_h, w.grid_w), dtype=torch.int32, device=dev),
@@ -326,7 +384,7 @@ def main():
             "comp_mass": torch.empty((F, w.grid_h, w.grid_w), dtype=torch.float64, device=dev)}
     t_heat, t_heat_warm = per_launch(lambda: flock.heatmap_frames(dens, area, heat_thr, 8, out=hout, stream=stream), K)
 
-    # 4. region-of-interest filter and counts (its own entry point, not part of
+    # 5. region-of-interest filter and counts (its own entry point, not part of
     #    `value`): a strip along the left wall, a five-vertex polygon
     Wq, Hq = 16 * w.width_px, 16 * w.height_px
     roi_poly = [[0, 0], [Wq // 8, 0], [Wq // 6, Hq // 2], [Wq // 8, Hq], [0, Hq]]
@@ -337,7 +395,7 @@ def main():
     t_roi, t_roi_warm = per_launch(lambda: flock.roi_filter_frames(dxy, doff, roi_poly, out=rout, stream=stream), K)
     kept = int(rout["offsets"][-1].item())
 
-    # 5. drinker-line proximity (its own entry point, not part of `value`): two
+    # 6. drinker-line proximity (its own entry point, not part of `value`): two
     #    drinker lines across the frame, 20 px
     dlines = [[Wq // 10, Hq // 4, 9 * Wq // 10, Hq // 4], [Wq // 10, 3 * Hq // 4, 9 * Wq // 10, 3 * Hq // 4]]
     dthr = 16 * 20
@@ -347,7 +405,7 @@ def main():
     t_drink, t_drink_warm = per_launch(
         lambda: flock.drinker_proximity_frames(dxy, doff, dlines, dthr, out=dout, stream=stream), K)
 
-    # 6. detection post-processing (its own entry point, not part of `value`):
+    # 7. detection post-processing (its own entry point, not part of `value`):
     #    a batch of segmentation outputs, its own synthetic input
     prob_np, mw = wl.mask_batch(args.mask_workload)
     prob = torch.from_numpy(prob_np).to(dev)
@@ -372,11 +430,13 @@ def main():
     density_flops = 2.0 * w.grid_w * w.grid_h * T
     cl = {"bound": "hbm", "achieved": cluster_bytes / t_cluster / 1e9, "peak": HBM_PEAK_GBS,
           "unit": "GB/s", "per_launch_us": t_cluster * 1e6, "warm_per_launch_us": w_cluster * 1e6,
+          "two_stream_per_launch_us": eager[True][1] * 1e6 if True in eager else None,
           "algorithmic_bytes": cluster_bytes}
     cl["frac"] = cl["achieved"] / cl["peak"]
     cl["traffic"] = committed_traffic("cluster", w.name)
     de = {"bound": "mfma", "achieved": density_flops / t_density / 1e12, "peak": MFMA_F16_PEAK_TFLOPS,
           "unit": "TFLOP/s", "per_launch_us": t_density * 1e6, "warm_per_launch_us": w_density * 1e6,
+          "two_stream_per_launch_us": eager[True][2] * 1e6 if True in eager else None,
           "algorithmic_flops": density_flops}
     de["frac"] = de["achieved"] / de["peak"]
     de["traffic"] = committed_traffic("density", w.name)
@@ -458,14 +518,20 @@ def main():
                    "grid": [w.grid_w, w.grid_h], "sigma_px": w.sigma_px, "parallelism": "single-gpu",
                    "streams": 2 if concurrent else 1},
         "birds_per_s": T / (wall / K),
-        "two_stream_frames_per_s": F / (walls[True] / K),
-        "one_stream_frames_per_s": F / (walls[False] / K),
-        "eager_two_stream_frames_per_s": F / (wall_eager / K),
-        "eager_one_stream_frames_per_s": F / (wall_seq / K),
-        "timing": graph_note or ("value: HIP graph replay of the faster of the two-stream and one-stream steps; "
-                                 "kernel durations (per_launch_us, roofline): HIP events around each launch in "
-                                 "an eager run of the same mode, each launch after a write of flush_mb MiB that "
-                                 "evicts L2 and the memory-side cache (warm_per_launch_us: back to back)"),
+        "warm_value": F / (warm_wall / K),
+        "rotation": rotation,
+        "two_stream_frames_per_s": F / (walls[True] / K) if True in walls else None,
+        "one_stream_frames_per_s": F / (walls[False] / K) if False in walls else None,
+        "eager_two_stream_frames_per_s": F / (eager[True][0] / K) if True in eager else None,
+        "eager_one_stream_frames_per_s": F / (eager[False][0] / K) if False in eager else None,
+        "timing": graph_note or ("value: HIP graph replay of the faster of the two-stream and one-stream steps, "
+                                 "step k on copy k mod rotation.copies of the batch (inputs and outputs), so its "
+                                 "data comes from HBM where the copies exceed the caches; warm_value: the same "
+                                 "replays on one copy; two/one_stream_frames_per_s: rotated, per mode; kernel "
+                                 "durations (per_launch_us, roofline): HIP events around each launch in an eager "
+                                 "one-stream run, each launch after a write of flush_mb MiB that evicts L2 and "
+                                 "the memory-side cache (warm_per_launch_us: back to back; "
+                                 "two_stream_per_launch_us: back to back, the two kernels on two streams)"),
         "flush_mb": args.flush_mb,
         "roofline": roof,
         "kernels": {"cluster_frames": cl, "density_frames": de, "heatmap_frames": he, "roi_filter_frames": ro,
@@ -473,7 +539,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
-        out["cpu_baseline"] = cpu_baseline(xy, off, w, args.cpu_budget_s)
+        out["cpu_baseline"] = cpu_baseline(xy, off, w, args.cpu_budget_s, args.cpu_one_thread_s)
     print(json.dumps(out), flush=True)
 
 
