@@ -38,6 +38,7 @@ struct DeviceInfo {
     bool gfx950 = false;
     int n_cus = 0;
     size_t lds_per_block = 0;
+    size_t lds_per_cu = 0;
     char arch[64] = {0};
 };
 
@@ -58,6 +59,7 @@ flock_status device_info(const DeviceInfo **out) {
         d.gfx950 = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
         d.n_cus = prop.multiProcessorCount;
         d.lds_per_block = prop.sharedMemPerBlock;
+        d.lds_per_cu = prop.maxSharedMemoryPerMultiProcessor;
         d.valid = true;
     });
     const DeviceInfo &d = g_devices[dev];
@@ -145,6 +147,7 @@ struct ClusterPlan {
     int32_t cap_points;
     int32_t cap_cells;
     size_t lds_bytes;
+    bool compact = false;  // two workgroups per compute unit
 };
 
 ClusterPlan plan_cluster(int32_t max_frame_points, size_t lds_limit) {
@@ -156,12 +159,38 @@ ClusterPlan plan_cluster(int32_t max_frame_points, size_t lds_limit) {
     if (cap && std::atoi(cap) > 0) limit = std::min(limit, std::atoi(cap));
     p.cap_points = (max_frame_points > 0 && max_frame_points < limit) ? max_frame_points : limit;
     const size_t reserve = 1024;  // static shared variables
-    const int64_t avail = (int64_t)lds_limit - (int64_t)reserve - 14 * (int64_t)p.cap_points - 4;
+    const int64_t avail = (int64_t)lds_limit - (int64_t)reserve - 13 * (int64_t)p.cap_points - 4;
     int64_t cells = std::max<int64_t>(4096, 2 * (int64_t)p.cap_points);
     cells = std::min<int64_t>(cells, avail / 6);
     p.cap_cells = (int32_t)cells;
     p.lds_bytes = flock::cluster_lds_bytes(p.cap_points, p.cap_cells);
     return p;
+}
+
+// With more frames than compute units and frames of at most
+// kClusterCompactCap points, two workgroups share a compute unit when half
+// its LDS holds the frame with a cell table of at least kCompactMinCells
+// entries (a 1080p frame at eps 40 px needs 2652).  A frame whose grid has
+// more cells than the table runs on a coarsened grid (correct, slower).
+// FLOCK_CLUSTER_COMPACT=0 turns this off.
+constexpr int64_t kCompactMinCells = 2048;
+
+void plan_compact(ClusterPlan *p, int32_t max_frame_points, int32_t n_frames, const DeviceInfo &dev) {
+    const char *env = std::getenv("FLOCK_CLUSTER_COMPACT");
+    if (env && std::strcmp(env, "0") == 0) return;
+    if (n_frames <= dev.n_cus || max_frame_points <= 0 || max_frame_points > flock::kClusterCompactCap) return;
+    if (max_frame_points > p->cap_points) return;
+    const size_t half = (dev.lds_per_cu ? dev.lds_per_cu : dev.lds_per_block) / 2;
+    const size_t fixed = flock::cluster_compact_static_lds() + 16;  // static variables, alignment
+    const int64_t avail = (int64_t)half - (int64_t)fixed - 13 * (int64_t)max_frame_points - 4;
+    const int64_t cells = std::min<int64_t>(avail / 6, 2 * (int64_t)max_frame_points + 4096);
+    if (cells < kCompactMinCells) return;
+    const size_t bytes = flock::cluster_lds_bytes(max_frame_points, (int32_t)cells);
+    if (bytes + fixed > half) return;
+    p->cap_points = max_frame_points;
+    p->cap_cells = (int32_t)cells;
+    p->lds_bytes = bytes;
+    p->compact = true;
 }
 
 }  // namespace
@@ -219,8 +248,9 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
         if (st != FLOCK_OK) return st;
     }
 
-    const ClusterPlan plan = plan_cluster(max_frame_points, dev->lds_per_block);
+    ClusterPlan plan = plan_cluster(max_frame_points, dev->lds_per_block);
     const bool big = max_frame_points == 0 || max_frame_points > plan.cap_points;
+    if (!big) plan_compact(&plan, max_frame_points, n_frames, *dev);
     const size_t ws_need = big ? flock::cluster_big_workspace(n_frames, total) : 0;
     if (workspace && workspace_bytes < ws_need)
         return fail(FLOCK_ENOMEM, "workspace of %zu bytes, %zu needed", workspace_bytes, ws_need);
@@ -246,7 +276,7 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
         const char *u = std::getenv("FLOCK_CLUSTER_UNION");
         a.union_regs = (u && std::strcmp(u, "lds") == 0) ? 0 : 1;
     }
-    hipError_t err = flock::launch_cluster_resident(a, plan.lds_bytes, s);
+    hipError_t err = flock::launch_cluster_resident(a, plan.lds_bytes, plan.compact, s);
     if (err != hipSuccess) return hip_fail(err, "cluster kernel launch");
     if (big && total > 0) {
         void *ws = workspace;

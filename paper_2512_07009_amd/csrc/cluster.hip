@@ -168,7 +168,11 @@ __device__ __forceinline__ void cluster_frame_inplace(const ClusterArgs &a, int 
 // ---------------------------------------------------------------------------
 
 constexpr uint16_t kNone = 0xffff;
-constexpr uint8_t kIsolated = 3;  // kind marker of a non-core point with no neighbour but itself (noise)
+// Per-point kind byte (by sorted position): the output kinds, plus a marker
+// for a non-core point with no neighbour but itself (noise, no border search).
+constexpr uint8_t kBorder = 1;
+constexpr uint8_t kCore = 2;
+constexpr uint8_t kIsolated = 3;
 constexpr int kMaxOffsets = 16;
 // Neighbour cells lie within +-reach cells, and reach <= 2 for every eps:
 // reach = 1 + (E - 1) / side with side >= max(1, floor(E / sqrt 2)) > (E - 1) / 2.
@@ -176,8 +180,12 @@ constexpr int kMaxOffsets = 16;
 constexpr int kMaxStencil = 25;
 constexpr int kBorderLanes = 8;  // lanes that share one border candidate
 // Points per thread held in registers during the sort: the planner keeps a
-// resident frame at <= kThreads * kPtsPerThread points.
+// resident frame at <= kThreads * kPtsPerThread points.  The compact kernel
+// (two workgroups per compute unit) holds kPtsCompact per thread, which
+// keeps it within 64 VGPRs (8 waves per SIMD).
 constexpr int kPtsPerThread = 10;
+constexpr int kPtsCompact = 5;
+static_assert(kClusterCompactCap == kThreads * kPtsCompact, "compact capacity");
 
 // Coordinates relative to the frame's bounding-box corner, packed as
 // x | y << 16 (the resident path takes frames whose extent fits 16 bits).
@@ -304,7 +312,7 @@ struct CellHead {
 
 __device__ __forceinline__ CellHead cell_head(const uint32_t *pxy, const uint8_t *score, int32_t q0, int32_t q1) {
     const int32_t q = min(q0 + 1, q1 - 1);
-    return CellHead{pxy[q0], pxy[q], score[q0] != 0, score[q] != 0};
+    return CellHead{pxy[q0], pxy[q], score[q0] == kCore, score[q] == kCore};
 }
 
 // Some core pair among the first two points of each cell within eps: in
@@ -321,10 +329,10 @@ __device__ __forceinline__ bool heads_touch(const CellHead &A, const CellHead &B
 __device__ __forceinline__ bool cells_touch(const uint32_t *pxy, const uint8_t *score, int32_t a0, int32_t a1,
                                             int32_t b0, int32_t b1, const Radius &r) {
     for (int32_t qa = a0; qa < a1; ++qa) {
-        if (!score[qa]) continue;
+        if (score[qa] != kCore) continue;
         const uint32_t va = pxy[qa];
         for (int32_t qb = b0; qb < b1; ++qb)
-            if ((score[qb] != 0) & (sq_dist_pk(va, pxy[qb], r.e1) <= r.e2)) return true;
+            if ((score[qb] == kCore) & (sq_dist_pk(va, pxy[qb], r.e1) <= r.e2)) return true;
     }
     return false;
 }
@@ -455,6 +463,24 @@ __device__ __forceinline__ bool hook_node(int32_t *parent, int32_t a, const int3
     return any;
 }
 
+// hook_node for the register stages, whose neighbour nodes are kept two to a
+// register (node ids are below 2^16): entry k is the low half of nbp[k / 2]
+// for even k, the high half for odd k.
+template <int NO>
+__device__ __forceinline__ bool hook_node_packed(int32_t *parent, int32_t a, const uint32_t (&nbp)[NO / 2],
+                                                 uint32_t m) {
+    int32_t nb[NO];
+#pragma unroll
+    for (int k = 0; k < NO; ++k) nb[k] = (int32_t)((k & 1) ? nbp[k >> 1] >> 16 : nbp[k >> 1] & 0xffffu);
+    return hook_node<NO>(parent, a, nb, m);
+}
+
+template <int NO>
+__device__ __forceinline__ void pack_nodes(const int32_t (&nb)[NO], uint32_t (&nbp)[NO / 2]) {
+#pragma unroll
+    for (int k = 0; k < NO / 2; ++k) nbp[k] = ((uint32_t)nb[2 * k] & 0xffffu) | ((uint32_t)nb[2 * k + 1] << 16);
+}
+
 // Jump step: node a's parent becomes its root (read-only walk; concurrent
 // writers only store roots, so every walk ends at the same root).
 __device__ __forceinline__ void jump_node(int32_t *parent, int32_t a) {
@@ -563,14 +589,14 @@ __device__ __forceinline__ bool core_near_strided(const UnionCtx &u, uint32_t va
     int32_t q = q0;
     for (; q + 3 * step < q1; q += 4 * step) {
         const uint32_t w0 = u.pxy[q], w1 = u.pxy[q + step], w2 = u.pxy[q + 2 * step], w3 = u.pxy[q + 3 * step];
-        const bool h = ((u.score[q] != 0) & (sq_dist_pk(va, w0, u.r.e1) <= u.r.e2)) |
-                       ((u.score[q + step] != 0) & (sq_dist_pk(va, w1, u.r.e1) <= u.r.e2)) |
-                       ((u.score[q + 2 * step] != 0) & (sq_dist_pk(va, w2, u.r.e1) <= u.r.e2)) |
-                       ((u.score[q + 3 * step] != 0) & (sq_dist_pk(va, w3, u.r.e1) <= u.r.e2));
+        const bool h = ((u.score[q] == kCore) & (sq_dist_pk(va, w0, u.r.e1) <= u.r.e2)) |
+                       ((u.score[q + step] == kCore) & (sq_dist_pk(va, w1, u.r.e1) <= u.r.e2)) |
+                       ((u.score[q + 2 * step] == kCore) & (sq_dist_pk(va, w2, u.r.e1) <= u.r.e2)) |
+                       ((u.score[q + 3 * step] == kCore) & (sq_dist_pk(va, w3, u.r.e1) <= u.r.e2));
         if (h) return true;
     }
     for (; q < q1; q += step)
-        if ((u.score[q] != 0) & (sq_dist_pk(va, u.pxy[q], u.r.e1) <= u.r.e2)) return true;
+        if ((u.score[q] == kCore) & (sq_dist_pk(va, u.pxy[q], u.r.e1) <= u.r.e2)) return true;
     return false;
 }
 
@@ -604,7 +630,7 @@ __device__ __forceinline__ void resolve_queue_coop(const UnionCtx &u, int nq, in
             const int32_t a1 = (int32_t)(u.cell[ca + 1] & 0xffffu);
             const int32_t b0 = (int32_t)(u.cell[cb] & 0xffffu), b1 = (int32_t)(u.cell[cb + 1] & 0xffffu);
             for (int32_t qa = (int32_t)(u.cell[ca] & 0xffffu) + gl; qa < a1 && !hit; qa += G)
-                if (u.score[qa]) hit = core_near_strided(u, u.pxy[qa], b0, b1, 1);
+                if (u.score[qa] == kCore) hit = core_near_strided(u, u.pxy[qa], b0, b1, 1);
         }
         const uint64_t hits = __ballot(hit);
         if (gl == 0 && (hits & gmask)) atomicOr(mask32 + (j >> 1), (1u << k) << (16 * (j & 1)));
@@ -670,7 +696,7 @@ __device__ __forceinline__ uint32_t far_candidates(bool have, int32_t ca, int32_
 // Wave-uniform call.
 template <int NO>
 __device__ __forceinline__ void cc_rounds(const UnionCtx &u, const int32_t (&node)[kRegCells],
-                                          const int32_t (&nb)[kRegCells][NO], const uint32_t (&m)[kRegCells],
+                                          const uint32_t (&nbp)[kRegCells][NO / 2], const uint32_t (&m)[kRegCells],
                                           int &round) {
     const int tid = threadIdx.x;
     // a round that hooks leaves fewer roots, so ncl + 1 rounds always
@@ -681,7 +707,7 @@ __device__ __forceinline__ void cc_rounds(const UnionCtx &u, const int32_t (&nod
         bool any = false;
 #pragma unroll
         for (int c = 0; c < kRegCells; ++c)
-            if (m[c]) any |= hook_node<NO>(u.parent, node[c], nb[c], m[c]);
+            if (m[c]) any |= hook_node_packed<NO>(u.parent, node[c], nbp[c], m[c]);
         if (any) u.hook3[round % 3] = 1;
         __syncthreads();
         if (!u.hook3[round % 3] || round >= last) break;  // every edge joins equal roots
@@ -704,7 +730,7 @@ __device__ __forceinline__ void union_regs(const UnionCtx &u, int nadj, int nfwd
     const int tid = threadIdx.x, lane = tid & 63;
     int32_t ca[kRegCells], node[kRegCells];
     {
-        int32_t nb[kRegCells][4];
+        uint32_t nbp[kRegCells][2];
         uint32_t m[kRegCells];
         if (tid == 0) *u.nq = 0;
         __syncthreads();
@@ -715,12 +741,14 @@ __device__ __forceinline__ void union_regs(const UnionCtx &u, int nadj, int nfwd
             ca[c] = 0;
             node[c] = 0;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) nb[c][k] = 0;
+            for (int k = 0; k < 2; ++k) nbp[c][k] = 0;
             if (tid - lane + c * kThreads >= u.ncl) continue;  // wave-uniform
             const CoreCell A = load_core_cell(u, j, have);
             ca[c] = A.ca;
             node[c] = A.node;
-            const uint32_t t = cell_edges_nb<4, false>(have, A, j, u, 0, nadj, nb[c]);
+            int32_t nb[4];
+            const uint32_t t = cell_edges_nb<4, false>(have, A, j, u, 0, nadj, nb);
+            pack_nodes<4>(nb, nbp[c]);
             if (have) u.emask[j] = (uint16_t)t;
         }
         __syncthreads();
@@ -728,7 +756,7 @@ __device__ __forceinline__ void union_regs(const UnionCtx &u, int nadj, int nfwd
         __syncthreads();
 #pragma unroll
         for (int c = 0; c < kRegCells; ++c) m[c] = tid + c * kThreads < u.ncl ? u.emask[tid + c * kThreads] : 0u;
-        cc_rounds<4>(u, node, nb, m, round);
+        cc_rounds<4>(u, node, nbp, m, round);
     }
 #pragma unroll
     for (int c = 0; c < kRegCells; ++c)
@@ -737,18 +765,20 @@ __device__ __forceinline__ void union_regs(const UnionCtx &u, int nadj, int nfwd
     if (tid == 0) *u.nq = 0;
     __syncthreads();
     {
-        int32_t nb[kRegCells][8];
+        uint32_t nbp[kRegCells][4];
         uint32_t m[kRegCells];
 #pragma unroll
         for (int c = 0; c < kRegCells; ++c) {
             const int32_t j = tid + c * kThreads;
             const bool have = j < u.ncl;
 #pragma unroll
-            for (int k = 0; k < 8; ++k) nb[c][k] = 0;
+            for (int k = 0; k < 4; ++k) nbp[c][k] = 0;
             if (tid - lane + c * kThreads >= u.ncl) continue;  // wave-uniform
             const int32_t ay = div_small(ca[c], u.g.ncx, u.inv_ncx), ax = ca[c] - ay * u.g.ncx;
             const int32_t ra = have ? (int32_t)(u.cell[ca[c]] >> 16) : 0;
-            const uint32_t t = far_candidates<8>(have, ca[c], ax, ay, ra, j, u, nadj, nfwd, nb[c]);
+            int32_t nb[8];
+            const uint32_t t = far_candidates<8>(have, ca[c], ax, ay, ra, j, u, nadj, nfwd, nb);
+            pack_nodes<8>(nb, nbp[c]);
             if (have) u.emask[j] = (uint16_t)t;
         }
         __syncthreads();
@@ -756,7 +786,7 @@ __device__ __forceinline__ void union_regs(const UnionCtx &u, int nadj, int nfwd
         __syncthreads();
 #pragma unroll
         for (int c = 0; c < kRegCells; ++c) m[c] = tid + c * kThreads < u.ncl ? u.emask[tid + c * kThreads] : 0u;
-        cc_rounds<8>(u, node, nb, m, round);
+        cc_rounds<8>(u, node, nbp, m, round);
     }
 }
 
@@ -772,7 +802,10 @@ __device__ __forceinline__ void wave_append(bool flag, uint16_t value, uint16_t 
     if (flag) list[base + __popcll(m & ((1ull << lane) - 1ull))] = value;
 }
 
-__global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs a) {
+// One frame per workgroup, PTS points per thread in the register sort (a
+// frame of up to kThreads * PTS points fits).
+template <int PTS>
+__device__ __forceinline__ void cluster_resident(const ClusterArgs &a) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ int s_bbox[4];
     __shared__ int s_wave[kWaves];
@@ -820,16 +853,16 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     // 1. bounding box; each thread keeps its points (i = tid + k * kThreads)
     //    in registers for the sort
     const bool fits = n <= a.cap_points;
-    int2 pt[kPtsPerThread];
+    int2 pt[PTS];
 #pragma unroll
-    for (int k = 0; k < kPtsPerThread; ++k) {
+    for (int k = 0; k < PTS; ++k) {
         const int32_t i = tid + k * kThreads;
         pt[k] = fits && i < n ? P[i] : make_int2(0, 0);
     }
     if (fits) {
         int xmn = INT_MAX, ymn = INT_MAX, xmx = INT_MIN, ymx = INT_MIN;
 #pragma unroll
-        for (int k = 0; k < kPtsPerThread; ++k) {
+        for (int k = 0; k < PTS; ++k) {
             if (tid + k * kThreads >= n) break;
             xmn = min(xmn, pt[k].x);
             ymn = min(ymn, pt[k].y);
@@ -865,10 +898,11 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     //   cell   uint32[cc+1]  first sorted position (low 16 bits) | smallest
     //                        core index in the cell, 0xffff if none (high 16)
     //   sid    uint16[cap]   original index of each sorted position
-    //   list   uint16[cap]   work list
+    //   list   uint16[cap]   work list (then edge bits and queue, then the
+    //                        border list, then kinds by original index)
     //   clist  uint16[cc]    cells that hold a core
-    //   score  uint8 [cap]   core flag by sorted position
-    //   kindo  uint8 [cap]   kind by original index
+    //   score  uint8 [cap]   kind by sorted position (kCore, kBorder,
+    //                        kIsolated, 0 for noise)
     const int32_t cap = a.cap_points, cc = a.cap_cells;
     uint32_t *pxy = reinterpret_cast<uint32_t *>(smem);
     int32_t *parent = reinterpret_cast<int32_t *>(pxy + cap);
@@ -877,7 +911,6 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     uint16_t *list = sid + cap;
     uint16_t *clist = list + cap;
     uint8_t *score = reinterpret_cast<uint8_t *>(clist + cc);
-    uint8_t *kindo = score + cap;
     auto cstart = [cell](int32_t c) -> int32_t { return (int32_t)(cell[c] & 0xffffu); };
     auto cnode = [cell](int32_t c) -> uint32_t { return cell[c] >> 16; };
 
@@ -929,10 +962,10 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         build_stencil(g.reach, g.side, r, lane, s_dxmax, s_sdx, s_sdy, &s_nsten, s_fdx, s_fdy, &s_nadj, &s_nfwd);
     }
     __syncthreads();
-    uint32_t pv[kPtsPerThread];
-    uint16_t prank[kPtsPerThread];
+    uint32_t pv[PTS];
+    uint16_t prank[PTS];
 #pragma unroll
-    for (int k = 0; k < kPtsPerThread; ++k) {
+    for (int k = 0; k < PTS; ++k) {
         if (tid + k * kThreads >= n) break;
         pv[k] = (uint32_t)(pt[k].x - x0) | ((uint32_t)(pt[k].y - y0) << 16);
         int32_t cx, cy;
@@ -957,7 +990,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     // scatter into sorted order; 4a. on the way, a cell holding >= min_pts
     // points is all core, and the other points go to the work list
 #pragma unroll
-    for (int k = 0; k < kPtsPerThread; ++k) {
+    for (int k = 0; k < PTS; ++k) {
         const int32_t i = tid + k * kThreads;
         if (tid - lane + k * kThreads >= n) break;  // wave-uniform
         bool need = false;
@@ -970,8 +1003,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
             pxy[pos] = pv[k];
             sid[pos] = (uint16_t)i;
             const bool dense = g.dense_ok && cstart(c + 1) - c0 >= a.min_pts;
-            score[pos] = dense ? 1 : 0;
-            kindo[i] = 0;
+            score[pos] = dense ? kCore : 0;
             need = !dense;
         }
         wave_append(need, (uint16_t)pos, list, &s_nlist);
@@ -1005,8 +1037,8 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
 #pragma unroll
             for (int k = 0; k < 5; ++k)
                 if (cnt < a.min_pts) cnt += count_span(pxy, q0[k], q1[k], v, r, a.min_pts - cnt);
-            if (cnt >= a.min_pts) score[p] = 1;
-            else if (cnt == 1) kindo[sid[p]] = kIsolated;  // no neighbour but itself: noise, no border search
+            if (cnt >= a.min_pts) score[p] = kCore;
+            else if (cnt == 1) score[p] = kIsolated;  // no neighbour but itself: noise, no border search
         }
     }
     __syncthreads();
@@ -1014,9 +1046,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     // 5. kinds of cores, forest roots, and each cell's smallest core index
     for (int32_t p = tid; p < n; p += kThreads) {
         parent[p] = p;
-        const bool core = score[p];
-        if (core) {
-            kindo[sid[p]] = 2;
+        if (score[p] == kCore) {
             int32_t cx, cy;
             const int32_t c = cell_id(pxy[p], g, &cx, &cy);
             atomicMin(&cell[c], (cell[c] & 0xffffu) | ((uint32_t)sid[p] << 16));
@@ -1142,13 +1172,13 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
         // coarsened grid: point-level unions (each pair once: the later point
         // of a cell, or the point in the earlier cell, does the work)
         for (int32_t p = tid; p < n; p += kThreads) {
-            if (!score[p]) continue;
+            if (score[p] != kCore) continue;
             const uint32_t v = pxy[p];
             const int32_t op = sid[p];
             int32_t cx, cy;
             const int32_t own = cell_id(v, g, &cx, &cy);
             for (int32_t q = cstart(own); q < p; ++q)
-                if (score[q] && sq_dist_pk(v, pxy[q], r.e1) <= r.e2) uf_unite<kGroup>(parent, op, sid[q]);
+                if (score[q] == kCore && sq_dist_pk(v, pxy[q], r.e1) <= r.e2) uf_unite<kGroup>(parent, op, sid[q]);
             for (int dy = 0; dy <= g.reach; ++dy) {
                 const int32_t ry = cy + dy;
                 if (ry >= g.ncy) break;
@@ -1158,7 +1188,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
                 if (rx0 > rx1) continue;
                 const int32_t q1 = cstart(ry * g.ncx + rx1 + 1);
                 for (int32_t q = cstart(ry * g.ncx + rx0); q < q1; ++q)
-                    if (score[q] && sq_dist_pk(v, pxy[q], r.e1) <= r.e2) uf_unite<kGroup>(parent, op, sid[q]);
+                    if (score[q] == kCore && sq_dist_pk(v, pxy[q], r.e1) <= r.e2) uf_unite<kGroup>(parent, op, sid[q]);
             }
         }
         __syncthreads();
@@ -1168,7 +1198,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     //    writes only roots), and roots are counted once
     int roots = 0;
     for (int32_t p = tid; p < n; p += kThreads) {
-        if (!score[p]) continue;
+        if (score[p] != kCore) continue;
         const int32_t o = sid[p];
         int32_t node = o;
         if (g.dense_ok) {
@@ -1184,7 +1214,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     // 8. border points: nearest core, ties by smaller (y, x)
     for (int32_t p0 = tid - lane; p0 < n; p0 += kThreads) {
         const int32_t p = p0 + lane;
-        wave_append(p < n && !score[p] && kindo[sid[p]] != kIsolated, (uint16_t)p, list, &s_nlist);
+        wave_append(p < n && score[p] == 0, (uint16_t)p, list, &s_nlist);
     }
     __syncthreads();
     {
@@ -1218,7 +1248,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
                     const uint32_t w = pxy[q];
                     const int32_t d2 = sq_dist_pk(v, w, r.e1);
                     const uint64_t key = ((uint64_t)(uint32_t)d2 << 32) | w;
-                    const bool take = (d2 <= r.e2) & (score[q] != 0) & (key < bestk);
+                    const bool take = (d2 <= r.e2) & (score[q] == kCore) & (key < bestk);
                     best = take ? q : best;
                     bestk = take ? key : bestk;
                 }
@@ -1235,7 +1265,7 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
                 const int32_t o = sid[p];
                 if (best >= 0) {
                     parent[o] = parent[sid[best]];
-                    kindo[o] = 1;
+                    score[p] = kBorder;  // 0 -> kBorder: concurrent core tests see no change
                 } else {
                     parent[o] = -1;
                 }
@@ -1246,7 +1276,11 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     if (lane == 0) atomicAdd(&s_red, roots);
     __syncthreads();
 
-    // 9. outputs in original order (coalesced)
+    // 9. kinds into original order (in the list's space, free now), then the
+    //    outputs in original order (coalesced)
+    uint8_t *kindo = reinterpret_cast<uint8_t *>(list);
+    for (int32_t p = tid; p < n; p += kThreads) kindo[sid[p]] = score[p];
+    __syncthreads();
     for (int32_t i = tid; i < n; i += kThreads) {
         const uint8_t k = kindo[i];
         a.labels[b + i] = k == kIsolated ? -1 : parent[i];
@@ -1255,12 +1289,23 @@ __global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs 
     if (tid == 0 && a.n_clusters) a.n_clusters[f] = s_red;
 }
 
+__global__ __launch_bounds__(kThreads) void cluster_resident_kernel(ClusterArgs a) {
+    cluster_resident<kPtsPerThread>(a);
+}
+
+// Two workgroups per compute unit: 8 waves per SIMD (at most 64 VGPRs) and
+// half the LDS each.
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(8))) void cluster_compact_kernel(
+    ClusterArgs a) {
+    cluster_resident<kPtsCompact>(a);
+}
+
 }  // namespace
 
 size_t cluster_lds_bytes(int32_t cap_points, int32_t cap_cells) {
-    // per point: packed coords 4, parent 4, sid 2, list 2, core 1, kind 1;
+    // per point: packed coords 4, parent 4, sid 2, list 2, kind 1;
     // per cell: start|node 4, cell list 2
-    size_t bytes = (size_t)cap_points * 14 + (size_t)cap_cells * 6 + 4;
+    size_t bytes = (size_t)cap_points * 13 + (size_t)cap_cells * 6 + 4;
     const size_t inplace = (size_t)kTile * (8 + 1);
     if (bytes < inplace) bytes = inplace;
     return (bytes + 15) & ~(size_t)15;
@@ -1270,14 +1315,26 @@ int32_t cluster_max_cap_points(size_t lds_limit) {
     // reserve room for the static shared variables and a 4096-entry cell table
     const size_t reserve = 1024 + 4096 * 6 + 4;
     if (lds_limit <= reserve) return 0;
-    size_t cap = (lds_limit - reserve) / 14;
+    size_t cap = (lds_limit - reserve) / 13;
     if (cap > (size_t)kThreads * kPtsPerThread) cap = (size_t)kThreads * kPtsPerThread;  // register sort
     return (int32_t)cap;
 }
 
-hipError_t launch_cluster_resident(const ClusterArgs &a, size_t lds_bytes, hipStream_t stream) {
-    hipLaunchKernelGGL(cluster_resident_kernel, dim3(a.n_frames), dim3(kThreads), lds_bytes, stream,
-                       a);
+size_t cluster_compact_static_lds() {
+    static const size_t bytes = [] {
+        hipFuncAttributes attr{};
+        if (hipFuncGetAttributes(&attr, reinterpret_cast<const void *>(&cluster_compact_kernel)) != hipSuccess)
+            return (size_t)4096;  // a safe over-estimate of the kernel's static shared variables
+        return (size_t)attr.sharedSizeBytes;
+    }();
+    return bytes;
+}
+
+hipError_t launch_cluster_resident(const ClusterArgs &a, size_t lds_bytes, bool compact, hipStream_t stream) {
+    if (compact)
+        hipLaunchKernelGGL(cluster_compact_kernel, dim3(a.n_frames), dim3(kThreads), lds_bytes, stream, a);
+    else
+        hipLaunchKernelGGL(cluster_resident_kernel, dim3(a.n_frames), dim3(kThreads), lds_bytes, stream, a);
     return hipGetLastError();
 }
 

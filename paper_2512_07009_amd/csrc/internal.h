@@ -43,7 +43,14 @@ size_t cluster_lds_bytes(int32_t cap_points, int32_t cap_cells);
 // at least min_cells entries.
 int32_t cluster_max_cap_points(size_t lds_limit);
 
-hipError_t launch_cluster_resident(const ClusterArgs &a, size_t lds_bytes, hipStream_t stream);
+// Static shared memory of the compact clustering kernel (bytes).
+size_t cluster_compact_static_lds();
+// Largest frame the compact kernel holds (points per thread x threads).
+constexpr int32_t kClusterCompactCap = 5120;
+// compact: the two-workgroups-per-compute-unit kernel (frames of at most
+// kClusterCompactCap points, lds_bytes at most half a compute unit's LDS
+// less its static shared memory).
+hipError_t launch_cluster_resident(const ClusterArgs &a, size_t lds_bytes, bool compact, hipStream_t stream);
 
 // Multi-workgroup path for frames above cap_points (cluster_big.hip).
 size_t cluster_big_workspace(int32_t n_frames, int32_t total);

@@ -159,6 +159,30 @@ def test_union_many_core_cells_gpu():
     assert_cluster_equal(got, xy, off, 640, 4, tag="lattice")
 
 
+def test_compact_plan_gpu(monkeypatch):
+    """More frames than compute units, none above 5120 points: two clustering
+    workgroups share a compute unit, with half its LDS each.  The batch mixes
+    random frames (ties, duplicates, empty frames), 4K-wide frames of 5000
+    points whose cell grid exceeds the compact cell table (coarsened grid),
+    and a lattice frame with 2660 core cells.  Results equal the oracle and
+    the one-workgroup-per-compute-unit plan (FLOCK_CLUSTER_COMPACT=0)."""
+    n_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    rng = np.random.default_rng(11)
+    xy_r, off_r = wl.random_batch(4242, n_cus + 40, 400)
+    frames = [xy_r[off_r[f]:off_r[f + 1]] for f in range(len(off_r) - 1)]
+    wide = [np.stack([rng.integers(0, 16 * 3840, 5000), rng.integers(0, 16 * 2160, 5000)], 1).astype(np.int32)
+            for _ in range(3)]
+    frames = frames[:100] + wide + [_lattice_frame(7, 70, 38, 640)] + frames[100:]
+    xy, off = wl.pack(frames)
+    assert len(off) - 1 > n_cus and max_count(off) <= 5120
+    got = run_cluster(xy, off, 640, 4)
+    assert_cluster_equal(got, xy, off, 640, 4, tag="compact")
+    monkeypatch.setenv("FLOCK_CLUSTER_COMPACT", "0")
+    ref = run_cluster(xy, off, 640, 4)
+    for a, b in zip(got, ref):
+        assert np.array_equal(a, b)
+
+
 @pytest.mark.parametrize("eps_q,min_pts", [(640, 4), (960, 5), (400, 6)])
 def test_union_lds_stage_gpu(eps_q, min_pts, monkeypatch):
     """FLOCK_CLUSTER_UNION=lds forces the general union stage for every frame."""
