@@ -255,7 +255,7 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
     if (workspace && workspace_bytes < ws_need)
         return fail(FLOCK_ENOMEM, "workspace of %zu bytes, %zu needed", workspace_bytes, ws_need);
     if (workspace && !aligned(workspace, 256)) return fail(FLOCK_EINVAL, "workspace must be 256-byte aligned");
-    flock::ClusterArgs a;
+    flock::ClusterArgs a{};
     a.xy = xy;
     a.offsets = offsets;
     a.n_frames = n_frames;
@@ -276,8 +276,15 @@ flock_status cluster_frames(const int32_t *xy, const int32_t *offsets, int32_t n
         const char *u = std::getenv("FLOCK_CLUSTER_UNION");
         a.union_regs = (u && std::strcmp(u, "lds") == 0) ? 0 : 1;
     }
-    hipError_t err = flock::launch_cluster_resident(a, plan.lds_bytes, plan.compact, s);
-    if (err != hipSuccess) return hip_fail(err, "cluster kernel launch");
+    // one frame above the on-chip capacity (offsets[1] = total): the
+    // multi-workgroup path alone, without an on-chip launch that would only
+    // return
+    a.big_all = big && n_frames == 1 && total > plan.cap_points ? 1 : 0;
+    hipError_t err = hipSuccess;
+    if (!a.big_all) {
+        err = flock::launch_cluster_resident(a, plan.lds_bytes, plan.compact, s);
+        if (err != hipSuccess) return hip_fail(err, "cluster kernel launch");
+    }
     if (big && total > 0) {
         void *ws = workspace;
         if (!ws) {

@@ -28,6 +28,7 @@
 // cell's smallest core index), union (cell pairs, or point pairs when the
 // grid was coarsened), flatten (labels of cores, cluster counts), border.
 
+#include <algorithm>
 #include <climits>
 
 #include "cluster_common.h"
@@ -44,6 +45,8 @@ constexpr int kPrepThreads = 1024;
 constexpr int kUnroll = 8;       // independent loads per thread and step in the bounding box
 constexpr int kScanUnroll = 32;  // cells per thread in a scan tile (32768 cells, 132 KiB of LDS)
 constexpr int kRec = 16;  // int32 fields per frame record
+constexpr int kClearBlocks = 8;  // cell-clearing workgroups per frame beside the bounding box
+constexpr int kClearFrames = 64; // ... for batches of at most this many frames
 
 enum RecField {
     kXmin = 0, kYmin, kXmax, kYmax, kSide, kNcx, kNcy, kDense, kReach, kDx0, kDx1, kDx2, kNcell, kBig
@@ -117,8 +120,17 @@ __device__ __forceinline__ int64_t cell_base(const int32_t *offsets, int f) {
 }
 
 struct BigGrid {
-    int32_t x0, y0, side, ncx, ncy, dense, reach, dx[3], ncell;
+    int32_t x0, y0, side, ncx, ncy, dense, reach, dx0, dx1, dx2, ncell;  // dx_k: half-width of stencil row |dy| = k
 };
+
+// Half-width of stencil row |dy| (0..2), blended with masks: an indexed
+// array, or selects between the record's fields (which the compiler turns
+// into a select of their addresses), would put the grid record in scratch
+// memory.
+__device__ __forceinline__ int32_t dx_of(const BigGrid &g, int ady) {
+    const int32_t m0 = -(int32_t)(ady == 0), m1 = -(int32_t)(ady == 1);
+    return (g.dx0 & m0) | (g.dx1 & m1) | (g.dx2 & ~(m0 | m1));
+}
 
 __device__ __forceinline__ BigGrid load_grid(const int32_t *rec) {
     BigGrid g;
@@ -129,9 +141,9 @@ __device__ __forceinline__ BigGrid load_grid(const int32_t *rec) {
     g.ncy = rec[kNcy];
     g.dense = rec[kDense];
     g.reach = rec[kReach];
-    g.dx[0] = rec[kDx0];
-    g.dx[1] = rec[kDx1];
-    g.dx[2] = rec[kDx2];
+    g.dx0 = rec[kDx0];
+    g.dx1 = rec[kDx1];
+    g.dx2 = rec[kDx2];
     g.ncell = rec[kNcell];
     return g;
 }
@@ -150,8 +162,26 @@ __global__ __launch_bounds__(kPrepThreads) void big_prep(ClusterArgs a, BigWs w)
     int32_t b, e;
     const bool ok = frame_ok(a, f, &b, &e);
     const int32_t n = ok ? e - b : 0;
-    if (!ok || n <= a.cap_points) {
-        if (tid == 0) rec[kBig] = 0;
+    const bool big = ok && n > 0 && (n > a.cap_points || a.big_all);
+    if (blockIdx.y > 0) {
+        // clearing share of a large frame's cell range (2 n + 2 entries, at
+        // least the ncell + 1 the grid uses), beside the bounding box
+        if (!big) return;
+        const int64_t base = cell_base(a.offsets, f), m = 2 * (int64_t)n + 2;
+        const int64_t per = (m + gridDim.y - 2) / (gridDim.y - 1);
+        const int64_t c0 = (int64_t)(blockIdx.y - 1) * per, c1 = min(m, c0 + per);
+        for (int64_t c = c0 + tid; c < c1; c += kPrepThreads) {
+            w.cstart[base + c] = 0;
+            w.cnode[base + c] = INT_MAX;
+        }
+        return;
+    }
+    if (!big) {
+        if (tid == 0) {
+            rec[kBig] = 0;
+            // without the on-chip kernel, the counts of empty and inconsistent frames
+            if (a.big_all && a.n_clusters) a.n_clusters[f] = ok ? 0 : -1;
+        }
         return;
     }
     if (tid == 0) {
@@ -228,10 +258,12 @@ __global__ __launch_bounds__(kPrepThreads) void big_prep(ClusterArgs a, BigWs w)
         rec[kBig] = 1;
         if (a.n_clusters) a.n_clusters[f] = 0;
     }
-    const int64_t base = cell_base(a.offsets, f);
-    for (int32_t c = tid; c <= ncell; c += kPrepThreads) {
-        w.cstart[base + c] = 0;
-        w.cnode[base + c] = INT_MAX;
+    if (gridDim.y == 1) {  // no clearing workgroups beside this one
+        const int64_t base = cell_base(a.offsets, f);
+        for (int32_t c = tid; c <= ncell; c += kPrepThreads) {
+            w.cstart[base + c] = 0;
+            w.cnode[base + c] = INT_MAX;
+        }
     }
 }
 
@@ -269,11 +301,14 @@ __global__ __launch_bounds__(kScanThreads) void big_scan(ClusterArgs a, BigWs w)
     int32_t *cs = w.cstart + cell_base(a.offsets, f);
     int carry = 0;
     for (int32_t t0 = 0; t0 < ncell; t0 += kTileCells) {
+        // every load in flight before the first use: indexes are clamped
+        // (cs[ncell] exists), values past ncell replaced by 0
+        int ld[kScanUnroll];
 #pragma unroll
-        for (int u = 0; u < kScanUnroll; ++u) {
-            const int32_t c = t0 + u * kScanThreads + tid;
-            s_tile[at(u * kScanThreads + tid)] = c < ncell ? cs[c] : 0;
-        }
+        for (int u = 0; u < kScanUnroll; ++u) ld[u] = cs[min(t0 + u * kScanThreads + tid, ncell)];
+#pragma unroll
+        for (int u = 0; u < kScanUnroll; ++u)
+            s_tile[at(u * kScanThreads + tid)] = t0 + u * kScanThreads + tid < ncell ? ld[u] : 0;
         __syncthreads();
         int v[kScanUnroll], sum = 0;
 #pragma unroll
@@ -317,6 +352,8 @@ __global__ __launch_bounds__(kBlock) void big_scatter(ClusterArgs a, BigWs w) {
     w.ssid[pos] = i - b;
 }
 
+// Neighbour counts (dense cells are all core, the rest stop at min_pts), the
+// union-find parents and kinds, and each core cell's node.
 __global__ __launch_bounds__(kBlock) void big_core(ClusterArgs a, BigWs w) {
     const int32_t p = blockIdx.x * kBlock + threadIdx.x;
     if (p >= a.total) return;
@@ -340,7 +377,7 @@ __global__ __launch_bounds__(kBlock) void big_core(ClusterArgs a, BigWs w) {
             const int dy = (k & 1) ? -((k + 1) >> 1) : (k >> 1);  // 0, -1, 1, -2, 2
             const int32_t ry = cy + dy;
             if (ry < 0 || ry >= g.ncy) continue;
-            const int dxm = g.dx[dy < 0 ? -dy : dy];
+            const int dxm = dx_of(g, dy < 0 ? -dy : dy);
             const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
             const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
             int32_t q = cs[ry * g.ncx + rx0];
@@ -358,26 +395,15 @@ __global__ __launch_bounds__(kBlock) void big_core(ClusterArgs a, BigWs w) {
     const int32_t o = w.ssid[p];
     a.labels[b + o] = o;  // union-find parent
     a.kind[b + o] = core ? 2 : 0;
-}
-
-__global__ __launch_bounds__(kBlock) void big_nodes(ClusterArgs a, BigWs w) {
-    const int32_t p = blockIdx.x * kBlock + threadIdx.x;
-    if (p >= a.total || !w.score[p]) return;
-    const int f = frame_of_point(a.offsets, a.n_frames, p);
-    if (f < 0) return;
-    const int32_t *rec = w.rec + (size_t)f * kRec;
-    if (!rec[kBig] || !rec[kDense]) return;
-    const BigGrid g = load_grid(rec);
-    int32_t cx, cy;
-    cell_xy(w.spos[p], g, &cx, &cy);
-    atomicMin(&w.cnode[cell_base(a.offsets, f) + (int64_t)cy * g.ncx + cx], w.ssid[p]);
+    // a core cell's node: its smallest core index (eps-diagonal grid)
+    if (core && g.dense) atomicMin(&w.cnode[cell_base(a.offsets, f) + own], o);
 }
 
 // k-th forward stencil offset (cells after this one in row-major order).
 __device__ __forceinline__ bool forward_offset(const BigGrid &g, int k, int *odx, int *ody) {
     for (int dy = 0; dy <= g.reach; ++dy) {
-        const int lo = dy == 0 ? 1 : -g.dx[dy];
-        const int cnt = g.dx[dy] - lo + 1;
+        const int lo = dy == 0 ? 1 : -dx_of(g, dy);
+        const int cnt = dx_of(g, dy) - lo + 1;
         if (cnt > 0 && k < cnt) {
             *odx = lo + k;
             *ody = dy;
@@ -390,12 +416,48 @@ __device__ __forceinline__ bool forward_offset(const BigGrid &g, int k, int *odx
 
 constexpr int kMaxForward = 12;
 
+// Point-pair unions of point p when its frame's grid was coarsened.
+__device__ void union_points_one(const ClusterArgs &a, const BigWs &w, int32_t p) {
+    if (p >= a.total || !w.score[p]) return;
+    const int f = frame_of_point(a.offsets, a.n_frames, p);
+    if (f < 0) return;
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig] || rec[kDense]) return;
+    const BigGrid g = load_grid(rec);
+    const int32_t b = a.offsets[f];
+    const int32_t *cs = w.cstart + cell_base(a.offsets, f);
+    const int2 *S = w.spos + b;
+    const uint8_t *core = w.score + b;
+    int32_t *parent = a.labels + b;
+    const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
+    const int32_t lp = p - b;
+    const int2 v = S[lp];
+    const int32_t op = w.ssid[p];
+    int32_t cx, cy;
+    cell_xy(v, g, &cx, &cy);
+    const int32_t own = cy * g.ncx + cx;
+    for (int32_t q = cs[own]; q < lp; ++q)
+        if (core[q] && within(v, S[q], r)) uf_unite<kAgent>(parent, op, w.ssid[b + q]);
+    for (int dy = 0; dy <= g.reach; ++dy) {
+        const int32_t ry = cy + dy;
+        if (ry >= g.ncy) break;
+        const int32_t rx0 = dy == 0 ? cx + 1 : max(cx - dx_of(g, dy), 0);
+        const int32_t rx1 = min(cx + dx_of(g, dy), g.ncx - 1);
+        if (rx0 > rx1) continue;
+        const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
+        for (int32_t q = cs[ry * g.ncx + rx0]; q < q1; ++q)
+            if (core[q] && within(v, S[q], r)) uf_unite<kAgent>(parent, op, w.ssid[b + q]);
+    }
+}
+
 // Cell-pair unions for frames with the eps-diagonal grid: the cores of a
 // cell are one node (its smallest core index).  Two launches: the adjacent
 // cells (far = 0), then the farther ones (far = 1), whose pairs mostly join
 // nodes that the first launch has already connected and skip their tests.
+// The far launch also runs the point unions of coarsened frames.
 __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w, int64_t n_items, int far) {
     const int64_t item = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (far && item < a.total) union_points_one(a, w, (int32_t)item);  // n_items >= total
     if (item >= n_items) return;
     const int64_t c = item / kMaxForward;
     const int k = (int)(item - c * kMaxForward);
@@ -451,41 +513,6 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
     }
 }
 
-// Point-pair unions for frames whose grid was coarsened.
-__global__ __launch_bounds__(kBlock) void big_union_points(ClusterArgs a, BigWs w) {
-    const int32_t p = blockIdx.x * kBlock + threadIdx.x;
-    if (p >= a.total || !w.score[p]) return;
-    const int f = frame_of_point(a.offsets, a.n_frames, p);
-    if (f < 0) return;
-    const int32_t *rec = w.rec + (size_t)f * kRec;
-    if (!rec[kBig] || rec[kDense]) return;
-    const BigGrid g = load_grid(rec);
-    const int32_t b = a.offsets[f];
-    const int32_t *cs = w.cstart + cell_base(a.offsets, f);
-    const int2 *S = w.spos + b;
-    const uint8_t *core = w.score + b;
-    int32_t *parent = a.labels + b;
-    const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
-    const int32_t lp = p - b;
-    const int2 v = S[lp];
-    const int32_t op = w.ssid[p];
-    int32_t cx, cy;
-    cell_xy(v, g, &cx, &cy);
-    const int32_t own = cy * g.ncx + cx;
-    for (int32_t q = cs[own]; q < lp; ++q)
-        if (core[q] && within(v, S[q], r)) uf_unite<kAgent>(parent, op, w.ssid[b + q]);
-    for (int dy = 0; dy <= g.reach; ++dy) {
-        const int32_t ry = cy + dy;
-        if (ry >= g.ncy) break;
-        const int32_t rx0 = dy == 0 ? cx + 1 : max(cx - g.dx[dy], 0);
-        const int32_t rx1 = min(cx + g.dx[dy], g.ncx - 1);
-        if (rx0 > rx1) continue;
-        const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
-        for (int32_t q = cs[ry * g.ncx + rx0]; q < q1; ++q)
-            if (core[q] && within(v, S[q], r)) uf_unite<kAgent>(parent, op, w.ssid[b + q]);
-    }
-}
-
 __global__ __launch_bounds__(kBlock) void big_flatten(ClusterArgs a, BigWs w) {
     const int32_t p = blockIdx.x * kBlock + threadIdx.x;
     bool counted = false;
@@ -511,6 +538,7 @@ __global__ __launch_bounds__(kBlock) void big_flatten(ClusterArgs a, BigWs w) {
     if (counted && a.n_clusters) atomicAdd(&a.n_clusters[f], 1);
 }
 
+// Border points: the nearest core within eps, ties by smaller (y, x).
 __global__ __launch_bounds__(kBlock) void big_border(ClusterArgs a, BigWs w) {
     const int32_t p = blockIdx.x * kBlock + threadIdx.x;
     if (p >= a.total || w.score[p]) return;
@@ -532,7 +560,7 @@ __global__ __launch_bounds__(kBlock) void big_border(ClusterArgs a, BigWs w) {
     for (int dy = -g.reach; dy <= g.reach; ++dy) {
         const int32_t ry = cy + dy;
         if (ry < 0 || ry >= g.ncy) continue;
-        const int dxm = g.dx[dy < 0 ? -dy : dy];
+        const int dxm = dx_of(g, dy < 0 ? -dy : dy);
         const int32_t rx0 = max(cx - dxm, 0), rx1 = min(cx + dxm, g.ncx - 1);
         const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
         // four candidates loaded per step (indices past the span repeat its
@@ -581,17 +609,18 @@ hipError_t launch_cluster_big(const ClusterArgs &a, void *workspace, hipStream_t
     const BigWs w = carve(workspace, a.n_frames, a.total);
     const int64_t cells = 2 * (int64_t)a.total + 2 * (int64_t)a.n_frames;
     const unsigned pts = blocks_for(a.total);
-    hipLaunchKernelGGL(big_prep, dim3(a.n_frames), dim3(kPrepThreads), 0, stream, a, w);
+    // a few frames: each frame's cell range is cleared by kClearBlocks
+    // workgroups beside the one that finds its bounding box
+    const unsigned prep_y = a.n_frames <= kClearFrames ? 1 + kClearBlocks : 1;
+    hipLaunchKernelGGL(big_prep, dim3(a.n_frames, prep_y), dim3(kPrepThreads), 0, stream, a, w);
     if (a.total > 0) {
         hipLaunchKernelGGL(big_hist, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_scan, dim3(a.n_frames), dim3(kScanThreads), 0, stream, a, w);
         hipLaunchKernelGGL(big_scatter, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_core, dim3(pts), dim3(kBlock), 0, stream, a, w);
-        hipLaunchKernelGGL(big_nodes, dim3(pts), dim3(kBlock), 0, stream, a, w);
         const int64_t items = cells * kMaxForward;
         hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items, 0);
         hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items, 1);
-        hipLaunchKernelGGL(big_union_points, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_flatten, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_border, dim3(pts), dim3(kBlock), 0, stream, a, w);
     }

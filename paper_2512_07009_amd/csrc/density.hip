@@ -357,14 +357,15 @@ __device__ __forceinline__ void contract_y(float4v (&acc)[TM][TN], const half8 (
 }
 
 // A work item is (frame, output region of 16 TM rows x 16 TN columns, slice
-// of the frame's birds); `waves` waves of a workgroup share an item, each
-// taking a contiguous part of the slice, and their tiles are added in a fixed
-// order at the end (deterministic).  With split > 1 the slices' grids go to
-// `partial` for a second kernel to add.
+// of the frame's birds); `waves` waves of a workgroup share an item, and
+// their tiles are added in a fixed order at the end (deterministic).  With
+// split > 1 the slices' grids go to `partial` for a second kernel to add.
+// The slices and waves of a (frame, region) take the frame's 64-bird blocks
+// in turn (a fixed assignment).
 //
 // Only birds whose window of cells (G - j .. G + j on both axes) meets the
 // region contribute to it: every other bird's factors there are table zeros.
-// Each wave reads its birds 64 at a time (one per lane), keeps the ones that
+// Each wave reads its blocks one at a time (one bird per lane), keeps the ones that
 // meet the region, in input order, in a ring of staged birds in LDS (ballot
 // ranks), and runs a k-step whenever 32 are staged; the last step is padded
 // with birds whose factors are all zero.  No barrier is needed until the
@@ -399,9 +400,11 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
         const int32_t e = a.offsets[f + 1];
         n = (b < 0 || e < b || e > a.total) ? 0 : e - b;
     }
-    const int32_t k0 = (int32_t)((int64_t)n * sl / split), k1 = (int32_t)((int64_t)n * (sl + 1) / split);
-    const int32_t p0 = k0 + (int32_t)((int64_t)(k1 - k0) * part / waves);
-    const int32_t p1 = k0 + (int32_t)((int64_t)(k1 - k0) * (part + 1) / waves);
+    // the split * waves (slice, part) units of a (frame, region) take the
+    // frame's 64-bird blocks in turn: unit u = sl * waves + part reads blocks
+    // u, u + split * waves, ...  Spatially grouped birds in the input then
+    // spread over all units instead of loading one of them.
+    const int32_t stride = 64 * split * waves;
     const int2 *P = reinterpret_cast<const int2 *>(a.xy) + b;
 
     GBird *ring = reinterpret_cast<GBird *>(lds + gg.table_bytes) + wave * kGRing;
@@ -422,31 +425,58 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
 
     // the first round's coordinates are in flight while the tables are built
     int2 qn = make_int2(0, 0);
-    if (p0 + lane < p1) qn = P[p0 + lane];
-    // the factor tables (exact: every distance is a multiple of 1/32 px), one
-    // row per thread: its PW factors in registers, then its pairs
+    int32_t next = 64 * (sl * waves + part);  // first bird of the next round
+    if (next + lane < n) qn = P[next + lane];
+    // the factor tables (exact: every distance is a multiple of 1/32 px).  A
+    // row's PW factors come in PW / 16 chunks of 16, one per thread, the
+    // threads of a row in adjacent lanes.  Entries -16 .. PW - 1 of a row form
+    // PW / 16 + 1 blocks of 16; block b pairs chunk b - 1 (low halves) with
+    // chunk b (high halves), chunks -1 and PW / 16 being zeros.  The thread of
+    // chunk k writes block k + 1 with its right neighbour's chunk, and the
+    // thread of chunk 0 also writes block 0.
     auto build = [&](const GatherAxis &t) {
-        for (int r = tid; r < t.c; r += kGThreads) {
-            uint32_t v[PW];
+        constexpr int kCh = PW / 16;
+        const int k = tid % kCh;
+        for (int r0 = 0; r0 < t.c; r0 += kGThreads / kCh) {  // uniform over the workgroup
+            const int r = r0 + tid / kCh;
+            uint32_t mine[8];  // factors 16 k + 2 q (low half) and 16 k + 2 q + 1 (high half)
 #pragma unroll
-            for (int i = 0; i < PW; ++i) {
-                float f = 0.0f;
-                if (i >= 1 && i <= 2 * t.j + 1) {
-                    const float d = (((float)(i - 1 - t.j) + 0.5f) * (float)t.c - (float)r) * 0.0625f;
-                    f = kLift * __builtin_amdgcn_exp2f(d * d * gg.neg_k);
+            for (int q = 0; q < 8; ++q) {
+                uint32_t h[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int i = 16 * k + 2 * q + u;
+                    float f = 0.0f;
+                    if (i >= 1 && i <= 2 * t.j + 1) {
+                        const float d = (((float)(i - 1 - t.j) + 0.5f) * (float)t.c - (float)r) * 0.0625f;
+                        f = kLift * __builtin_amdgcn_exp2f(d * d * gg.neg_k);
+                    }
+                    h[u] = __builtin_bit_cast(uint16_t, (_Float16)f);
                 }
-                v[i] = __builtin_bit_cast(uint16_t, (_Float16)f);
+                mine[q] = h[0] | (h[1] << 16);
             }
-            uint4 *row = reinterpret_cast<uint4 *>(lds + t.tab + r * (PW + 16) * 4);
+            uint32_t right[8];
 #pragma unroll
-            for (int q = 0; q < (PW + 16) / 4; ++q) {
-                uint32_t w[4];
+            for (int q = 0; q < 8; ++q) {
+                const uint32_t v = (uint32_t)__shfl_down((int)mine[q], 1, 64);
+                right[q] = k + 1 < kCh ? v : 0u;
+            }
+            if (r < t.c) {
+                uint4 *row = reinterpret_cast<uint4 *>(lds + t.tab + r * (PW + 16) * 4);
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int i = 4 * q + u - 16;  // entry i = (T(i), T(i + 16)); T = 0 past PW - 2
-                    w[u] = (i >= 0 ? v[i] : 0u) | ((i + 16 < PW ? v[i + 16] : 0u) << 16);
+                for (int q = 0; q < 4; ++q) {
+                    // entries 16 k + 4 q .. + 3 of block k + 1: (mine, right) pairs
+                    row[4 * (k + 1) + q] = make_uint4(__builtin_amdgcn_perm(right[2 * q], mine[2 * q], 0x05040100u),
+                                                      __builtin_amdgcn_perm(right[2 * q], mine[2 * q], 0x07060302u),
+                                                      __builtin_amdgcn_perm(right[2 * q + 1], mine[2 * q + 1], 0x05040100u),
+                                                      __builtin_amdgcn_perm(right[2 * q + 1], mine[2 * q + 1], 0x07060302u));
                 }
-                row[q] = make_uint4(w[0], w[1], w[2], w[3]);
+                if (k == 0) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)  // block 0: (0, chunk 0)
+                        row[q] = make_uint4(mine[2 * q] << 16, mine[2 * q] & 0xffff0000u, mine[2 * q + 1] << 16,
+                                            mine[2 * q + 1] & 0xffff0000u);
+                }
             }
         }
     };
@@ -463,16 +493,15 @@ __global__ __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2))) 
     };
     const uint64_t below = (1ull << lane) - 1ull;
     int32_t head = 0, tail = 0;  // ring positions, taken modulo kGRing
-    int32_t next = p0;           // first bird of the next round
     // stage rounds of 64 birds until a k-step's worth meets the region (or
     // the birds run out); the last, partial step is filled with birds whose
     // factors are all zero
     auto fill = [&] {
-        while (tail - head < kGStep && next < p1) {
+        while (tail - head < kGStep && next < n) {
             const int2 q = qn;
-            const bool have = next + lane < p1;
-            next += 64;
-            if (next + lane < p1) qn = P[next + lane];  // the following round in flight
+            const bool have = next + lane < n;
+            next += stride;
+            if (next + lane < n) qn = P[next + lane];  // the following round in flight
             GBird gb{gg.ay.tab, kGFar, gg.ax.tab, kGFar};
             bool keep = false;
             if (have) {
@@ -781,7 +810,11 @@ DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit) {
     GatherGeom gg;
     if (!force_recur && make_gather_geom(a, &gg) && (size_t)gg.lds_bytes <= lds_limit) {
         const double birds = a.n_frames > 0 ? (double)a.total / a.n_frames : 0.0;
-        const Shape sh = gather_shape(gg.ay.j, gg.ax.j, a.grid_w, a.grid_h, birds);
+        Shape sh = gather_shape(gg.ay.j, gg.ax.j, a.grid_w, a.grid_h, birds);
+        int grm = 0, grn = 0;
+        if (force && std::sscanf(force, "%d,%d", &grm, &grn) == 2)
+            for (const Shape &k : kGShapes)
+                if (k.rm == grm && k.rn == grn) sh = k;
         DensityPlan p{};
         p.gather = 1;
         p.rm = sh.rm;

@@ -24,6 +24,9 @@ struct ClusterArgs {
     int32_t cap_cells;        // cell-table entries available on chip
     int32_t big_path;         // 1: frames above cap_points go to the multi-workgroup
                               // path; 0: the on-chip kernel clusters them in place
+    int32_t big_all;          // 1: the multi-workgroup path takes every frame and also
+                              // writes the counts of empty and inconsistent frames
+                              // (the on-chip kernel is not launched)
     int32_t union_regs;       // 1: the on-chip unions keep up to 3072 core cells'
                               // edges in registers; 0: always re-read them from LDS
     // Neighbour-cell tables for cells of side cell_side (as the on-chip

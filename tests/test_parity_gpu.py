@@ -251,6 +251,23 @@ def test_lattice_ties_gpu():
         assert_cluster_equal(got, xy, off, 640, min_pts, tag=f"lattice minPts {min_pts}")
 
 
+def test_single_large_frame_gpu():
+    """A batch of one frame above the on-chip capacity runs the
+    multi-workgroup path alone (no on-chip launch).  With offsets that break
+    the contract, a frame past total gets n_clusters -1 and a frame shorter
+    than total is still clustered."""
+    rng = np.random.default_rng(21)
+    big = np.stack([rng.integers(0, 16 * 900, 12000), rng.integers(0, 16 * 700, 12000)], 1).astype(np.int32)
+    xy, off = wl.pack([big])
+    got = run_cluster(xy, off, 160, 5, max_fp=0)
+    assert_cluster_equal(got, xy, off, 160, 5, tag="one large frame")
+    _, _, ncl = run_cluster(xy, np.array([0, 13000], np.int32), 160, 5, max_fp=0)
+    assert ncl[0] == -1
+    short = np.array([0, 500], np.int32)
+    got = run_cluster(xy, short, 160, 5, max_fp=0)
+    assert_cluster_equal(got, xy, short, 160, 5, tag="frame shorter than total")
+
+
 def test_bad_offsets_do_not_fault_gpu():
     xy = np.zeros((10, 2), np.int32)
     off = np.array([0, 5, 3, 10, 12], np.int32)   # frame 1 negative, frame 3 past total
