@@ -1225,6 +1225,18 @@ __device__ __forceinline__ void cluster_resident(const ClusterArgs &a) {
         const int32_t nl = s_nlist;
         const int ns = s_nsten;
         const int gl = lane & (kBorderLanes - 1);
+        // this lane's stencil cells gl, gl + kBorderLanes, ... are the same
+        // for every point: their offsets stay in registers
+        constexpr int kSlots = (kMaxStencil + kBorderLanes - 1) / kBorderLanes;
+        int32_t sdx[kSlots], sdy[kSlots];
+        bool sv[kSlots];
+#pragma unroll
+        for (int k = 0; k < kSlots; ++k) {
+            const int st = gl + k * kBorderLanes;
+            sv[k] = st < ns;
+            sdx[k] = sv[k] ? s_sdx[st] : 0;
+            sdy[k] = sv[k] ? s_sdy[st] : 0;
+        }
         for (int32_t j = tid / kBorderLanes; j < nl; j += kThreads / kBorderLanes) {
             const int32_t p = list[j];
             const uint32_t v = pxy[p];
@@ -1233,18 +1245,41 @@ __device__ __forceinline__ void cluster_resident(const ClusterArgs &a) {
             cell_id(v, g, &cx, &cy);
             uint64_t bestk = ~0ull;
             int32_t best = -1;
-            for (int s = gl; s < ns; s += kBorderLanes) {
-                const int32_t rx = cx + s_sdx[s], ry = cy + s_sdy[s];
-                if ((rx < 0) | (rx >= g.ncx) | (ry < 0) | (ry >= g.ncy)) continue;
-                const int32_t c = ry * g.ncx + rx;
-                const uint32_t cw = cell[c];
-                if ((cw >> 16) == kNone) continue;  // no core in this cell
+            // every cell word of the lane's cells first (one round of LDS loads)
+            uint32_t cw[kSlots], ce[kSlots];
+            bool ok[kSlots];
+#pragma unroll
+            for (int k = 0; k < kSlots; ++k) {
+                const int32_t rx = cx + sdx[k], ry = cy + sdy[k];
+                ok[k] = sv[k] & (rx >= 0) & (rx < g.ncx) & (ry >= 0) & (ry < g.ncy);
+                const int32_t c = ok[k] ? ry * g.ncx + rx : 0;
+                cw[k] = cell[c];
+                ce[k] = cell[c + 1];
+            }
+#pragma unroll
+            for (int k = 0; k < kSlots; ++k) {
+                if (!ok[k] || (cw[k] >> 16) == kNone) continue;  // no core in this cell
+                const int32_t rx = cx + sdx[k], ry = cy + sdy[k];
                 const int32_t x0c = rx * g.side, y0c = ry * g.side;
                 const int32_t ddx = min(max(max(x0c - vx, vx - (x0c + g.side - 1)), 0), r.e1);
                 const int32_t ddy = min(max(max(y0c - vy, vy - (y0c + g.side - 1)), 0), r.e1);
                 if (__mul24(ddx, ddx) + __mul24(ddy, ddy) > r.e2) continue;  // cell out of reach
-                const int32_t q1 = cstart(c + 1);
-                for (int32_t q = (int32_t)(cw & 0xffffu); q < q1; ++q) {
+                const int32_t q1 = (int32_t)(ce[k] & 0xffffu);
+                int32_t q = (int32_t)(cw[k] & 0xffffu);
+                for (; q + 1 < q1; q += 2) {  // two candidates per step, in order
+                    const uint32_t w0 = pxy[q], w1 = pxy[q + 1];
+                    const bool c0 = score[q] == kCore, c1 = score[q + 1] == kCore;
+                    const int32_t d0 = sq_dist_pk(v, w0, r.e1), d1 = sq_dist_pk(v, w1, r.e1);
+                    const uint64_t k0 = ((uint64_t)(uint32_t)d0 << 32) | w0;
+                    const uint64_t k1 = ((uint64_t)(uint32_t)d1 << 32) | w1;
+                    const bool t0 = (d0 <= r.e2) & c0 & (k0 < bestk);
+                    best = t0 ? q : best;
+                    bestk = t0 ? k0 : bestk;
+                    const bool t1 = (d1 <= r.e2) & c1 & (k1 < bestk);
+                    best = t1 ? q + 1 : best;
+                    bestk = t1 ? k1 : bestk;
+                }
+                if (q < q1) {
                     const uint32_t w = pxy[q];
                     const int32_t d2 = sq_dist_pk(v, w, r.e1);
                     const uint64_t key = ((uint64_t)(uint32_t)d2 << 32) | w;
