@@ -481,7 +481,10 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
     if (nb == INT_MAX) return;
     const int32_t b = a.offsets[f];
     int32_t *parent = a.labels + b;
-    if (uf_find<kAgent>(parent, na) == uf_find<kAgent>(parent, nb)) return;
+    // the farther pairs mostly join nodes already connected: skip those
+    // before the point tests (the adjacent pairs rarely are; their unite
+    // finds the roots anyway)
+    if (far && uf_find<kAgent>(parent, na) == uf_find<kAgent>(parent, nb)) return;
     const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
     const int32_t *cs = w.cstart + base;
     const int32_t a0 = cs[ca], a1 = cs[ca + 1], b0 = cs[cb], b1 = cs[cb + 1];
