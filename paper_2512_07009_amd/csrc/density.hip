@@ -249,7 +249,7 @@ constexpr int kGStep = 32;                 // birds per MFMA k-step (16 x 16 x 3
 constexpr int kGRedTiles = 8;              // 16 x 16 tiles per round of the cross-wave sum
 constexpr int kGRing = 128;                // staged birds per wave (one k-step left over + one round)
 constexpr int kGMaxTableBytes = 96 * 1024; // both factor tables
-constexpr int kGMinWaveBirds = 48;         // kept birds per wave, at least, when a launch splits frames
+constexpr int kGMinWaveBirds = 32;         // kept birds per wave, at least, when a launch splits frames
 constexpr int32_t kGFar = 1 << 28;         // bird term that clamps every row to a zero entry
 
 typedef float float4v __attribute__((ext_vector_type(4)));
@@ -701,10 +701,11 @@ double step_cycles(const Shape &sh) { return 112.0 * ((sh.rm + 1) / 2 + (sh.rn +
 // k-step share on every region its window meets, the test that keeps or
 // drops every bird on every region (about 3 cycles a bird), and a fixed cost
 // per region (tables, the final sum and the stores).
-Shape gather_shape(int jy, int jx, int grid_w, int grid_h, double birds) {
+Shape gather_shape(int jy, int jx, int grid_w, int grid_h, double birds, int max_tiles = 1 << 30) {
     Shape best = kGShapes[0];
     double best_cost = 1e300;
     for (const Shape &sh : kGShapes) {
+        if (sh.rm * sh.rn > max_tiles) continue;
         const long long ry = axis_regions(grid_h, 16 * sh.rm), rx = axis_regions(grid_w, 16 * sh.rn);
         const double meets = ry * meet_share(jy, 16 * sh.rm, ry) * rx * meet_share(jx, 16 * sh.rn, rx);
         const double cost = birds / kGStep * meets * step_cycles(sh) + (3.2 * birds + 4000.0) * (double)(ry * rx);
@@ -824,6 +825,20 @@ DensityPlan plan_density(const DensityArgs &a, int n_cus, size_t lds_limit) {
         const double kept = birds * meet_share(gg.ay.j, 16 * sh.rm, p.regions_y) *
                             meet_share(gg.ax.j, 16 * sh.rn, p.regions_x);
         gather_split(a.n_frames, kept, (long long)p.regions_y * p.regions_x, n_cus, &p.waves, &p.split);
+        if (p.split > 1 && !(force && grm)) {
+            // few frames for the chip: the launch is bound by each wave's own
+            // path, whose fixed part grows with the tiles an item's waves add
+            // up at the end (kGRedTiles per round); shapes of at most 16 tiles
+            // keep that to two rounds
+            sh = gather_shape(gg.ay.j, gg.ax.j, a.grid_w, a.grid_h, birds, 16);
+            p.rm = sh.rm;
+            p.rn = sh.rn;
+            p.regions_y = (a.grid_h + 16 * sh.rm - 1) / (16 * sh.rm);
+            p.regions_x = (a.grid_w + 16 * sh.rn - 1) / (16 * sh.rn);
+            const double kept2 = birds * meet_share(gg.ay.j, 16 * sh.rm, p.regions_y) *
+                                 meet_share(gg.ax.j, 16 * sh.rn, p.regions_x);
+            gather_split(a.n_frames, kept2, (long long)p.regions_y * p.regions_x, n_cus, &p.waves, &p.split);
+        }
         const long long items = (long long)a.n_frames * p.regions_y * p.regions_x * p.split;
         const int per_wg = kGWaves / p.waves;
         p.blocks = (items + per_wg - 1) / per_wg;
