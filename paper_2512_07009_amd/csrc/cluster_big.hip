@@ -23,10 +23,13 @@
 // caller's labels array (frame-local indices), with agent-scope atomics.
 //
 // Kernels, in stream order: prep (one workgroup per frame: bounding box,
-// grid, clearing), hist (cell counts and ranks), scan (one workgroup per
-// frame), scatter, core (neighbour counts with early exit), nodes (each
-// cell's smallest core index), union (cell pairs, or point pairs when the
-// grid was coarsened), flatten (labels of cores, cluster counts), border.
+// grid; the cell clearing there or, for a few frames, in extra workgroups
+// beside it), hist (cell counts and ranks), scan (one workgroup per frame),
+// scatter, core (neighbour counts with early exit, and each cell's smallest
+// core index), union of adjacent cell pairs, union of the farther cell pairs
+// (and point pairs where the grid was coarsened), flatten (labels of cores,
+// cluster counts), border.  A batch of one large frame skips the on-chip
+// kernel, and prep then writes the counts of an empty or inconsistent frame.
 
 #include <algorithm>
 #include <climits>
@@ -415,6 +418,7 @@ __device__ __forceinline__ bool forward_offset(const BigGrid &g, int k, int *odx
 }
 
 constexpr int kMaxForward = 12;
+constexpr int kAdjacent = 4;  // forward adjacent cells
 
 // Point-pair unions of point p when its frame's grid was coarsened.
 __device__ void union_points_one(const ClusterArgs &a, const BigWs &w, int32_t p) {
@@ -459,8 +463,9 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
     const int64_t item = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (far && item < a.total) union_points_one(a, w, (int32_t)item);  // n_items >= total
     if (item >= n_items) return;
-    const int64_t c = item / kMaxForward;
-    const int k = (int)(item - c * kMaxForward);
+    const int per = far ? kMaxForward : kAdjacent;
+    const int64_t c = item / per;
+    const int k = (int)(item - c * per);
     const int f = frame_of_cell(a.offsets, a.n_frames, c);
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig] || !rec[kDense]) return;
@@ -471,8 +476,14 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
     const int32_t na = w.cnode[base + ca];
     if (na == INT_MAX) return;
     int odx, ody;
-    if (!forward_offset(g, k, &odx, &ody)) return;
-    if ((odx >= -1 && odx <= 1 && ody <= 1) == (far != 0)) return;  // the other launch's pair
+    if (!far) {
+        // the forward adjacent cells (1, 0), (-1, 1), (0, 1), (1, 1)
+        odx = k == 0 ? 1 : k - 2;
+        ody = k == 0 ? 0 : 1;
+    } else {
+        if (!forward_offset(g, k, &odx, &ody)) return;
+        if (odx >= -1 && odx <= 1 && ody <= 1) return;  // an adjacent pair: the first launch's
+    }
     const int32_t ay = ca / g.ncx, ax = ca - ay * g.ncx;
     const int32_t bx = ax + odx, by = ay + ody;
     if (bx < 0 || bx >= g.ncx || by >= g.ncy) return;
@@ -621,8 +632,8 @@ hipError_t launch_cluster_big(const ClusterArgs &a, void *workspace, hipStream_t
         hipLaunchKernelGGL(big_scan, dim3(a.n_frames), dim3(kScanThreads), 0, stream, a, w);
         hipLaunchKernelGGL(big_scatter, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_core, dim3(pts), dim3(kBlock), 0, stream, a, w);
-        const int64_t items = cells * kMaxForward;
-        hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items, 0);
+        const int64_t adj = cells * kAdjacent, items = cells * kMaxForward;
+        hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(adj)), dim3(kBlock), 0, stream, a, w, adj, 0);
         hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items, 1);
         hipLaunchKernelGGL(big_flatten, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_border, dim3(pts), dim3(kBlock), 0, stream, a, w);
