@@ -20,16 +20,18 @@
 // side doubles from the eps-diagonal side until the grid fits; the same-cell
 // shortcut holds only at the undoubled side), so the table never depends on
 // anything the host does not know.  The union-find forest lives in the
-// caller's labels array (frame-local indices), with agent-scope atomics.
+// caller's labels array (frame-local indices): walks read it through the
+// cache, hooks are agent-scope compare-and-swap.
 //
 // Kernels, in stream order: prep (one workgroup per frame: bounding box,
 // grid; the cell clearing there or, for a few frames, in extra workgroups
 // beside it), hist (cell counts and ranks), scan (one workgroup per frame),
 // scatter, core (neighbour counts with early exit, and each cell's smallest
 // core index), union of adjacent cell pairs, union of the farther cell pairs
-// (and point pairs where the grid was coarsened), flatten (labels of cores,
-// cluster counts), border.  A batch of one large frame skips the on-chip
-// kernel, and prep then writes the counts of an empty or inconsistent frame.
+// (and point pairs where the grid was coarsened), labels (cores: their
+// tree's root and the cluster counts; other points: the root of the nearest
+// core's tree).  A batch of one large frame skips the on-chip kernel, and
+// prep then writes the counts of an empty or inconsistent frame.
 
 #include <algorithm>
 #include <climits>
@@ -45,7 +47,7 @@ using namespace cl;
 constexpr int kBlock = 256;
 constexpr int kScanThreads = 1024;
 constexpr int kPrepThreads = 1024;
-constexpr int kUnroll = 8;       // independent loads per thread and step in the bounding box
+constexpr int kUnroll = 32;      // independent loads per thread and step in the bounding box
 constexpr int kScanUnroll = 32;  // cells per thread in a scan tile (32768 cells, 132 KiB of LDS)
 constexpr int kRec = 16;  // int32 fields per frame record
 constexpr int kClearBlocks = 8;  // cell-clearing workgroups per frame beside the bounding box
@@ -420,6 +422,48 @@ __device__ __forceinline__ bool forward_offset(const BigGrid &g, int k, int *odx
 constexpr int kMaxForward = 12;
 constexpr int kAdjacent = 4;  // forward adjacent cells
 
+// Walks a and b to their roots through cached parents, in step (one load
+// latency per level of the deeper tree).  Path splitting here (plain
+// stores of grandparents) made both the unions and the later label walks
+// slower.
+__device__ __forceinline__ void roots_cached(const int32_t *parent, int32_t *a, int32_t *b) {
+    int32_t x = *a, y = *b;
+    for (;;) {
+        const int32_t px = ld_rlx<kGroup>(parent + x), py = ld_rlx<kGroup>(parent + y);
+        if ((px == x) & (py == y)) break;
+        x = px;
+        y = py;
+    }
+    *a = x;
+    *b = y;
+}
+
+// Merge the trees of nodes a and b in a frame's global forest.  The walks
+// read parents through the cache of this workgroup's XCD, so they may miss
+// what workgroups on other XCDs hooked during this launch; every value they
+// see is still an ancestor (a parent only ever moves to a smaller node of
+// the same tree), so a walk ends at some ancestor.  Only the compare-and-swap
+// that hooks a root under a smaller node is coherent (agent scope); when it
+// fails, the parent it returns is current and the walk goes on from there.
+// Each failure lowers the larger of the two nodes, so the loop ends, and
+// every tree's root stays its smallest node.
+__device__ __forceinline__ void uf_unite_cached(int32_t *parent, int32_t a, int32_t b) {
+    roots_cached(parent, &a, &b);
+    for (;;) {
+        if (a == b) return;
+        if (a < b) {
+            const int32_t t = a;
+            a = b;
+            b = t;
+        }
+        int32_t expected = a;
+        if (__hip_atomic_compare_exchange_strong(parent + a, &expected, b, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                 kAgent))
+            return;
+        a = uf_root<kGroup>(parent, expected);
+    }
+}
+
 // Point-pair unions of point p when its frame's grid was coarsened.
 __device__ void union_points_one(const ClusterArgs &a, const BigWs &w, int32_t p) {
     if (p >= a.total || !w.score[p]) return;
@@ -441,7 +485,7 @@ __device__ void union_points_one(const ClusterArgs &a, const BigWs &w, int32_t p
     cell_xy(v, g, &cx, &cy);
     const int32_t own = cy * g.ncx + cx;
     for (int32_t q = cs[own]; q < lp; ++q)
-        if (core[q] && within(v, S[q], r)) uf_unite<kAgent>(parent, op, w.ssid[b + q]);
+        if (core[q] && within(v, S[q], r)) uf_unite_cached(parent, op, w.ssid[b + q]);
     for (int dy = 0; dy <= g.reach; ++dy) {
         const int32_t ry = cy + dy;
         if (ry >= g.ncy) break;
@@ -450,7 +494,7 @@ __device__ void union_points_one(const ClusterArgs &a, const BigWs &w, int32_t p
         if (rx0 > rx1) continue;
         const int32_t q1 = cs[ry * g.ncx + rx1 + 1];
         for (int32_t q = cs[ry * g.ncx + rx0]; q < q1; ++q)
-            if (core[q] && within(v, S[q], r)) uf_unite<kAgent>(parent, op, w.ssid[b + q]);
+            if (core[q] && within(v, S[q], r)) uf_unite_cached(parent, op, w.ssid[b + q]);
     }
 }
 
@@ -473,8 +517,6 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
     const int64_t base = cell_base(a.offsets, f);
     const int32_t ca = (int32_t)(c - base);
     if (ca >= g.ncell) return;
-    const int32_t na = w.cnode[base + ca];
-    if (na == INT_MAX) return;
     int odx, ody;
     if (!far) {
         // the forward adjacent cells (1, 0), (-1, 1), (0, 1), (1, 1)
@@ -488,14 +530,19 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
     const int32_t bx = ax + odx, by = ay + ody;
     if (bx < 0 || bx >= g.ncx || by >= g.ncy) return;
     const int32_t cb = by * g.ncx + bx;
-    const int32_t nb = w.cnode[base + cb];
-    if (nb == INT_MAX) return;
+    const int32_t na = w.cnode[base + ca], nb = w.cnode[base + cb];  // both loads in flight
+    if ((na == INT_MAX) | (nb == INT_MAX)) return;
     const int32_t b = a.offsets[f];
     int32_t *parent = a.labels + b;
     // the farther pairs mostly join nodes already connected: skip those
     // before the point tests (the adjacent pairs rarely are; their unite
-    // finds the roots anyway)
-    if (far && uf_find<kAgent>(parent, na) == uf_find<kAgent>(parent, nb)) return;
+    // finds the roots anyway).  Cached walks: a common ancestor in a view
+    // that misses recent hooks is still a common ancestor.
+    if (far) {
+        int32_t ra = na, rb = nb;
+        roots_cached(parent, &ra, &rb);
+        if (ra == rb) return;
+    }
     const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
     const int32_t *cs = w.cstart + base;
     const int32_t a0 = cs[ca], a1 = cs[ca + 1], b0 = cs[cb], b1 = cs[cb + 1];
@@ -521,53 +568,50 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
         }
         for (; qb < b1 && !hit; ++qb) hit = core[qb] && within(va, S[qb], r);
         if (hit) {
-            uf_unite<kAgent>(parent, na, nb);
+            uf_unite_cached(parent, na, nb);
             return;
         }
     }
 }
 
-__global__ __launch_bounds__(kBlock) void big_flatten(ClusterArgs a, BigWs w) {
-    const int32_t p = blockIdx.x * kBlock + threadIdx.x;
-    bool counted = false;
-    int f = 0;
-    if (p < a.total && w.score[p]) {
-        f = frame_of_point(a.offsets, a.n_frames, p);
-        if (f >= 0 && w.rec[(size_t)f * kRec + kBig]) {
-            const int32_t *rec = w.rec + (size_t)f * kRec;
-            const BigGrid g = load_grid(rec);
-            const int32_t b = a.offsets[f];
-            const int32_t o = w.ssid[p];
-            int32_t node = o;
-            if (g.dense) {
-                int32_t cx, cy;
-                cell_xy(w.spos[p], g, &cx, &cy);
-                node = w.cnode[cell_base(a.offsets, f) + (int64_t)cy * g.ncx + cx];
-            }
-            const int32_t root = uf_root<kAgent>(a.labels + b, node);
-            st_rlx<kAgent>(a.labels + b + o, root);
-            counted = root == o;
-        }
-    }
-    if (counted && a.n_clusters) atomicAdd(&a.n_clusters[f], 1);
+// Labels, one thread per sorted point, after the unions have ended: a core
+// takes its tree's root (its cell's node on the eps-diagonal grid, else the
+// point itself, walked to the root) and counts the cluster if it is that
+// root; a non-core point searches its stencil for the nearest core within
+// eps (ties by smaller (y, x)) and takes the root of that core's node.  The
+// walks read parents through the cache: the forest no longer changes but
+// for cores storing their roots, which leaves every walk's end the same.
+__device__ __forceinline__ int32_t node_of(const BigWs &w, const ClusterArgs &a, const BigGrid &g, int f, int32_t b,
+                                           int32_t q, int2 v) {
+    if (!g.dense) return w.ssid[b + q];
+    int32_t cx, cy;
+    cell_xy(v, g, &cx, &cy);
+    return w.cnode[cell_base(a.offsets, f) + (int64_t)cy * g.ncx + cx];
 }
 
-// Border points: the nearest core within eps, ties by smaller (y, x).
-__global__ __launch_bounds__(kBlock) void big_border(ClusterArgs a, BigWs w) {
+__global__ __launch_bounds__(kBlock) void big_label(ClusterArgs a, BigWs w) {
     const int32_t p = blockIdx.x * kBlock + threadIdx.x;
-    if (p >= a.total || w.score[p]) return;
+    if (p >= a.total) return;
     const int f = frame_of_point(a.offsets, a.n_frames, p);
     if (f < 0) return;
     const int32_t *rec = w.rec + (size_t)f * kRec;
     if (!rec[kBig]) return;
     const BigGrid g = load_grid(rec);
     const int32_t b = a.offsets[f];
+    int32_t *parent = a.labels + b;
+    const int32_t o = w.ssid[p];
+    const int2 v = w.spos[p];
+    if (w.score[p]) {
+        const int32_t root = uf_root<kGroup>(parent, node_of(w, a, g, f, b, p - b, v));
+        st_rlx<kAgent>(parent + o, root);
+        if (root == o && a.n_clusters) atomicAdd(&a.n_clusters[f], 1);
+        return;
+    }
     const int64_t base = cell_base(a.offsets, f);
     const int32_t *cs = w.cstart + base;
     const int2 *S = w.spos + b;
     const uint8_t *core = w.score + b;
     const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
-    const int2 v = w.spos[p];
     int32_t cx, cy;
     cell_xy(v, g, &cx, &cy);
     int32_t best = -1, best_d2 = INT32_MAX, by = 0, bx = 0;
@@ -599,12 +643,11 @@ __global__ __launch_bounds__(kBlock) void big_border(ClusterArgs a, BigWs w) {
             }
         }
     }
-    const int32_t o = w.ssid[p];
     if (best >= 0) {
-        a.labels[b + o] = a.labels[b + w.ssid[b + best]];
+        parent[o] = uf_root<kGroup>(parent, node_of(w, a, g, f, b, best, make_int2(bx, by)));
         a.kind[b + o] = 1;
     } else {
-        a.labels[b + o] = -1;
+        parent[o] = -1;
     }
 }
 
@@ -635,8 +678,7 @@ hipError_t launch_cluster_big(const ClusterArgs &a, void *workspace, hipStream_t
         const int64_t adj = cells * kAdjacent, items = cells * kMaxForward;
         hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(adj)), dim3(kBlock), 0, stream, a, w, adj, 0);
         hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items, 1);
-        hipLaunchKernelGGL(big_flatten, dim3(pts), dim3(kBlock), 0, stream, a, w);
-        hipLaunchKernelGGL(big_border, dim3(pts), dim3(kBlock), 0, stream, a, w);
+        hipLaunchKernelGGL(big_label, dim3(pts), dim3(kBlock), 0, stream, a, w);
     }
     return hipGetLastError();
 }
