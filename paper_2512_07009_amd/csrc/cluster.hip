@@ -988,25 +988,25 @@ __device__ __forceinline__ void cluster_resident(const ClusterArgs &a) {
     }
     __syncthreads();
     // scatter into sorted order; 4a. on the way, a cell holding >= min_pts
-    // points is all core, and the other points go to the work list
+    // points is all core
 #pragma unroll
     for (int k = 0; k < PTS; ++k) {
         const int32_t i = tid + k * kThreads;
-        if (tid - lane + k * kThreads >= n) break;  // wave-uniform
-        bool need = false;
-        int32_t pos = 0;
-        if (i < n) {
-            int32_t cx, cy;
-            const int32_t c = cell_id(pv[k], g, &cx, &cy);
-            const int32_t c0 = cstart(c);
-            pos = c0 + prank[k];
-            pxy[pos] = pv[k];
-            sid[pos] = (uint16_t)i;
-            const bool dense = g.dense_ok && cstart(c + 1) - c0 >= a.min_pts;
-            score[pos] = dense ? kCore : 0;
-            need = !dense;
-        }
-        wave_append(need, (uint16_t)pos, list, &s_nlist);
+        if (i >= n) break;
+        int32_t cx, cy;
+        const int32_t c = cell_id(pv[k], g, &cx, &cy);
+        const int32_t c0 = cstart(c);
+        const int32_t pos = c0 + prank[k];
+        pxy[pos] = pv[k];
+        sid[pos] = (uint16_t)i;
+        score[pos] = g.dense_ok && cstart(c + 1) - c0 >= a.min_pts ? kCore : 0;
+    }
+    __syncthreads();
+    // the other points go to the work list in sorted order, so that the
+    // lanes of a wave count neighbours of nearby points (similar scans)
+    for (int32_t p0 = tid - lane; p0 < n; p0 += kThreads) {
+        const int32_t p = p0 + lane;
+        wave_append(p < n && score[p] != kCore, (uint16_t)p, list, &s_nlist);
     }
     __syncthreads();
     // 4b. count the listed points' neighbours, nearest rows first, stopping
