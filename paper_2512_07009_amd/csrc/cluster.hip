@@ -216,11 +216,13 @@ struct Grid {
     bool dense_ok;       // side is the eps-diagonal side: same cell => neighbours
 };
 
-// floor(v / side) for 0 <= v < 2^16, via a float reciprocal and one correction.
+// floor(v / side) for 0 <= v < 2^16, via a float reciprocal and one
+// branch-free correction (the product is within one of the quotient, and
+// c * side stays below 2^24, so 24-bit multiplies are exact).
 __device__ __forceinline__ int32_t cell_coord(int32_t v, const Grid &g, int32_t ncoord) {
     int32_t c = (int32_t)((float)v * g.inv_side);
-    if (c * g.side > v) --c;
-    else if ((c + 1) * g.side <= v) ++c;
+    const int32_t cs = __mul24(c, g.side);
+    c += (int32_t)(cs + g.side <= v) - (int32_t)(cs > v);
     return min(max(c, 0), ncoord - 1);
 }
 
@@ -249,8 +251,8 @@ __device__ __forceinline__ int32_t count_span(const uint32_t *pxy, int32_t q0, i
 // correction step.
 __device__ __forceinline__ int32_t div_small(int32_t x, int32_t d, float inv_d) {
     int32_t q = (int32_t)((float)x * inv_d);
-    if (q * d > x) --q;
-    else if ((q + 1) * d <= x) ++q;
+    const int32_t qd = __mul24(q, d);  // below 2^23: exact
+    q += (int32_t)(qd + d <= x) - (int32_t)(qd > x);
     return q;
 }
 
@@ -962,51 +964,58 @@ __device__ __forceinline__ void cluster_resident(const ClusterArgs &a) {
         build_stencil(g.reach, g.side, r, lane, s_dxmax, s_sdx, s_sdy, &s_nsten, s_fdx, s_fdy, &s_nadj, &s_nfwd);
     }
     __syncthreads();
-    uint32_t pv[PTS];
-    uint16_t prank[PTS];
+    // each point's cell (below 2^16: the table fits LDS) and rank in it,
+    // packed as cell << 16 | rank
+    uint32_t pv[PTS], pcr[PTS];
 #pragma unroll
     for (int k = 0; k < PTS; ++k) {
         if (tid + k * kThreads >= n) break;
         pv[k] = (uint32_t)(pt[k].x - x0) | ((uint32_t)(pt[k].y - y0) << 16);
         int32_t cx, cy;
-        prank[k] = (uint16_t)atomicAdd(&cell[cell_id(pv[k], g, &cx, &cy)], 1u);  // rank in cell
+        const int32_t c = cell_id(pv[k], g, &cx, &cy);
+        pcr[k] = ((uint32_t)c << 16) | atomicAdd(&cell[c], 1u);
     }
     __syncthreads();
     {
+        // one scan of two counts per cell, packed (each total is below
+        // 2^16): its points (low half) and, unless it is a dense cell, its
+        // points again (high half), which go to the work list; the list's
+        // offset of each cell waits in clist, unused until step 5
         const int32_t chunk = (g.ncell + kThreads - 1) / kThreads;
         const int32_t c0 = min(tid * chunk, g.ncell);
         const int32_t c1 = min(c0 + chunk, g.ncell);
+        auto both = [&](int v) { return v | (g.dense_ok && v >= a.min_pts ? 0 : v << 16); };
         int sum = 0;
-        for (int32_t c = c0; c < c1; ++c) sum += (int)cell[c];
+        for (int32_t c = c0; c < c1; ++c) sum += both((int)cell[c]);
         int run = block_exclusive_scan(sum, s_wave);
         for (int32_t c = c0; c < c1; ++c) {
             const int v = (int)cell[c];
-            cell[c] = (uint32_t)run | 0xffff0000u;
-            run += v;
+            cell[c] = (uint32_t)(run & 0xffff) | 0xffff0000u;
+            clist[c] = (uint16_t)(run >> 16);
+            run += both(v);
         }
-        if (tid == kThreads - 1) cell[g.ncell] = (uint32_t)run | 0xffff0000u;
+        if (tid == kThreads - 1) {
+            cell[g.ncell] = (uint32_t)(run & 0xffff) | 0xffff0000u;
+            s_nlist = run >> 16;
+        }
     }
     __syncthreads();
     // scatter into sorted order; 4a. on the way, a cell holding >= min_pts
-    // points is all core
+    // points is all core, and the other points go to the work list, in
+    // sorted order too (so that the lanes of a wave count neighbours of
+    // nearby points, with similar scans)
 #pragma unroll
     for (int k = 0; k < PTS; ++k) {
         const int32_t i = tid + k * kThreads;
         if (i >= n) break;
-        int32_t cx, cy;
-        const int32_t c = cell_id(pv[k], g, &cx, &cy);
+        const int32_t c = (int32_t)(pcr[k] >> 16), rank = (int32_t)(pcr[k] & 0xffffu);
         const int32_t c0 = cstart(c);
-        const int32_t pos = c0 + prank[k];
+        const int32_t pos = c0 + rank;
         pxy[pos] = pv[k];
         sid[pos] = (uint16_t)i;
-        score[pos] = g.dense_ok && cstart(c + 1) - c0 >= a.min_pts ? kCore : 0;
-    }
-    __syncthreads();
-    // the other points go to the work list in sorted order, so that the
-    // lanes of a wave count neighbours of nearby points (similar scans)
-    for (int32_t p0 = tid - lane; p0 < n; p0 += kThreads) {
-        const int32_t p = p0 + lane;
-        wave_append(p < n && score[p] != kCore, (uint16_t)p, list, &s_nlist);
+        const bool dense = g.dense_ok && cstart(c + 1) - c0 >= a.min_pts;
+        score[pos] = dense ? kCore : 0;
+        if (!dense) list[clist[c] + rank] = (uint16_t)pos;
     }
     __syncthreads();
     // 4b. count the listed points' neighbours, nearest rows first, stopping
