@@ -268,6 +268,26 @@ def test_single_large_frame_gpu():
     assert_cluster_equal(got, xy, short, 160, 5, tag="frame shorter than total")
 
 
+def test_large_frame_one_component_gpu():
+    """Frames above the on-chip capacity whose cores form one component
+    spanning the whole frame (a jittered lattice, every cell of the grid
+    holding cores): many concurrent hooks meet in one tree of the global
+    forest, and the farther cell pairs all find their cells joined.  Beside
+    them, one frame of many small components (a sparse lattice of tight
+    groups)."""
+    rng = np.random.default_rng(33)
+    g = np.stack(np.meshgrid(np.arange(150), np.arange(100)), -1).reshape(-1, 2) * 96
+    one = (g + rng.integers(0, 48, g.shape)).astype(np.int32)           # 15000 points, spacing 6 px
+    c = np.stack(np.meshgrid(np.arange(40), np.arange(30)), -1).reshape(-1, 2) * 16 * 40
+    groups = (np.repeat(c, 10, 0) + rng.integers(0, 16 * 6, (c.shape[0] * 10, 2))).astype(np.int32)  # 12000
+    xy, off = wl.pack([one, groups])
+    for eps_q, min_pts in ((160, 4), (200, 6)):
+        got = run_cluster(xy, off, eps_q, min_pts, max_fp=0)
+        assert_cluster_equal(got, xy, off, eps_q, min_pts, tag=f"one component eps {eps_q}")
+        ncl = got[2]
+        assert ncl[0] == 1, ncl
+
+
 def test_bad_offsets_do_not_fault_gpu():
     xy = np.zeros((10, 2), np.int32)
     off = np.array([0, 5, 3, 10, 12], np.int32)   # frame 1 negative, frame 3 past total
