@@ -27,10 +27,10 @@
 // grid; the cell clearing there or, for a few frames, in extra workgroups
 // beside it), hist (cell counts and ranks), scan (one workgroup per frame),
 // scatter, core (neighbour counts with early exit, and each cell's smallest
-// core index), union of adjacent cell pairs, union of the farther cell pairs
-// (and point pairs where the grid was coarsened), labels (cores: their
-// tree's root and the cluster counts; other points: the root of the nearest
-// core's tree).  A batch of one large frame skips the on-chip kernel, and
+// core index), union of adjacent cell pairs (blocks of cells joined in LDS
+// first), union of the farther cell pairs (and point pairs where the grid
+// was coarsened), labels (cores: their tree's root and the cluster counts;
+// other points: the root of the nearest core's tree).  A batch of one large frame skips the on-chip kernel, and
 // prep then writes the counts of an empty or inconsistent frame.
 
 #include <algorithm>
@@ -498,66 +498,19 @@ __device__ void union_points_one(const ClusterArgs &a, const BigWs &w, int32_t p
     }
 }
 
-// Cell-pair unions for frames with the eps-diagonal grid: the cores of a
-// cell are one node (its smallest core index).  Two launches: the adjacent
-// cells (far = 0), then the farther ones (far = 1), whose pairs mostly join
-// nodes that the first launch has already connected and skip their tests.
-// The far launch also runs the point unions of coarsened frames.
-__global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w, int64_t n_items, int far) {
-    const int64_t item = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (far && item < a.total) union_points_one(a, w, (int32_t)item);  // n_items >= total
-    if (item >= n_items) return;
-    const int per = far ? kMaxForward : kAdjacent;
-    const int64_t c = item / per;
-    const int k = (int)(item - c * per);
-    const int f = frame_of_cell(a.offsets, a.n_frames, c);
-    const int32_t *rec = w.rec + (size_t)f * kRec;
-    if (!rec[kBig] || !rec[kDense]) return;
-    const BigGrid g = load_grid(rec);
-    const int64_t base = cell_base(a.offsets, f);
-    const int32_t ca = (int32_t)(c - base);
-    if (ca >= g.ncell) return;
-    int odx, ody;
-    if (!far) {
-        // the forward adjacent cells (1, 0), (-1, 1), (0, 1), (1, 1)
-        odx = k == 0 ? 1 : k - 2;
-        ody = k == 0 ? 0 : 1;
-    } else {
-        if (!forward_offset(g, k, &odx, &ody)) return;
-        if (odx >= -1 && odx <= 1 && ody <= 1) return;  // an adjacent pair: the first launch's
-    }
-    const int32_t ay = ca / g.ncx, ax = ca - ay * g.ncx;
-    const int32_t bx = ax + odx, by = ay + ody;
-    if (bx < 0 || bx >= g.ncx || by >= g.ncy) return;
-    const int32_t cb = by * g.ncx + bx;
-    const int32_t na = w.cnode[base + ca], nb = w.cnode[base + cb];  // both loads in flight
-    if ((na == INT_MAX) | (nb == INT_MAX)) return;
-    const int32_t b = a.offsets[f];
-    int32_t *parent = a.labels + b;
-    // the farther pairs mostly join nodes already connected: skip those
-    // before the point tests (the adjacent pairs rarely are; their unite
-    // finds the roots anyway).  Cached walks: a common ancestor in a view
-    // that misses recent hooks is still a common ancestor.
-    if (far) {
-        int32_t ra = na, rb = nb;
-        roots_cached(parent, &ra, &rb);
-        if (ra == rb) return;
-    }
-    const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
-    const int32_t *cs = w.cstart + base;
-    const int32_t a0 = cs[ca], a1 = cs[ca + 1], b0 = cs[cb], b1 = cs[cb + 1];
-    const int2 *S = w.spos + b;
-    const uint8_t *core = w.score + b;
-    const int32_t rx0 = g.x0 + bx * g.side, rx1 = rx0 + g.side - 1;
-    const int32_t ry0 = g.y0 + by * g.side, ry1 = ry0 + g.side - 1;
+// True if some core of sorted points [a0, a1) lies within eps of some core
+// of [b0, b1), whose cell covers [rx0, rx1] x [ry0, ry1]: A's cores out of
+// reach of that rectangle are skipped, B is read four points per step (the
+// scan of a large pair is bound by the latency of these loads).
+__device__ __forceinline__ bool cores_touch(const int2 *S, const uint8_t *core, int32_t a0, int32_t a1, int32_t b0,
+                                            int32_t b1, int32_t rx0, int32_t rx1, int32_t ry0, int32_t ry1,
+                                            const Radius &r) {
     for (int32_t qa = a0; qa < a1; ++qa) {
         if (!core[qa]) continue;
         const int2 va = S[qa];
         const int32_t ddx = min(max(max(rx0 - va.x, va.x - rx1), 0), r.e1);
         const int32_t ddy = min(max(max(ry0 - va.y, va.y - ry1), 0), r.e1);
         if (__mul24(ddx, ddx) + __mul24(ddy, ddy) > r.e2) continue;
-        // four independent loads in flight per step: the scan of a large
-        // cell pair is bound by their latency, not by the tests
         int32_t qb = b0;
         bool hit = false;
         for (; qb + 4 <= b1 && !hit; qb += 4) {
@@ -567,11 +520,189 @@ __global__ __launch_bounds__(kBlock) void big_union_cells(ClusterArgs a, BigWs w
                   (c3 && within(va, s3, r));
         }
         for (; qb < b1 && !hit; ++qb) hit = core[qb] && within(va, S[qb], r);
-        if (hit) {
-            uf_unite_cached(parent, na, nb);
-            return;
-        }
+        if (hit) return true;
     }
+    return false;
+}
+
+// Adjacent cell-pair unions, tiled.  A workgroup takes blocks of kTileW x
+// kTileH cells of one frame; with their forward adjacent neighbours (one
+// more column each side, one more row below) they form its region.  It
+// tests the adjacent pairs of its cells (one per thread), joins them in a
+// forest over the region in LDS (synchronous hook-and-jump rounds), and
+// then hooks every region cell's node to the smallest node of its local
+// tree in the frame's global forest (uf_unite_cached), so that each
+// compare-and-swap meets the node's own root.  Every local edge is a true
+// edge and every adjacent pair is tested by the block owning its first
+// cell, so the global forest ends with the components of the adjacent
+// edges, with far fewer global hooks than one per edge.
+constexpr int kTileW = 16, kTileH = 8;
+constexpr int kTileCells = kTileW * kTileH;
+constexpr int kTileThreads = kTileCells * kAdjacent;   // one adjacent pair per thread
+constexpr int kRegW = kTileW + 2, kRegH = kTileH + 1, kRegionCells = kRegW * kRegH;
+
+// Workgroups of frame f in the tiled launch: [slot(f), slot(f + 1)), at
+// least one per frame (the + f), about one per kTileCells cell-table entries.
+__device__ __forceinline__ int64_t tile_slot(const int32_t *offsets, int f) {
+    return cell_base(offsets, f) / kTileCells + f;
+}
+
+__device__ __forceinline__ int frame_of_slot(const int32_t *offsets, int n_frames, int64_t wg) {
+    int lo = 0, hi = n_frames - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (tile_slot(offsets, mid) <= wg) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+__global__ __launch_bounds__(kTileThreads) void big_union_tiles(ClusterArgs a, BigWs w) {
+    __shared__ int32_t s_node[kRegionCells];  // node of each region cell; INT_MAX: no core, or off the grid
+    __shared__ int32_t s_par[kRegionCells];   // local forest over region cells
+    __shared__ int32_t s_min[kRegionCells];   // smallest node of each local tree (at its root)
+    __shared__ uint32_t s_edge[kTileCells];   // bit k: an edge to adjacent neighbour k
+    __shared__ int s_hook[3];
+    const int tid = threadIdx.x;
+    const int64_t wg = blockIdx.x;
+    const int f = frame_of_slot(a.offsets, a.n_frames, wg);
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig]) return;
+    const BigGrid g = load_grid(rec);
+    const int32_t b = a.offsets[f];
+    const int64_t s0 = tile_slot(a.offsets, f), nslots = tile_slot(a.offsets, f + 1) - s0;
+    if (wg >= s0 + nslots || !g.dense) return;  // past the last frame's slots; coarsened grids: far launch
+    if (tid == 0) s_hook[0] = 0;
+    const int64_t base = cell_base(a.offsets, f);
+    const int32_t *cs = w.cstart + base;
+    const int32_t *cn = w.cnode + base;
+    const int2 *S = w.spos + b;
+    const uint8_t *core = w.score + b;
+    int32_t *parent = a.labels + b;
+    const Radius r{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q};
+    const int tiles_x = (g.ncx + kTileW - 1) / kTileW, tiles_y = (g.ncy + kTileH - 1) / kTileH;
+    auto region = [](int ox, int oy) { return oy * kRegW + ox + 1; };
+    // adjacent neighbour k: (1, 0), (-1, 1), (0, 1), (1, 1)
+    auto adx = [](int k) { return k == 0 ? 1 : k - 2; };
+    auto ady = [](int k) { return k == 0 ? 0 : 1; };
+    auto root = [&](int i) {
+        while (s_par[i] != i) i = s_par[i];
+        return i;
+    };
+    // tests the pair (owned cell j, its adjacent neighbour k) and sets bit k on a hit
+    auto test = [&](int tx0, int ty0, int j, int k) {
+        const int ox = j % kTileW, oy = j / kTileW;
+        const int odx = adx(k), ody = ady(k);
+        const int ia = region(ox, oy), ib = region(ox + odx, oy + ody);
+        if ((s_node[ia] == INT_MAX) | (s_node[ib] == INT_MAX)) return;
+        const int32_t ax = tx0 + ox, ay = ty0 + oy, bx = ax + odx, by = ay + ody;
+        const int32_t ca = ay * g.ncx + ax, cb = by * g.ncx + bx;
+        const int32_t rx0 = g.x0 + bx * g.side, ry0 = g.y0 + by * g.side;
+        if (cores_touch(S, core, cs[ca], cs[ca + 1], cs[cb], cs[cb + 1], rx0, rx0 + g.side - 1, ry0,
+                        ry0 + g.side - 1, r))
+            atomicOr(&s_edge[j], 1u << k);
+    };
+    // hook-and-jump rounds over the block's edges (each round that hooks
+    // leaves fewer local roots, so the loop ends)
+    int round = 0;
+    auto rounds = [&]() {
+        for (int guard = 0; guard <= kRegionCells; ++guard, ++round) {
+            if (tid == 0) s_hook[(round + 1) % 3] = 0;
+            bool any = false;
+            if (tid < kTileCells && s_edge[tid]) {
+                const uint32_t m = s_edge[tid];
+                const int ox = tid % kTileW, oy = tid / kTileW;
+                const int32_t pa = s_par[region(ox, oy)];
+                int32_t pb[kAdjacent];
+                int32_t lo = pa;
+#pragma unroll
+                for (int k = 0; k < kAdjacent; ++k) {
+                    pb[k] = ((m >> k) & 1u) ? s_par[region(ox + adx(k), oy + ady(k))] : pa;
+                    lo = min(lo, pb[k]);
+                }
+                if (pa != lo) {
+                    atomicMin(&s_par[pa], lo);
+                    any = true;
+                }
+#pragma unroll
+                for (int k = 0; k < kAdjacent; ++k)
+                    if (pb[k] != lo) {
+                        atomicMin(&s_par[pb[k]], lo);
+                        any = true;
+                    }
+            }
+            if (any) s_hook[round % 3] = 1;
+            __syncthreads();
+            if (!s_hook[round % 3]) break;
+            for (int i = tid; i < kRegionCells; i += kTileThreads) s_par[i] = root(i);
+            __syncthreads();
+        }
+        ++round;
+    };
+    for (int64_t t = wg - s0; t < (int64_t)tiles_x * tiles_y; t += nslots) {
+        const int tx0 = (int)(t % tiles_x) * kTileW, ty0 = (int)(t / tiles_x) * kTileH;
+        for (int i = tid; i < kRegionCells; i += kTileThreads) {
+            const int32_t rx = tx0 - 1 + i % kRegW, ry = ty0 + i / kRegW;
+            s_node[i] = (rx >= 0 && rx < g.ncx && ry < g.ncy) ? cn[ry * g.ncx + rx] : INT_MAX;
+            s_par[i] = i;
+        }
+        if (tid < kTileCells) s_edge[tid] = 0;
+        __syncthreads();
+        test(tx0, ty0, tid / kAdjacent, tid % kAdjacent);
+        __syncthreads();
+        rounds();
+        // every node of a local tree is hooked to the tree's smallest node,
+        // so that each compare-and-swap meets the node's own root
+        for (int i = tid; i < kRegionCells; i += kTileThreads) s_min[i] = INT_MAX;
+        __syncthreads();
+        for (int i = tid; i < kRegionCells; i += kTileThreads)
+            if (s_node[i] != INT_MAX) atomicMin(&s_min[root(i)], s_node[i]);
+        __syncthreads();
+        for (int i = tid; i < kRegionCells; i += kTileThreads) {
+            const int32_t m = s_min[root(i)];
+            if (s_node[i] != INT_MAX && s_node[i] != m) uf_unite_cached(parent, s_node[i], m);
+        }
+        __syncthreads();  // the next block rewrites the region
+    }
+}
+
+// Farther cell-pair unions (forward offsets beyond the adjacent ones), one
+// item per (cell, offset), after the adjacent unions: most pairs find their
+// two nodes already joined (cached walks: a common ancestor in a stale view
+// is still one) and skip the point tests.  Also the point unions of frames
+// whose grid was coarsened.
+__global__ __launch_bounds__(kBlock) void big_union_far(ClusterArgs a, BigWs w, int64_t n_items) {
+    const int64_t item = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (item < a.total) union_points_one(a, w, (int32_t)item);  // n_items >= total
+    if (item >= n_items) return;
+    const int64_t c = item / kMaxForward;
+    const int k = (int)(item - c * kMaxForward);
+    const int f = frame_of_cell(a.offsets, a.n_frames, c);
+    const int32_t *rec = w.rec + (size_t)f * kRec;
+    if (!rec[kBig] || !rec[kDense]) return;
+    const BigGrid g = load_grid(rec);
+    const int64_t base = cell_base(a.offsets, f);
+    const int32_t ca = (int32_t)(c - base);
+    if (ca >= g.ncell) return;
+    int odx, ody;
+    if (!forward_offset(g, k, &odx, &ody)) return;
+    if (odx >= -1 && odx <= 1 && ody <= 1) return;  // adjacent: the tiled launch's
+    const int32_t ay = ca / g.ncx, ax = ca - ay * g.ncx;
+    const int32_t bx = ax + odx, by = ay + ody;
+    if (bx < 0 || bx >= g.ncx || by >= g.ncy) return;
+    const int32_t cb = by * g.ncx + bx;
+    int32_t na = w.cnode[base + ca], nb = w.cnode[base + cb];  // both loads in flight
+    if ((na == INT_MAX) | (nb == INT_MAX)) return;
+    const int32_t b = a.offsets[f];
+    int32_t *parent = a.labels + b;
+    int32_t ra = na, rb = nb;
+    roots_cached(parent, &ra, &rb);
+    if (ra == rb) return;
+    const int32_t *cs = w.cstart + base;
+    const int32_t rx0 = g.x0 + bx * g.side, ry0 = g.y0 + by * g.side;
+    if (cores_touch(w.spos + b, w.score + b, cs[ca], cs[ca + 1], cs[cb], cs[cb + 1], rx0, rx0 + g.side - 1, ry0,
+                    ry0 + g.side - 1, Radius{a.eps_q, a.eps_q + 1, a.eps_q * a.eps_q}))
+        uf_unite_cached(parent, na, nb);
 }
 
 // Labels, one thread per sorted point, after the unions have ended: a core
@@ -675,9 +806,10 @@ hipError_t launch_cluster_big(const ClusterArgs &a, void *workspace, hipStream_t
         hipLaunchKernelGGL(big_scan, dim3(a.n_frames), dim3(kScanThreads), 0, stream, a, w);
         hipLaunchKernelGGL(big_scatter, dim3(pts), dim3(kBlock), 0, stream, a, w);
         hipLaunchKernelGGL(big_core, dim3(pts), dim3(kBlock), 0, stream, a, w);
-        const int64_t adj = cells * kAdjacent, items = cells * kMaxForward;
-        hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(adj)), dim3(kBlock), 0, stream, a, w, adj, 0);
-        hipLaunchKernelGGL(big_union_cells, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items, 1);
+        // one more slot per frame than the cell table's blocks (tile_slot)
+        const int64_t slots = cells / kTileCells + a.n_frames, items = cells * kMaxForward;
+        hipLaunchKernelGGL(big_union_tiles, dim3((unsigned)slots), dim3(kTileThreads), 0, stream, a, w);
+        hipLaunchKernelGGL(big_union_far, dim3(blocks_for(items)), dim3(kBlock), 0, stream, a, w, items);
         hipLaunchKernelGGL(big_label, dim3(pts), dim3(kBlock), 0, stream, a, w);
     }
     return hipGetLastError();
