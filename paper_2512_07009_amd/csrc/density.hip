@@ -600,8 +600,16 @@ __global__ __launch_bounds__(256) void density_reduce_kernel(float *density, con
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
         const int64_t f = i / cells, c = i - f * cells;
         const float *src = partial + f * split * cells + c;
+        // slices in order, eight loads in flight at a time (a missing slice
+        // adds +0, which leaves the non-negative sum unchanged)
         float s = 0.0f;
-        for (int k = 0; k < split; ++k) s += src[k * cells];
+        for (int k0 = 0; k0 < split; k0 += 8) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = k0 + u < split ? src[(int64_t)(k0 + u) * cells] : 0.0f;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
         density[i] = s * scale;
     }
 }
