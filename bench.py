@@ -49,13 +49,16 @@ METRIC = "frames/sec (cluster+density) at 2000 birds/frame"
 HBM_PEAK_GBS = 8000.0
 MFMA_F16_PEAK_TFLOPS = 2500.0
 
+# the sources each entry point's kernels are built from (a counter summary
+# holds for the traffic of the current kernels only if all of them match)
 KERNEL_SOURCES = {
-    "cluster": "paper_2512_07009_amd/csrc/cluster.hip",
-    "density": "paper_2512_07009_amd/csrc/density.hip",
-    "heatmap": "paper_2512_07009_amd/csrc/heatmap.hip",
-    "roi": "paper_2512_07009_amd/csrc/roi.hip",
-    "drinker": "paper_2512_07009_amd/csrc/roi.hip",
-    "mask": "paper_2512_07009_amd/csrc/mask.hip",
+    "cluster": ["paper_2512_07009_amd/csrc/cluster.hip", "paper_2512_07009_amd/csrc/cluster_big.hip",
+                "paper_2512_07009_amd/csrc/cluster_common.h"],
+    "density": ["paper_2512_07009_amd/csrc/density.hip"],
+    "heatmap": ["paper_2512_07009_amd/csrc/heatmap.hip", "paper_2512_07009_amd/csrc/cluster_common.h"],
+    "roi": ["paper_2512_07009_amd/csrc/roi.hip"],
+    "drinker": ["paper_2512_07009_amd/csrc/roi.hip"],
+    "mask": ["paper_2512_07009_amd/csrc/mask.hip", "paper_2512_07009_amd/csrc/cluster_common.h"],
 }
 
 
@@ -63,9 +66,13 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def source_hash(rel: str) -> str:
-    with open(os.path.join(ROOT, rel), "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()[:16]
+def source_hash(rels) -> str:
+    """sha256[:16] of the named source files, concatenated in order."""
+    h = hashlib.sha256()
+    for rel in rels:
+        with open(os.path.join(ROOT, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def committed_traffic(kernel: str, workload: str):
