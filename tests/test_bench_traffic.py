@@ -1,0 +1,46 @@
+"""bench.py reports a kernel's HBM traffic from a committed counter summary
+only while that summary was taken from the current sources: every file the
+entry point's kernels are built from must match the recorded hash."""
+import os
+
+import bench
+
+
+def _setup(tmp_path, monkeypatch, sources):
+    for rel, text in sources.items():
+        path = tmp_path / rel
+        path.parent.mkdir(parents=True, exist_ok=True)
+        path.write_text(text)
+    (tmp_path / "profiles").mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "KERNEL_SOURCES", {"cluster": list(sources)})
+
+
+def _write_summary(tmp_path, digest, nbytes=12345):
+    (tmp_path / "profiles" / "cluster_w_counters.md").write_text(
+        f"HBM bytes per launch (scaled): {nbytes}\n\nsource sha256[:16]: `{digest}` (files)\n")
+
+
+def test_traffic_needs_every_source_to_match(tmp_path, monkeypatch):
+    sources = {"a.hip": "kernel a", "b.hip": "kernel b", "c.h": "common"}
+    _setup(tmp_path, monkeypatch, sources)
+    digest = bench.source_hash(list(sources))
+    _write_summary(tmp_path, digest)
+    assert bench.committed_traffic("cluster", "w") == 12345.0
+    # a change in any one of the files voids the summary
+    (tmp_path / "b.hip").write_text("kernel b, changed")
+    assert bench.committed_traffic("cluster", "w") is None
+
+
+def test_traffic_absent_or_unhashed(tmp_path, monkeypatch):
+    _setup(tmp_path, monkeypatch, {"a.hip": "kernel a"})
+    assert bench.committed_traffic("cluster", "w") is None  # no summary
+    (tmp_path / "profiles" / "cluster_w_counters.md").write_text("HBM bytes per launch (scaled): 5\n")
+    assert bench.committed_traffic("cluster", "w") is None  # no hash line
+
+
+def test_source_hash_is_order_sensitive(tmp_path, monkeypatch):
+    _setup(tmp_path, monkeypatch, {"a.hip": "x", "b.hip": "y"})
+    assert bench.source_hash(["a.hip", "b.hip"]) != bench.source_hash(["b.hip", "a.hip"])
+    assert len(bench.source_hash(["a.hip"])) == 16
+    assert os.path.isabs(bench.ROOT)
