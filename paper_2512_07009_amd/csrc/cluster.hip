@@ -902,7 +902,8 @@ __device__ __forceinline__ void cluster_resident(const ClusterArgs &a) {
     //   sid    uint16[cap]   original index of each sorted position
     //   list   uint16[cap]   work list (then edge bits and queue, then the
     //                        border list, then kinds by original index)
-    //   clist  uint16[cc]    cells that hold a core
+    //   clist  uint16[cc]    each cell's offset in the work list (sort),
+    //                        then the cells that hold a core
     //   score  uint8 [cap]   kind by sorted position (kCore, kBorder,
     //                        kIsolated, 0 for noise)
     const int32_t cap = a.cap_points, cc = a.cap_cells;
