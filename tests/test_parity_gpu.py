@@ -288,6 +288,21 @@ def test_large_frame_one_component_gpu():
         assert ncl[0] == 1, ncl
 
 
+def test_large_frame_thin_grids_gpu():
+    """Frames above the on-chip capacity whose cell grids are thinner than
+    the 16 x 8-cell blocks of the tiled unions: one row of cells, three
+    columns of cells, and a grid whose width and height leave partial
+    blocks on both edges."""
+    rng = np.random.default_rng(44)
+    eps_q, min_pts = 200, 4  # cells of 141 quanta
+    row = np.stack([rng.integers(0, 2_000_000, 12000), rng.integers(0, 120, 12000)], 1).astype(np.int32)
+    col = np.stack([rng.integers(0, 400, 12000), rng.integers(0, 1_000_000, 12000)], 1).astype(np.int32)
+    odd = np.stack([rng.integers(0, 141 * 137, 12000), rng.integers(0, 141 * 73, 12000)], 1).astype(np.int32)
+    xy, off = wl.pack([row, col, odd])
+    got = run_cluster(xy, off, eps_q, min_pts, max_fp=0)
+    assert_cluster_equal(got, xy, off, eps_q, min_pts, tag="thin grids")
+
+
 def test_bad_offsets_do_not_fault_gpu():
     xy = np.zeros((10, 2), np.int32)
     off = np.array([0, 5, 3, 10, 12], np.int32)   # frame 1 negative, frame 3 past total
