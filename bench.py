@@ -309,7 +309,30 @@ def main():
         return (torch.equal(b["labels"], ref[0]) and torch.equal(b["kind"], ref[1]) and torch.equal(b["ncl"], ref[2])
                 and torch.equal(b["dens"], ref[3]))
 
-    def replay_wall(concurrent, bufs):
+    def capture_steps(grp, concurrent, joined, cap):
+        """The steps of one graph: one stream; or two streams joined after
+        every step; or two streams, the clustering launches of the steps in
+        order on one and the density launches on the other, joined once at
+        the graph's end (each step still runs both over its own batch copy;
+        a step's density launch may start before the previous step's
+        clustering has ended)."""
+        if concurrent and not joined:
+            fork = torch.cuda.Event()
+            fork.record(cap)
+            side.wait_event(fork)
+            for b in grp:
+                flock.cluster_frames(b["xy"], b["off"], w.eps_px, w.min_pts, max_fp,
+                                     out=(b["labels"], b["kind"], b["ncl"]), stream=cap)
+                flock.density_frames(b["xy"], b["off"], w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px,
+                                     max_fp, out=b["dens"], stream=side)
+            join = torch.cuda.Event()
+            join.record(side)
+            cap.wait_event(join)
+        else:
+            for k, b in enumerate(grp):
+                run_pair(k, concurrent, launch_stream=cap, buf=b)
+
+    def replay_wall(concurrent, bufs, joined=False):
         """Capture graphs of `gsteps` steps cycling over `bufs`, check one pass
         over every copy against the eager outputs, then time K steps."""
         cap = torch.cuda.Stream(dev)
@@ -319,16 +342,14 @@ def main():
         for grp in groups:
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g, stream=cap):
-                for k, b in enumerate(grp):
-                    run_pair(k, concurrent, launch_stream=cap, buf=b)
+                capture_steps(grp, concurrent, joined, cap)
             graphs.append(g)
         rem = None
         if K % gsteps:
             grp = groups[(K // gsteps) % len(groups)][:K % gsteps]
             rem = torch.cuda.CUDAGraph()
             with torch.cuda.graph(rem, stream=cap):
-                for k, b in enumerate(grp):
-                    run_pair(k, concurrent, launch_stream=cap, buf=b)
+                capture_steps(grp, concurrent, joined, cap)
         torch.cuda.synchronize(dev)
         for b in bufs:
             b["labels"].fill_(-7)
@@ -349,11 +370,14 @@ def main():
     graph_note = None
     modes = {"auto": (True, False), "1": (False,), "2": (True,)}[args.streams]
     walls, warm_walls = {}, {}
+    joined_wall = None
     if not args.no_graph:
         try:
             for concurrent in modes:
                 walls[concurrent] = replay_wall(concurrent, copies)
                 warm_walls[concurrent] = replay_wall(concurrent, [home]) if n_copies > 1 else walls[concurrent]
+            if True in modes:
+                joined_wall = replay_wall(True, copies, joined=True)
         except RuntimeError as ex:
             graph_note = f"graph replay unavailable ({ex}); value timed eagerly on one copy"
             log(graph_note)
@@ -528,13 +552,17 @@ def main():
         "warm_value": F / (warm_wall / K),
         "rotation": rotation,
         "two_stream_frames_per_s": F / (walls[True] / K) if True in walls else None,
+        "two_stream_joined_frames_per_s": F / (joined_wall / K) if joined_wall else None,
         "one_stream_frames_per_s": F / (walls[False] / K) if False in walls else None,
         "eager_two_stream_frames_per_s": F / (eager[True][0] / K) if True in eager else None,
         "eager_one_stream_frames_per_s": F / (eager[False][0] / K) if False in eager else None,
         "timing": graph_note or ("value: HIP graph replay of the faster of the two-stream and one-stream steps, "
                                  "step k on copy k mod rotation.copies of the batch (inputs and outputs), so its "
-                                 "data comes from HBM where the copies exceed the caches; warm_value: the same "
-                                 "replays on one copy; two/one_stream_frames_per_s: rotated, per mode; kernel "
+                                 "data comes from HBM where the copies exceed the caches; two streams: the "
+                                 "clustering launches of a graph's steps in order on one stream, the density "
+                                 "launches on the other, joined once per graph of up to 10 steps "
+                                 "(two_stream_joined_frames_per_s: joined after every step instead); warm_value: "
+                                 "the same replays on one copy; two/one_stream_frames_per_s: rotated, per mode; kernel "
                                  "durations (per_launch_us, roofline): HIP events around each launch in an eager "
                                  "one-stream run, each launch after a write of flush_mb MiB that evicts L2 and "
                                  "the memory-side cache (warm_per_launch_us: back to back; "
