@@ -72,6 +72,66 @@ def test_graph_replays_match_eager(case):
             assert torch.equal(got, want), f"{name}: replay {rep} {what} differs from eager"
 
 
+@pytest.mark.parametrize("case", range(2))
+def test_graph_pipelined_steps_match_eager(case):
+    """Several steps in one graph on two streams joined once at its end (the
+    clustering launches of the steps in order on one stream, the density
+    launches on the other), each step on its own copy of the batch; every
+    replay, with eager work in between, equals the eager outputs of every
+    copy bit for bit."""
+    name, xy, off, w, mfp = list(_batches())[case]
+    dev = torch.device("cuda")
+    F, T = len(off) - 1, xy.shape[0]
+    steps = 3
+    bufs = []
+    for k in range(steps):
+        bufs.append({"xy": torch.from_numpy(xy).to(dev), "off": torch.from_numpy(off).to(dev),
+                     "labels": torch.empty(T, dtype=torch.int32, device=dev),
+                     "kind": torch.empty(T, dtype=torch.uint8, device=dev),
+                     "ncl": torch.empty(F, dtype=torch.int32, device=dev),
+                     "dens": torch.empty((F, w.grid_h, w.grid_w), dtype=torch.float32, device=dev)})
+    outs = ("labels", "kind", "ncl", "dens")
+    main, side = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+    with torch.cuda.stream(main):
+        b = bufs[0]
+        flock.cluster_frames(b["xy"], b["off"], w.eps_px, w.min_pts, mfp, out=(b["labels"], b["kind"], b["ncl"]),
+                             stream=main)
+        flock.density_frames(b["xy"], b["off"], w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px, mfp,
+                             out=b["dens"], stream=main)
+    torch.cuda.synchronize()
+    ref = [bufs[0][o].clone() for o in outs]
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=main):
+        fork = torch.cuda.Event()
+        fork.record(main)
+        side.wait_event(fork)
+        for b in bufs:
+            flock.cluster_frames(b["xy"], b["off"], w.eps_px, w.min_pts, mfp,
+                                 out=(b["labels"], b["kind"], b["ncl"]), stream=main)
+            flock.density_frames(b["xy"], b["off"], w.width_px, w.height_px, w.grid_w, w.grid_h, w.sigma_px, mfp,
+                                 out=b["dens"], stream=side)
+        join = torch.cuda.Event()
+        join.record(side)
+        main.wait_event(join)
+    torch.cuda.synchronize()
+
+    other_xy, other_off = wl.random_batch(9, 5, 300)
+    oxy, ooff = torch.from_numpy(other_xy).to(dev), torch.from_numpy(other_off).to(dev)
+    for rep in range(4):
+        for b in bufs:
+            for o, v in zip(outs, (-7, 9, -3, -1.0)):
+                b[o].fill_(v)
+        flock.cluster_frames(oxy, ooff, 40.0, 4, 300)
+        flock.density_frames(oxy, ooff, 1920, 1080, 128, 72, 30.0, 300)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k, b in enumerate(bufs):
+            for o, want in zip(outs, ref):
+                assert torch.equal(b[o], want), f"{name}: replay {rep} step {k} {o} differs from eager"
+
+
 def test_graph_replays_match_eager_analytics():
     """heatmap_frames, roi_filter_frames, drinker_proximity_frames and
     mask_components_frames captured in one graph, replayed several times with
