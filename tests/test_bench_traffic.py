@@ -1,6 +1,7 @@
-"""bench.py reports a kernel's HBM traffic from a committed counter summary
-only while that summary was taken from the current sources: every file the
-entry point's kernels are built from must match the recorded hash."""
+"""bench.py on the CPU: it reports a kernel's HBM traffic from a committed
+counter summary only while that summary was taken from the current sources
+(every file the entry point's kernels are built from must match the
+recorded hash), and it refuses to measure more than one GPU."""
 import os
 
 import bench
@@ -44,3 +45,18 @@ def test_source_hash_is_order_sensitive(tmp_path, monkeypatch):
     assert bench.source_hash(["a.hip", "b.hip"]) != bench.source_hash(["b.hip", "a.hip"])
     assert len(bench.source_hash(["a.hip"])) == 16
     assert os.path.isabs(bench.ROOT)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: --gpus above 1 (or a multi-rank launch)
+    exits with status 2 and says why, before touching torch or the GPU."""
+    import subprocess
+    import sys
+    env = dict(os.environ, WORLD_SIZE="1")
+    r = subprocess.run([sys.executable, os.path.join(bench.ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, env=env, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr
+    env["WORLD_SIZE"] = "4"
+    r = subprocess.run([sys.executable, os.path.join(bench.ROOT, "bench.py")], capture_output=True, text=True,
+                       env=env, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr
