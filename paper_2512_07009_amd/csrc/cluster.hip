@@ -1017,6 +1017,9 @@ __device__ __forceinline__ void cluster_resident(const ClusterArgs &a) {
         const bool dense = g.dense_ok && cstart(c + 1) - c0 >= a.min_pts;
         score[pos] = dense ? kCore : 0;
         if (!dense) list[clist[c] + rank] = (uint16_t)pos;
+        // a dense cell's node (smallest core index): the start half of the
+        // word is the same on both sides, so the minimum acts on the node
+        else atomicMin(&cell[c], (uint32_t)c0 | ((uint32_t)i << 16));
     }
     __syncthreads();
     // 4b. count the listed points' neighbours, nearest rows first, stopping
@@ -1053,9 +1056,11 @@ __device__ __forceinline__ void cluster_resident(const ClusterArgs &a) {
     }
     __syncthreads();
 
-    // 5. kinds of cores, forest roots, and each cell's smallest core index
-    for (int32_t p = tid; p < n; p += kThreads) {
-        parent[p] = p;
+    // 5. forest roots, and the smallest core index of each cell whose cores
+    //    came from the counts (dense cells had theirs set in the scatter)
+    for (int32_t p = tid; p < n; p += kThreads) parent[p] = p;
+    for (int32_t j = tid; j < s_nlist; j += kThreads) {
+        const int32_t p = list[j];
         if (score[p] == kCore) {
             int32_t cx, cy;
             const int32_t c = cell_id(pxy[p], g, &cx, &cy);
